@@ -1,0 +1,400 @@
+"""Seeded synthetic workloads for the action-expert denoising loop.
+
+This module is shared by the tests, the benchmark and the oracle's callers.
+It holds shapes, seeds and storage formats only: none of the expert's
+arithmetic lives here.  Every tensor is drawn from its own counter-keyed
+PCG64 stream, so a single request's inputs can be regenerated without
+generating the whole batch.
+
+Storage formats produced here (what the library and the oracle consume):
+  * ``f32``  -- float32 values.
+  * ``bf16`` -- uint16 bit patterns, rounded to nearest-even from float32.
+  * ``fp8``  -- uint8 OCP e4m3fn codes plus one float32 scale per output
+               column (round-to-nearest weight quantisation, as in the
+               paper's offline RTN quantiser, Section "Optimization Methods",
+               paragraph "Quantization").
+
+Linear weights are stored ``[in][out]`` (``y = x @ W + b``).
+"""
+from __future__ import annotations
+
+import dataclasses
+import zlib
+from typing import Dict, Optional
+
+import numpy as np
+
+__all__ = [
+    "ExpertConfig", "CONFIGS", "StoredTensor", "weight_specs", "make_weights",
+    "make_prefix", "make_prefix_lengths", "make_noise", "make_state",
+    "default_timesteps", "make_case", "bf16_bits_from_f32", "e4m3fn_encode",
+    "quantize_fp8_per_column", "TRUNK_LINEARS",
+]
+
+
+@dataclasses.dataclass(frozen=True)
+class ExpertConfig:
+    """Shape and format of one expert workload.
+
+    variant: ``pi0`` (time mixed into action tokens by an MLP), ``pi05``
+    (adaRMSNorm time conditioning) or ``dit`` (DiT head with adaLN-zero,
+    alternating cross/self attention).
+    """
+    name: str
+    cfg_id: int
+    variant: str
+    n_layers: int
+    d_model: int
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    d_mlp: int
+    horizon: int
+    action_dim: int
+    n_steps: int
+    prefix_cap: int           # rows reserved per request in the prefix buffer
+    prefix_min: int           # ragged prefix lengths drawn uniform in [min, max]
+    prefix_max: int
+    batch: int
+    state_token: bool
+    rope: bool
+    weight_dtype: str         # f32 | bf16 | fp8
+    kv_dtype: str             # f32 | bf16
+    d_feat: int = 0           # DiT: width of the VLM feature tokens
+    time_dim: int = 0         # width of the sinusoidal timestep embedding
+    rms_eps: float = 1e-6
+    sin_min_period: float = 4e-3
+    sin_max_period: float = 4.0
+    rope_base: float = 10000.0
+    init_std: float = 0.02
+
+    @property
+    def tokens(self) -> int:
+        """Suffix tokens per request (state token, if any, plus actions)."""
+        return self.horizon + (1 if self.state_token else 0)
+
+    @property
+    def ragged(self) -> bool:
+        return self.prefix_min != self.prefix_max
+
+    @property
+    def prefix_width(self) -> int:
+        """Columns of one prefix row: n_kv*head_dim, or d_feat for DiT."""
+        return self.d_feat if self.variant == "dit" else self.n_kv_heads * self.head_dim
+
+    def replace(self, **kw) -> "ExpertConfig":
+        return dataclasses.replace(self, **kw)
+
+
+def _cfg(**kw) -> ExpertConfig:
+    kw.setdefault("time_dim", kw["d_model"])
+    return ExpertConfig(**kw)
+
+
+# The five workloads: a tiny fp32 expert, the pi0-shaped expert at batch 1,
+# the pi0.5-shaped expert (adaRMSNorm), a DiT-style action head, and the
+# pi0-shaped expert at rollout batch 64 with ragged prefixes and fp8 weights.
+CONFIGS: Dict[str, ExpertConfig] = {
+    "tiny_fp32": _cfg(
+        name="tiny_fp32", cfg_id=1, variant="pi0", n_layers=2, d_model=256,
+        n_q_heads=4, n_kv_heads=1, head_dim=64, d_mlp=1024, horizon=16,
+        action_dim=7, n_steps=4, prefix_cap=64, prefix_min=64, prefix_max=64,
+        batch=1, state_token=False, rope=False, weight_dtype="f32", kv_dtype="f32"),
+    "pi0_bf16_b1": _cfg(
+        name="pi0_bf16_b1", cfg_id=2, variant="pi0", n_layers=18, d_model=1024,
+        n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=4096, horizon=50,
+        action_dim=32, n_steps=10, prefix_cap=816, prefix_min=816, prefix_max=816,
+        batch=1, state_token=True, rope=True, weight_dtype="bf16", kv_dtype="bf16"),
+    "pi05_bf16_b1": _cfg(
+        name="pi05_bf16_b1", cfg_id=3, variant="pi05", n_layers=18, d_model=1024,
+        n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=4096, horizon=50,
+        action_dim=32, n_steps=10, prefix_cap=968, prefix_min=968, prefix_max=968,
+        batch=1, state_token=False, rope=True, weight_dtype="bf16", kv_dtype="bf16"),
+    "dit_bf16_b1": _cfg(
+        name="dit_bf16_b1", cfg_id=4, variant="dit", n_layers=16, d_model=1536,
+        n_q_heads=12, n_kv_heads=12, head_dim=128, d_mlp=6144, horizon=16,
+        action_dim=32, n_steps=4, prefix_cap=300, prefix_min=300, prefix_max=300,
+        batch=1, state_token=True, rope=False, weight_dtype="bf16", kv_dtype="bf16",
+        d_feat=2048, time_dim=256),
+    "pi0_fp8_b64": _cfg(
+        name="pi0_fp8_b64", cfg_id=5, variant="pi0", n_layers=18, d_model=1024,
+        n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=4096, horizon=50,
+        action_dim=32, n_steps=10, prefix_cap=1000, prefix_min=600, prefix_max=1000,
+        batch=64, state_token=True, rope=True, weight_dtype="fp8", kv_dtype="bf16"),
+}
+
+# Per-layer linears that carry the fp8 format when weight_dtype == "fp8".
+TRUNK_LINEARS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
+
+
+@dataclasses.dataclass
+class StoredTensor:
+    dtype: str                 # f32 | bf16 | fp8
+    data: np.ndarray           # float32 | uint16 | uint8, shape [rows][cols]
+    scale: Optional[np.ndarray] = None   # fp8: float32 [cols]
+
+    @property
+    def rows(self) -> int:
+        return int(self.data.shape[0])
+
+    @property
+    def cols(self) -> int:
+        return int(self.data.shape[1])
+
+
+# ----------------------------------------------------------------------------
+# Storage-format conversions (input preparation, pinned against torch's casts)
+# ----------------------------------------------------------------------------
+
+def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
+    """Round float32 to bfloat16 (nearest, ties to even); return uint16 bits."""
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    rounded = u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))
+    out = (rounded >> np.uint32(16)).astype(np.uint16)
+    nan = np.isnan(x)
+    if nan.any():
+        out[nan] = np.uint16(0x7FC0)
+    return out
+
+
+def e4m3fn_encode(v: np.ndarray) -> np.ndarray:
+    """Encode float values as OCP e4m3fn codes: saturate to +-448, then round
+    to nearest with ties to even.  (No NaN/inf inputs.)"""
+    v = np.asarray(v, dtype=np.float64)
+    sign = np.signbit(v)
+    a = np.minimum(np.abs(v), 448.0)
+    # Exponent of the binade; subnormals share the quantum of the lowest binade.
+    with np.errstate(divide="ignore"):
+        e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
+    e = np.clip(e, -6, 8)
+    q = np.exp2(e - 3)                         # spacing of representable values
+    n = np.round(a / q)                        # numpy rounds half to even
+    val = np.minimum(n * q, 448.0)
+    # value -> code
+    code = np.zeros(v.shape, dtype=np.int64)
+    sub = val < 2.0 ** -6
+    code[sub] = np.round(val[sub] / 2.0 ** -9).astype(np.int64)
+    nrm = ~sub
+    en = np.floor(np.log2(val[nrm]))
+    mant = np.round((val[nrm] / np.exp2(en) - 1.0) * 8.0).astype(np.int64)
+    code[nrm] = ((en.astype(np.int64) + 7) << 3) | mant
+    code = code | (sign.astype(np.int64) << 7)
+    return code.astype(np.uint8)
+
+
+def quantize_fp8_per_column(w: np.ndarray):
+    """Round-to-nearest fp8 weight quantisation with one scale per output column.
+
+    scale_j = max_i |W_ij| / 448 (1 for an all-zero column); codes encode
+    W_ij / scale_j.  Returns (codes uint8 [rows][cols], scales float32 [cols]).
+    """
+    w = np.asarray(w, dtype=np.float32)
+    amax = np.abs(w).max(axis=0).astype(np.float32)
+    scale = np.where(amax > 0, amax / np.float32(448.0), np.float32(1.0)).astype(np.float32)
+    codes = e4m3fn_encode(w.astype(np.float64) / scale.astype(np.float64)[None, :])
+    return codes, scale
+
+
+# ----------------------------------------------------------------------------
+# Parameter inventory
+# ----------------------------------------------------------------------------
+
+def weight_specs(cfg: ExpertConfig) -> Dict[str, tuple]:
+    """Name -> (rows, cols) of every parameter, in a fixed order.
+
+    Vectors (biases, norm weights) are stored as one row.
+    """
+    d, A, F = cfg.d_model, cfg.action_dim, cfg.d_mlp
+    qd = cfg.n_q_heads * cfg.head_dim
+    kd = cfg.n_kv_heads * cfg.head_dim
+    s: Dict[str, tuple] = {}
+    s["in_w"] = (A, d)
+    s["in_b"] = (1, d)
+    if cfg.variant == "pi0":
+        s["time_w1"] = (d + cfg.time_dim, d)
+        s["time_b1"] = (1, d)
+        s["time_w2"] = (d, d)
+        s["time_b2"] = (1, d)
+    else:
+        s["cond_w1"] = (cfg.time_dim, d)
+        s["cond_b1"] = (1, d)
+        s["cond_w2"] = (d, d)
+        s["cond_b2"] = (1, d)
+    if cfg.state_token:
+        s["state_w"] = (A, d)
+        s["state_b"] = (1, d)
+    if cfg.variant == "dit":
+        s["pos_emb"] = (cfg.horizon, d)
+    for l in range(cfg.n_layers):
+        p = f"layers.{l}."
+        if cfg.variant == "pi0":
+            s[p + "attn_norm"] = (1, d)
+        elif cfg.variant == "pi05":
+            s[p + "attn_mod_w"] = (d, 2 * d)
+            s[p + "attn_mod_b"] = (1, 2 * d)
+        else:
+            s[p + "ada_w"] = (d, 6 * d)
+            s[p + "ada_b"] = (1, 6 * d)
+        s[p + "wq"] = (d, qd)
+        kin = cfg.d_feat if (cfg.variant == "dit" and l % 2 == 0) else d
+        s[p + "wk"] = (kin, kd)
+        s[p + "wv"] = (kin, kd)
+        s[p + "wo"] = (qd, d)
+        if cfg.variant == "pi0":
+            s[p + "mlp_norm"] = (1, d)
+        elif cfg.variant == "pi05":
+            s[p + "mlp_mod_w"] = (d, 2 * d)
+            s[p + "mlp_mod_b"] = (1, 2 * d)
+        if cfg.variant == "dit":
+            s[p + "mlp_w1"] = (d, F)
+            s[p + "mlp_b1"] = (1, F)
+            s[p + "mlp_w2"] = (F, d)
+            s[p + "mlp_b2"] = (1, d)
+        else:
+            s[p + "w_gate"] = (d, F)
+            s[p + "w_up"] = (d, F)
+            s[p + "w_down"] = (F, d)
+    if cfg.variant == "pi0":
+        s["final_norm"] = (1, d)
+    elif cfg.variant == "pi05":
+        s["final_mod_w"] = (d, 2 * d)
+        s["final_mod_b"] = (1, 2 * d)
+    else:
+        s["final_ada_w"] = (d, 2 * d)
+        s["final_ada_b"] = (1, 2 * d)
+    s["out_w"] = (d, A)
+    s["out_b"] = (1, A)
+    return s
+
+
+def storage_dtype(cfg: ExpertConfig, name: str) -> str:
+    if cfg.weight_dtype == "fp8":
+        leaf = name.rsplit(".", 1)[-1]
+        return "fp8" if (name.startswith("layers.") and leaf in TRUNK_LINEARS) else "bf16"
+    return cfg.weight_dtype
+
+
+def _rng(*key: int) -> np.random.Generator:
+    return np.random.Generator(np.random.PCG64(np.random.SeedSequence(list(key))))
+
+
+def _store(x: np.ndarray, dtype: str) -> StoredTensor:
+    if dtype == "f32":
+        return StoredTensor("f32", np.ascontiguousarray(x, dtype=np.float32))
+    if dtype == "bf16":
+        return StoredTensor("bf16", bf16_bits_from_f32(x))
+    codes, scale = quantize_fp8_per_column(x)
+    return StoredTensor("fp8", codes, scale)
+
+
+def make_weights(cfg: ExpertConfig, seed: int = 0,
+                 overrides: Optional[Dict[str, np.ndarray]] = None) -> Dict[str, StoredTensor]:
+    """Every parameter ~ N(0, init_std) in float32, then stored in the config's
+    format.  ``overrides`` replaces named float32 masters before storage (used
+    by tests that zero or plant specific weights)."""
+    out: Dict[str, StoredTensor] = {}
+    overrides = overrides or {}
+    for name, (r, c) in weight_specs(cfg).items():
+        if name in overrides:
+            x = np.asarray(overrides[name], dtype=np.float32).reshape(r, c)
+        else:
+            g = _rng(seed, cfg.cfg_id, 0, zlib.crc32(name.encode()))
+            x = g.standard_normal((r, c), dtype=np.float32) * np.float32(cfg.init_std)
+        out[name] = _store(x, storage_dtype(cfg, name))
+    return out
+
+
+def make_prefix_lengths(cfg: ExpertConfig, seed: int = 0, batch: Optional[int] = None) -> np.ndarray:
+    B = cfg.batch if batch is None else batch
+    if not cfg.ragged:
+        return np.full(B, cfg.prefix_max, dtype=np.int32)
+    g = _rng(seed, cfg.cfg_id, 5)
+    return g.integers(cfg.prefix_min, cfg.prefix_max + 1, size=B).astype(np.int32)
+
+
+def _prefix_block(cfg, seed, l, kv, b, n):
+    g = _rng(seed, cfg.cfg_id, 1, l, kv, b)
+    return g.standard_normal((n, cfg.prefix_width), dtype=np.float32)
+
+
+def make_prefix(cfg: ExpertConfig, prefix_len: np.ndarray, seed: int = 0,
+                requests=None, pad_value: float = 0.0) -> np.ndarray:
+    """Prefix buffer for the requests listed (default: all).
+
+    pi0/pi0.5: the frozen prefix K/V cache, layout [L][2][B][P_cap][n_kv*d_h].
+    DiT: the VLM feature tokens, layout [B][P_cap][d_feat].
+    Valid rows ~ N(0, 1); rows at or beyond prefix_len[b] hold ``pad_value``.
+    Returns uint16 bf16 bits or float32 according to kv_dtype.
+    """
+    reqs = list(range(len(prefix_len))) if requests is None else list(requests)
+    P, W = cfg.prefix_cap, cfg.prefix_width
+    bf = cfg.kv_dtype == "bf16"
+    dt = np.uint16 if bf else np.float32
+    if cfg.variant == "dit":
+        buf = np.empty((len(reqs), P, W), dtype=dt)
+    else:
+        buf = np.empty((cfg.n_layers, 2, len(reqs), P, W), dtype=dt)
+    pad = bf16_bits_from_f32(np.float32([pad_value]))[0] if bf else np.float32(pad_value)
+    for i, b in enumerate(reqs):
+        n = int(prefix_len[b])
+        if cfg.variant == "dit":
+            blk = _prefix_block(cfg, seed, 0, 0, b, n)
+            buf[i, :n] = bf16_bits_from_f32(blk) if bf else blk
+            buf[i, n:] = pad
+        else:
+            for l in range(cfg.n_layers):
+                for kv in range(2):
+                    blk = _prefix_block(cfg, seed, l, kv, b, n)
+                    buf[l, kv, i, :n] = bf16_bits_from_f32(blk) if bf else blk
+                    buf[l, kv, i, n:] = pad
+    return buf
+
+
+def make_noise(cfg: ExpertConfig, seed: int = 0, requests=None, batch=None) -> np.ndarray:
+    B = cfg.batch if batch is None else batch
+    reqs = list(range(B)) if requests is None else list(requests)
+    out = np.empty((len(reqs), cfg.horizon, cfg.action_dim), dtype=np.float32)
+    for i, b in enumerate(reqs):
+        out[i] = _rng(seed, cfg.cfg_id, 3, b).standard_normal(
+            (cfg.horizon, cfg.action_dim), dtype=np.float32)
+    return out
+
+
+def make_state(cfg: ExpertConfig, seed: int = 0, requests=None, batch=None) -> Optional[np.ndarray]:
+    if not cfg.state_token:
+        return None
+    B = cfg.batch if batch is None else batch
+    reqs = list(range(B)) if requests is None else list(requests)
+    out = np.empty((len(reqs), cfg.action_dim), dtype=np.float32)
+    for i, b in enumerate(reqs):
+        out[i] = _rng(seed, cfg.cfg_id, 4, b).standard_normal(cfg.action_dim, dtype=np.float32)
+    return out
+
+
+def default_timesteps(n_steps: int) -> np.ndarray:
+    """Uniform schedule t_k = 1 - k/K, k = 0..K (from noise at t=1 to t=0)."""
+    return (1.0 - np.arange(n_steps + 1, dtype=np.float64) / n_steps).astype(np.float32)
+
+
+@dataclasses.dataclass
+class Case:
+    cfg: ExpertConfig
+    weights: Dict[str, StoredTensor]
+    prefix: np.ndarray
+    prefix_len: np.ndarray
+    noise: np.ndarray
+    state: Optional[np.ndarray]
+    timesteps: np.ndarray
+
+
+def make_case(cfg: ExpertConfig, seed: int = 0, batch: Optional[int] = None,
+              weights: Optional[Dict[str, StoredTensor]] = None) -> Case:
+    B = cfg.batch if batch is None else batch
+    plen = make_prefix_lengths(cfg, seed, B)
+    return Case(cfg=cfg,
+                weights=weights if weights is not None else make_weights(cfg, seed),
+                prefix=make_prefix(cfg, plen, seed),
+                prefix_len=plen,
+                noise=make_noise(cfg, seed, batch=B),
+                state=make_state(cfg, seed, batch=B),
+                timesteps=default_timesteps(cfg.n_steps))
