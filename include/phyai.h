@@ -1,0 +1,181 @@
+/*
+ * phyai.h -- C ABI of the MI355X (gfx950) action-expert denoising library.
+ *
+ * The library runs the flow-matching action-expert loop of a pi0-style
+ * vision-language-action policy (PhyAI, arXiv 2608.03682): a request's
+ * action chunk x (H actions of A values) starts as noise and is refined by K
+ * Euler steps, x <- x + (t_{k+1} - t_k) * v(x, t_k), where v is an L-layer
+ * transformer over the action tokens that attends to a frozen prefix K/V
+ * cache from the vision-language model (Section "Embodied Task Formulation",
+ * "From Observation to Action"; Section "PhyAI Architecture", paragraphs
+ * "Graph replay" and "Profiled operator selection").  The prefix state is
+ * valid for one chunk: it is read, never written, and stays fixed across
+ * the K steps.  Requests in a batch are independent (Section "Cloud
+ * Batching").
+ *
+ * Every step runs in hand-written HIP kernels; the K-step loop is captured
+ * in a HIP graph per (batch, steps) bucket and replayed.
+ *
+ * Conventions for every entry point:
+ *   - Pointers documented "device" must be device memory of the current HIP
+ *     device; "host" pointers are read before the call returns.
+ *   - Arguments are validated on the host before anything is enqueued; a
+ *     failing call enqueues nothing and leaves outputs untouched.
+ *   - Return value: PHYAI_OK or a negative phyai_status; the text of the last
+ *     error on the calling thread is returned by phyai_last_error().
+ *   - A handle is not thread-safe: at most one call in flight per handle.
+ *   - "stream" is a hipStream_t passed as void* (NULL = the null stream).
+ */
+#ifndef PHYAI_H
+#define PHYAI_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  PHYAI_OK = 0,
+  PHYAI_EINVAL = -1,        /* bad argument, shape or missing tensor       */
+  PHYAI_ENOMEM = -2,        /* device or host allocation failed            */
+  PHYAI_EHIP = -3,          /* a HIP runtime call failed                   */
+  PHYAI_EUNSUPPORTED = -4   /* valid but not implemented (shape, dtype)    */
+} phyai_status;
+
+typedef enum {
+  PHYAI_VARIANT_PI0 = 0,    /* time mixed into action tokens by a 2-layer MLP; optional state token */
+  PHYAI_VARIANT_PI05 = 1,   /* adaRMSNorm timestep conditioning in every norm                      */
+  PHYAI_VARIANT_DIT = 2     /* DiT head: adaLN-zero, alternating cross/self attention              */
+} phyai_variant;
+
+typedef enum {
+  PHYAI_DTYPE_F32 = 0,
+  PHYAI_DTYPE_BF16 = 1,     /* uint16 bit patterns of bfloat16                                     */
+  PHYAI_DTYPE_FP8E4M3 = 2   /* uint8 OCP e4m3fn codes with one float32 scale per output column     */
+} phyai_dtype;
+
+/* Shape of one expert.  Derived sizes: M = horizon + state_token suffix
+ * tokens per request.  weight_dtype F32 selects the fp32 path (all compute
+ * in fp32); BF16 and FP8E4M3 select the bf16 MFMA path (fp32 accumulate,
+ * fp32 residual stream, norms, softmax and solver state). */
+typedef struct {
+  int32_t variant;          /* phyai_variant                                                      */
+  int32_t n_layers;         /* L                                                                  */
+  int32_t d_model;          /* d (multiple of 64)                                                 */
+  int32_t n_q_heads;        /* query heads                                                        */
+  int32_t n_kv_heads;       /* key/value heads (1 for MQA)                                        */
+  int32_t head_dim;         /* 64, 128 or 256                                                     */
+  int32_t d_mlp;            /* MLP width F (multiple of 64)                                       */
+  int32_t horizon;          /* H action tokens per chunk                                          */
+  int32_t action_dim;       /* A values per action (<= 64)                                        */
+  int32_t max_steps;        /* largest K accepted by phyai_denoise                                */
+  int32_t prefix_cap;       /* P_cap: prefix rows reserved per request in the prefix buffer        */
+  int32_t max_batch;        /* largest B accepted by phyai_denoise                                */
+  int32_t state_token;      /* 1: one state token is prepended (needs `state`)                   */
+  int32_t rope;             /* 1: RoPE on suffix queries/keys at positions prefix_len + i          */
+  int32_t weight_dtype;     /* phyai_dtype of the per-layer trunk linears                         */
+  int32_t kv_dtype;         /* phyai_dtype of the prefix buffer (F32 or BF16)                     */
+  int32_t d_feat;           /* DiT: width of the VLM feature tokens; 0 otherwise                  */
+  int32_t time_dim;         /* width of the sinusoidal timestep embedding                         */
+  float rms_eps;            /* norm epsilon (1e-6)                                                */
+  float sin_min_period;     /* sinusoid periods run geometrically from min to max                 */
+  float sin_max_period;
+  float rope_base;          /* 10000                                                              */
+} phyai_config;
+
+/* One named parameter, stored [rows][cols] row-major on the host.  Linear
+ * weights are [in][out] (y = x W + b); vectors have rows = 1.  dtype must be
+ * the config's weight_dtype for the per-layer trunk linears
+ * (wq, wk, wv, wo, w_gate, w_up, w_down) and F32 or BF16 (matching the path:
+ * F32 for the fp32 path, BF16 otherwise) for every other tensor.  For
+ * FP8E4M3, `scale` holds `cols` float32 scales (W_ij = code_ij * scale_j). */
+typedef struct {
+  const char* name;         /* e.g. "in_w", "layers.3.wq" (see phyai_load_expert)               */
+  int32_t dtype;            /* phyai_dtype                                                        */
+  int32_t rows, cols;
+  const void* data;         /* host                                                               */
+  const float* scale;       /* host, FP8E4M3 only                                                 */
+} phyai_tensor;
+
+typedef struct phyai_expert phyai_expert;
+
+/* Validate `cfg`, copy and repack every tensor into library-owned device
+ * memory (MFMA operand order; the Q/K/V projections are fused into one
+ * weight and gate/up into another, as in the paper's single QKV and single
+ * gate+up GEMMs, Section "Optimization Methods", paragraph "Kernel fusion"),
+ * allocate the working buffers for up to max_batch requests, and build the
+ * timestep tables of the default schedule t_k = 1 - k/max_steps.
+ *
+ * Tensor names (L = n_layers, l = layer index):
+ *   all:   in_w [A][d], in_b [1][d], out_w [d][A], out_b [1][A],
+ *          layers.l.{wq [d][nq*dh], wk, wv [din][nkv*dh], wo [nq*dh][d]}
+ *          (din = d_feat on even DiT layers, else d)
+ *   state_token: state_w [A][d], state_b [1][d]
+ *   PI0:   time_w1 [d+time_dim][d], time_b1, time_w2 [d][d], time_b2,
+ *          layers.l.{attn_norm, mlp_norm} [1][d], final_norm [1][d],
+ *          layers.l.{w_gate, w_up} [d][F], layers.l.w_down [F][d]
+ *   PI05:  cond_w1 [time_dim][d], cond_b1, cond_w2 [d][d], cond_b2,
+ *          layers.l.{attn_mod_w, mlp_mod_w} [d][2d] (+ _b [1][2d]),
+ *          final_mod_w [d][2d], final_mod_b, gate/up/down as PI0
+ *   DIT:   cond_w1 [time_dim][d], cond_b1, cond_w2, cond_b2, pos_emb [H][d],
+ *          layers.l.ada_w [d][6d], ada_b [1][6d], layers.l.mlp_w1 [d][F],
+ *          mlp_b1 [1][F], mlp_w2 [F][d], mlp_b2 [1][d],
+ *          final_ada_w [d][2d], final_ada_b [1][2d]
+ * Host buffers may be freed after the call returns.  On failure *out is set
+ * to NULL and nothing is leaked.  The call synchronises `stream`. */
+int phyai_load_expert(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_tensors,
+                      void* stream, phyai_expert** out);
+
+/* Produce one action chunk per request (the K-step Euler loop).
+ *
+ *   prefix      device, read-only, caller-owned.  PI0/PI05: the frozen prefix
+ *               K/V cache, [L][2][B][prefix_cap][n_kv*head_dim] (index 0 = K,
+ *               1 = V; keys already rotated), dtype kv_dtype.  DIT: the VLM
+ *               feature tokens [B][prefix_cap][d_feat], dtype kv_dtype.
+ *               Rows at or beyond prefix_len[b] are never read.
+ *   prefix_len  host [B], 0 <= prefix_len[b] <= prefix_cap (DIT: >= 1).
+ *   noise       device float32 [B][H][A]: x at t_0.
+ *   timesteps   host float32 [n_steps + 1]: t_0 .. t_K (any values; the
+ *               default schedule runs from 1 to 0).  Tables that depend only
+ *               on the schedule are rebuilt when it differs from the last.
+ *   n_steps     K, 1 <= K <= max_steps.
+ *   batch       B, 1 <= B <= max_batch.
+ *   state       device float32 [B][A] when state_token = 1, else ignored.
+ *   out_actions device float32 [B][H][A]: x at t_K.  May alias `noise`.
+ *   stream      work is enqueued on it; the call returns after enqueueing.
+ *
+ * The first call for a (batch, n_steps) pair captures a HIP graph of the
+ * whole loop; later calls replay it and allocate nothing. */
+int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len,
+                  const float* noise, const float* timesteps, int32_t n_steps, int32_t batch,
+                  const float* state, float* out_actions, void* stream);
+
+/* Capture the graph for (batch, n_steps) ahead of the first phyai_denoise. */
+int phyai_prepare(phyai_expert* e, int32_t batch, int32_t n_steps, void* stream);
+
+/* Copy the residual stream h [B*M][d] (float32) left by the last
+ * phyai_denoise call (after the final step's last layer, before the final
+ * norm) into `dst` (device).  Diagnostic for layer-by-layer parity tests. */
+int phyai_debug_hidden(phyai_expert* e, float* dst, int32_t batch, void* stream);
+
+/* Decode `n` OCP e4m3fn codes (device uint8) to bfloat16 bit patterns (device
+ * uint16) with the same conversion the GEMM kernels use when they expand fp8
+ * weights (the W8A16 path of the paper's quantised GEMMs, paragraph
+ * "Quantization").  Codes 0x7f/0xff (NaN) give a NaN pattern. */
+int phyai_fp8_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, void* stream);
+
+/* Free every device buffer and graph of the handle.  NULL is accepted. */
+void phyai_free_expert(phyai_expert* e);
+
+/* Thread-local text of the last error ("" if none). */
+const char* phyai_last_error(void);
+
+/* Library ABI version (major * 100 + minor). */
+int phyai_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PHYAI_H */

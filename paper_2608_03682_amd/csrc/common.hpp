@@ -1,0 +1,130 @@
+// Device helpers shared by the gfx950 kernels: bf16/fp8 conversion, MFMA
+// operand types, wave/block reductions.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace phyai {
+
+typedef __attribute__((__vector_size__(8 * sizeof(__bf16)))) __bf16 bf16x8;
+typedef __attribute__((__vector_size__(4 * sizeof(float)))) float f32x4;
+typedef __attribute__((__vector_size__(2 * sizeof(float)))) float f32x2;
+typedef __attribute__((__vector_size__(2 * sizeof(__bf16)))) __bf16 bf16x2;
+
+typedef uint16_t bf16_t;   // storage type of bfloat16 values
+
+constexpr int kWave = 64;
+
+// ---------------------------------------------------------------------------
+// bf16 <-> f32
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float bf16_to_f32(bf16_t b) {
+  return __uint_as_float(static_cast<uint32_t>(b) << 16);
+}
+
+// Round to nearest even (NaN stays NaN).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<bf16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<bf16_t>(u >> 16);
+}
+
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  return static_cast<uint32_t>(f32_to_bf16(lo)) | (static_cast<uint32_t>(f32_to_bf16(hi)) << 16);
+}
+
+// ---------------------------------------------------------------------------
+// fp8 (OCP e4m3fn) -> bf16, exact.  gfx950's v_cvt_scalef32_pk_bf16_fp8
+// decodes two codes (selected by word_sel) with a unit scale.
+// ---------------------------------------------------------------------------
+template <bool HI>
+__device__ __forceinline__ uint32_t fp8x2_to_bf16x2(uint32_t codes4) {
+  bf16x2 r = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(codes4, 1.0f, HI);
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+// 8 fp8 codes (two dwords) -> 8 bf16 as an MFMA operand.
+__device__ __forceinline__ bf16x8 fp8x8_to_bf16x8(uint32_t lo, uint32_t hi) {
+  uint4 r;
+  r.x = fp8x2_to_bf16x2<false>(lo);
+  r.y = fp8x2_to_bf16x2<true>(lo);
+  r.z = fp8x2_to_bf16x2<false>(hi);
+  r.w = fp8x2_to_bf16x2<true>(hi);
+  return __builtin_bit_cast(bf16x8, r);
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+// D = A(16x32) * B(32x16) + C, bf16 operands, fp32 accumulate.
+// Lane l holds A[l%16][k8(l/16) .. +7], B[k8(l/16) .. +7][l%16] and
+// C[4*(l/16) + v][l%16] (v = 0..3).  The k order inside a lane only has to
+// agree between A and B.
+__device__ __forceinline__ f32x4 mfma16x16x32(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+// ---------------------------------------------------------------------------
+// reductions
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
+  return v;
+}
+
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
+  return v;
+}
+
+// Sum over the block; `scratch` holds one float per wave.  All threads get it.
+template <int NT>
+__device__ __forceinline__ float block_sum(float v, float* scratch) {
+  constexpr int NW = NT / kWave;
+  v = wave_sum(v);
+  const int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
+  __syncthreads();
+  if (l == 0) scratch[w] = v;
+  __syncthreads();
+  float t = 0.f;
+#pragma unroll
+  for (int i = 0; i < NW; ++i) t += scratch[i];
+  return t;
+}
+
+// ---------------------------------------------------------------------------
+// activations (fp32)
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float swish_f(float z) { return z / (1.0f + __expf(-z)); }
+
+__device__ __forceinline__ float gelu_tanh_f(float z) {
+  const float k0 = 0.7978845608028654f;   // sqrt(2/pi)
+  const float u = k0 * (z + 0.044715f * z * z * z);
+  return 0.5f * z * (1.0f + tanhf(u));
+}
+
+enum Act { ACT_NONE = 0, ACT_SWISH = 1, ACT_GELU = 2 };
+
+__device__ __forceinline__ float apply_act(int act, float v) {
+  if (act == ACT_SWISH) return swish_f(v);
+  if (act == ACT_GELU) return gelu_tanh_f(v);
+  return v;
+}
+
+// Activation storage: bf16 on the MFMA path, f32 on the fp32 path.
+template <typename T> struct ActIO;
+template <> struct ActIO<float> {
+  static __device__ __forceinline__ float round(float v) { return v; }
+  static __device__ __forceinline__ float load(const float* p) { return *p; }
+  static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
+};
+template <> struct ActIO<bf16_t> {
+  static __device__ __forceinline__ float round(float v) { return bf16_to_f32(f32_to_bf16(v)); }
+  static __device__ __forceinline__ float load(const bf16_t* p) { return bf16_to_f32(*p); }
+  static __device__ __forceinline__ void store(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+};
+
+}  // namespace phyai

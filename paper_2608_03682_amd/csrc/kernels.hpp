@@ -1,0 +1,223 @@
+// Kernel interfaces of the denoising loop: argument blocks, GEMM epilogues
+// and the host-side launchers the runtime composes into a HIP graph.
+#pragma once
+
+#include "common.hpp"
+
+namespace phyai {
+
+constexpr int kMaxBatch = 512;
+
+// Per-call arguments, written into device memory by a one-block kernel right
+// before each graph replay (kernel arguments are copied at launch, so the
+// host copy can go away immediately).  Kernels inside the graph read the
+// caller's pointers and prefix lengths from here.
+struct CallDesc {
+  const void* prefix;
+  const float* noise;
+  const float* state;
+  float* out;
+  int32_t prefix_len[kMaxBatch];
+};
+
+// ---------------------------------------------------------------------------
+// GEMM: C[R][N] = A[R][K] * W[K][N], W pre-packed in MFMA operand order.
+// Columns are processed in "pair tiles" of 32: packed columns 32p .. 32p+15
+// (half 0) and 32p+16 .. 32p+31 (half 1) reach the epilogue together, in the
+// same thread, so that pairs (GeGLU gate/up, RoPE x1/x2) can be combined
+// without a shuffle.  Which logical columns a pair tile holds is decided by
+// the packing order chosen on the host.
+// ---------------------------------------------------------------------------
+enum WeightKind { W_F32 = 0, W_BF16 = 1, W_FP8 = 2 };
+
+struct GemmArgs {
+  const void* A;            // [R][lda], bf16 (MFMA path) or f32 (fp32 path)
+  const void* A_lo;         // optional second bf16 term: A = A + A_lo (compensated operand)
+  const void* const* A_ind; // if set: A = *A_ind + a_off (a per-call pointer in CallDesc)
+  int64_t a_off;
+  int lda;
+  int R;
+  int K;                    // multiple of 64 on the MFMA path
+  int NPT;                  // pair tiles (N / 32)
+  const void* W;            // packed weights
+  const float* scale;       // fp8: one scale per packed column
+  int kind;                 // WeightKind
+  // optional A-row validity: rows r with (r % rows_per_req) >= prefix_len[r / rows_per_req]
+  // read as zero (used for feature rows beyond a request's length)
+  int rows_per_req;
+  const CallDesc* desc;
+};
+
+template <typename OutT>
+struct EpiStore {
+  OutT* out; int ldo;
+  const float* bias;        // [N] or null
+  const float* rowvec;      // [N] added to every row, or null
+  int act;                  // Act
+  int grp, grp_stride, grp_off;   // row remap: (r/grp)*grp_stride + grp_off + r%grp (grp=0: identity)
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    int orow = r;
+    if (grp > 0) orow = (r / grp) * grp_stride + grp_off + (r % grp);
+    float v[2] = {a0, a1};
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int col = 32 * p + 16 * hf + c;
+      float t = v[hf];
+      if (bias) t += bias[col];
+      if (rowvec) t += rowvec[col];
+      ActIO<OutT>::store(out + (int64_t)orow * ldo + col, apply_act(act, t));
+    }
+  }
+};
+
+// h[r][col] += gate[col] * (acc + bias[col])
+struct EpiResid {
+  float* h; int ldh;
+  const float* bias;
+  const float* gate;
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    float v[2] = {a0, a1};
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int col = 32 * p + 16 * hf + c;
+      float t = v[hf];
+      if (bias) t += bias[col];
+      if (gate) t *= gate[col];
+      h[(int64_t)r * ldh + col] += t;
+    }
+  }
+};
+
+// pair tile p holds gate column 16p+c (half 0) and up column 16p+c (half 1).
+// With `lo` set (bf16 only) the rounding residue is stored there, so that
+// out + lo carries about 16 significant bits into the next GEMM.
+template <typename OutT>
+struct EpiGeglu {
+  OutT* out; int ldo;
+  OutT* lo;
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    const float v = gelu_tanh_f(a0) * a1;
+    const int64_t i = (int64_t)r * ldo + 16 * p + c;
+    ActIO<OutT>::store(out + i, v);
+    if (lo) ActIO<OutT>::store(lo + i, v - ActIO<OutT>::round(v));
+  }
+};
+
+// Fused QKV.  Heads are ordered [n_q query | n_kv key | n_kv value], each
+// head_dim wide; head h owns pair tiles h*D/32 .. (h+1)*D/32-1, and pair tile
+// j of a head holds dimension i = 16j+c (half 0) and i + D/2 (half 1), the
+// two halves that RoPE rotates together.
+template <typename OutT>
+struct EpiQkv {
+  OutT* q; OutT* k; OutT* v;
+  int D, nq, nkv;
+  int rope;
+  int M;                    // suffix tokens per request
+  const float* inv_freq;    // [D/2]: base^(-2i/D)
+  const CallDesc* desc;     // positions start at prefix_len[b]
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    const int tiles = D / 32;
+    const int head = p / tiles;
+    const int i = 16 * (p % tiles) + c;
+    if (rope && head < nq + nkv) {
+      const int b = r / M;
+      const float pos = (float)(desc->prefix_len[b] + (r % M));
+      float s, co;
+      sincosf(pos * inv_freq[i], &s, &co);
+      const float x1 = a0, x2 = a1;
+      a0 = x1 * co - x2 * s;
+      a1 = x2 * co + x1 * s;
+    }
+    OutT* dst;
+    int64_t base;
+    if (head < nq) { dst = q; base = (int64_t)r * nq * D + head * D; }
+    else if (head < nq + nkv) { dst = k; base = (int64_t)r * nkv * D + (head - nq) * D; }
+    else { dst = v; base = (int64_t)r * nkv * D + (head - nq - nkv) * D; }
+    ActIO<OutT>::store(dst + base + i, a0);
+    ActIO<OutT>::store(dst + base + i + D / 2, a1);
+  }
+};
+
+void gemm_store_bf16(const GemmArgs&, const EpiStore<bf16_t>&, hipStream_t);
+void gemm_store_f32(const GemmArgs&, const EpiStore<float>&, hipStream_t);
+void gemm_resid(const GemmArgs&, const EpiResid&, hipStream_t);
+void gemm_geglu_bf16(const GemmArgs&, const EpiGeglu<bf16_t>&, hipStream_t);
+void gemm_geglu_f32(const GemmArgs&, const EpiGeglu<float>&, hipStream_t);
+void gemm_qkv_bf16(const GemmArgs&, const EpiQkv<bf16_t>&, hipStream_t);
+void gemm_qkv_f32(const GemmArgs&, const EpiQkv<float>&, hipStream_t);
+
+// ---------------------------------------------------------------------------
+// Attention of suffix queries over two key segments:
+//   segment 1 (prefix K/V cache, or projected DiT features): per request,
+//     rows 0 .. len1(b)-1 at seg1_k/v + b*seg1_bstride + row*seg1_ld;
+//   segment 2 (the suffix tokens' own K/V): rows b*M .. b*M+len2-1 of sk/sv.
+// Query rows of (request b, kv head h) are token*G + g for the G = nq/nkv
+// query heads that share kv head h.
+// ---------------------------------------------------------------------------
+struct AttnArgs {
+  const void* q; int ldq;
+  const void* const* seg1_ind;  // if set, segment-1 base = *seg1_ind (+ offsets)
+  const void* seg1_k; const void* seg1_v;
+  int64_t seg1_k_off, seg1_v_off;
+  int64_t seg1_bstride; int seg1_ld;
+  int use_seg1;
+  const void* sk; const void* sv; int ld2; int len2;
+  int mask_mode;            // 0: all keys; 1: block mask (suffix token 0 is the state token)
+  void* out; int ldo;
+  float* part;              // split-KV partials (n_split > 1)
+  int n_split;
+  const CallDesc* desc;
+  int B, M, nq, nkv, D;
+  float scale;              // 1/sqrt(D)
+};
+
+void attention_bf16(const AttnArgs&, hipStream_t);
+void attention_f32(const AttnArgs&, hipStream_t);
+int64_t attention_partial_floats(int B, int M, int nq, int nkv, int D, int n_split);
+
+// ---------------------------------------------------------------------------
+// Row kernels
+// ---------------------------------------------------------------------------
+enum NormMode { NORM_RMS = 0, NORM_LN = 1 };
+
+// n = normalise(h) * (1 + mul) + shift ; RMS or mean-centred LayerNorm.
+// With n_lo set, n_lo receives the bf16 rounding residue of n (two-term operand).
+void norm_rows_bf16(const float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode,
+                    const float* mul, const float* shift, hipStream_t);
+void norm_rows_f32(const float* h, float* n, int R, int d, float eps, int mode,
+                   const float* mul, const float* shift, hipStream_t);
+
+struct EmbedArgs {
+  const float* x;           // solver state [B][H][A]
+  const float* in_w;        // [A][d] fp32
+  const float* in_b;        // [d]
+  const float* pos;         // [H][d] or null
+  const float* e_state;     // [B][d] or null (state rows of h)
+  float* h;                 // [B*M][d]: destination of state rows, and of action rows if act_out == null
+  void* act_out;            // [B*H][d] Act: destination of action rows (pi0 time MLP input)
+  int act_is_bf16;
+  int B, H, M, A, d, off;   // off = 1 if a state token leads each request
+};
+void embed_actions(const EmbedArgs&, hipStream_t);
+
+// e[b][c] = state[b] . W[:, c] + bias[c]; state read from CallDesc.
+void embed_state(const CallDesc* desc, const float* w, const float* b, float* e, int B, int A, int d,
+                 hipStream_t);
+
+struct ReadoutArgs {
+  const float* h; int B, H, M, off, d, A;
+  float eps; int mode;
+  const float* mul; const float* shift;   // final norm: * (1 + mul) + shift
+  const float* out_w;       // [d][A] fp32
+  const float* out_b;       // [A]
+  const float* dt;          // t_{k+1} - t_k (device scalar)
+  float* x;                 // [B][H][A], updated in place
+};
+void readout_euler(const ReadoutArgs&, hipStream_t);
+
+void copy_noise_to_state(const CallDesc* desc, float* x, int64_t n, hipStream_t);
+void copy_state_to_out(const CallDesc* desc, const float* x, int64_t n, hipStream_t);
+void set_call_desc(const CallDesc& host_desc, CallDesc* dev, hipStream_t);
+void fp8_to_bf16(const uint8_t* codes, bf16_t* out, int64_t n, hipStream_t);
+
+}  // namespace phyai

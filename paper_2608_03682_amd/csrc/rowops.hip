@@ -1,0 +1,202 @@
+// Row-wise kernels of the denoising loop: (ada)RMSNorm / adaLN normalisation,
+// action and state embedding, the fused final-norm + output-projection +
+// Euler update, and the per-call copies.
+#include "kernels.hpp"
+
+namespace phyai {
+
+namespace {
+
+constexpr int kMaxPer = 8;   // d <= 2048 with 256 threads
+
+// n = normalise(h) * (1 + mul) + shift.  RMS: h / sqrt(mean(h^2) + eps);
+// LN: (h - mean) / sqrt(var + eps).  Statistics in fp32.
+template <typename OutT>
+__global__ __launch_bounds__(256) void norm_rows_kernel(const float* __restrict__ h, OutT* __restrict__ n,
+                                                        OutT* __restrict__ n_lo, int d, float eps, int mode,
+                                                        const float* __restrict__ mul,
+                                                        const float* __restrict__ shift) {
+  __shared__ float scratch[4];
+  const int row = blockIdx.x;
+  const float* hr = h + (int64_t)row * d;
+  float v[kMaxPer];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    v[i] = c < d ? hr[c] : 0.f;
+    s += v[i];
+  }
+  float mu = 0.f;
+  if (mode == NORM_LN) mu = block_sum<256>(s, scratch) / d;
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    const float t = c < d ? v[i] - mu : 0.f;
+    ss += t * t;
+  }
+  const float r = rsqrtf(block_sum<256>(ss, scratch) / d + eps);
+  OutT* nr = n + (int64_t)row * d;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c < d) {
+      float t = (v[i] - mu) * r * (1.f + mul[c]);
+      if (shift) t += shift[c];
+      ActIO<OutT>::store(nr + c, t);
+      if (n_lo) ActIO<OutT>::store(n_lo + (int64_t)row * d + c, t - ActIO<OutT>::round(t));
+    }
+  }
+}
+
+// One block per suffix token row (b, t).
+__global__ __launch_bounds__(256) void embed_kernel(EmbedArgs e) {
+  __shared__ float xs[64];
+  const int row = blockIdx.x;
+  const int b = row / e.M, t = row % e.M;
+  if (e.off && t == 0) {
+    for (int c = threadIdx.x; c < e.d; c += 256) e.h[(int64_t)row * e.d + c] = e.e_state[(int64_t)b * e.d + c];
+    return;
+  }
+  const int j = t - e.off;
+  if (threadIdx.x < e.A) xs[threadIdx.x] = e.x[((int64_t)b * e.H + j) * e.A + threadIdx.x];
+  __syncthreads();
+  for (int c = threadIdx.x; c < e.d; c += 256) {
+    float y = e.in_b[c];
+    for (int a = 0; a < e.A; ++a) y = fmaf(xs[a], e.in_w[(int64_t)a * e.d + c], y);
+    if (e.pos) y += e.pos[(int64_t)j * e.d + c];
+    if (e.act_out) {
+      const int64_t o = ((int64_t)b * e.H + j) * e.d + c;
+      if (e.act_is_bf16) static_cast<bf16_t*>(e.act_out)[o] = f32_to_bf16(y);
+      else static_cast<float*>(e.act_out)[o] = y;
+    } else {
+      e.h[(int64_t)row * e.d + c] = y;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void state_embed_kernel(const CallDesc* desc, const float* w, const float* bias,
+                                                          float* e, int A, int d) {
+  __shared__ float xs[64];
+  const int b = blockIdx.x;
+  if (threadIdx.x < A) xs[threadIdx.x] = desc->state[(int64_t)b * A + threadIdx.x];
+  __syncthreads();
+  for (int c = threadIdx.x; c < d; c += 256) {
+    float y = bias[c];
+    for (int a = 0; a < A; ++a) y = fmaf(xs[a], w[(int64_t)a * d + c], y);
+    e[(int64_t)b * d + c] = y;
+  }
+}
+
+// One block per action row: final norm -> v = n W_out + b_out -> x += dt v.
+__global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs r) {
+  __shared__ float nrm[2048];
+  __shared__ float red[4][64];
+  __shared__ float scratch[4];
+  const int ar = blockIdx.x;                 // b*H + j
+  const int b = ar / r.H, j = ar % r.H;
+  const float* hr = r.h + ((int64_t)b * r.M + r.off + j) * r.d;
+  float v[kMaxPer];
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    v[i] = c < r.d ? hr[c] : 0.f;
+    s += v[i];
+  }
+  float mu = 0.f;
+  if (r.mode == NORM_LN) mu = block_sum<256>(s, scratch) / r.d;
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    const float t = c < r.d ? v[i] - mu : 0.f;
+    ss += t * t;
+  }
+  const float rs = rsqrtf(block_sum<256>(ss, scratch) / r.d + r.eps);
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c < r.d) {
+      float t = (v[i] - mu) * rs * (1.f + r.mul[c]);
+      if (r.shift) t += r.shift[c];
+      nrm[c] = t;
+    }
+  }
+  __syncthreads();
+  const int a = threadIdx.x % 64, gq = threadIdx.x / 64;
+  float part = 0.f;
+  if (a < r.A)
+    for (int c = gq; c < r.d; c += 4) part = fmaf(nrm[c], r.out_w[(int64_t)c * r.A + a], part);
+  red[gq][a] = part;
+  __syncthreads();
+  if (threadIdx.x < r.A) {
+    const float vel = red[0][a] + red[1][a] + red[2][a] + red[3][a] + r.out_b[a];
+    r.x[(int64_t)ar * r.A + a] += r.dt[0] * vel;
+  }
+}
+
+__global__ void copy_in_kernel(const CallDesc* desc, float* x, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) x[i] = desc->noise[i];
+}
+
+__global__ void copy_out_kernel(const CallDesc* desc, const float* x, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) desc->out[i] = x[i];
+}
+
+__global__ void set_desc_kernel(CallDesc d, CallDesc* dst) {
+  constexpr int W = sizeof(CallDesc) / 4;
+  const int32_t* src = reinterpret_cast<const int32_t*>(&d);
+  int32_t* out = reinterpret_cast<int32_t*>(dst);
+  for (int i = threadIdx.x; i < W; i += blockDim.x) out[i] = src[i];
+}
+
+__global__ void fp8_decode_kernel(const uint8_t* codes, bf16_t* out, int64_t n) {
+  const int64_t i = ((int64_t)blockIdx.x * blockDim.x + threadIdx.x) * 4;
+  if (i >= n) return;
+  uint32_t w = 0;
+  for (int k = 0; k < 4 && i + k < n; ++k) w |= static_cast<uint32_t>(codes[i + k]) << (8 * k);
+  const uint32_t lo = fp8x2_to_bf16x2<false>(w), hi = fp8x2_to_bf16x2<true>(w);
+  const bf16_t r[4] = {static_cast<bf16_t>(lo & 0xffff), static_cast<bf16_t>(lo >> 16),
+                       static_cast<bf16_t>(hi & 0xffff), static_cast<bf16_t>(hi >> 16)};
+  for (int k = 0; k < 4 && i + k < n; ++k) out[i + k] = r[k];
+}
+
+}  // namespace
+
+void norm_rows_bf16(const float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode, const float* mul,
+                    const float* shift, hipStream_t s) {
+  hipLaunchKernelGGL(norm_rows_kernel<bf16_t>, dim3(R), dim3(256), 0, s, h, n, n_lo, d, eps, mode, mul, shift);
+}
+void norm_rows_f32(const float* h, float* n, int R, int d, float eps, int mode, const float* mul,
+                   const float* shift, hipStream_t s) {
+  hipLaunchKernelGGL(norm_rows_kernel<float>, dim3(R), dim3(256), 0, s, h, n, nullptr, d, eps, mode, mul, shift);
+}
+void embed_actions(const EmbedArgs& e, hipStream_t s) {
+  hipLaunchKernelGGL(embed_kernel, dim3(e.B * e.M), dim3(256), 0, s, e);
+}
+void embed_state(const CallDesc* desc, const float* w, const float* b, float* e, int B, int A, int d,
+                 hipStream_t s) {
+  hipLaunchKernelGGL(state_embed_kernel, dim3(B), dim3(256), 0, s, desc, w, b, e, A, d);
+}
+void readout_euler(const ReadoutArgs& r, hipStream_t s) {
+  hipLaunchKernelGGL(readout_kernel, dim3(r.B * r.H), dim3(256), 0, s, r);
+}
+void copy_noise_to_state(const CallDesc* desc, float* x, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(copy_in_kernel, dim3((n + 255) / 256), dim3(256), 0, s, desc, x, n);
+}
+void copy_state_to_out(const CallDesc* desc, const float* x, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(copy_out_kernel, dim3((n + 255) / 256), dim3(256), 0, s, desc, x, n);
+}
+void set_call_desc(const CallDesc& d, CallDesc* dev, hipStream_t s) {
+  hipLaunchKernelGGL(set_desc_kernel, dim3(1), dim3(256), 0, s, d, dev);
+}
+void fp8_to_bf16(const uint8_t* codes, bf16_t* out, int64_t n, hipStream_t s) {
+  const int64_t groups = (n + 3) / 4;
+  hipLaunchKernelGGL(fp8_decode_kernel, dim3((groups + 255) / 256), dim3(256), 0, s, codes, out, n);
+}
+
+}  // namespace phyai

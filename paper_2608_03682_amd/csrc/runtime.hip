@@ -1,0 +1,861 @@
+// Host runtime behind the C ABI: validation, weight packing, working buffers,
+// timestep tables, and capture/replay of the K-step loop as a HIP graph.
+//
+// The runner owns every mutable buffer of the loop and the graph buckets
+// keyed by (batch, steps); the prefix state is a read-only per-call input
+// whose validity is one chunk (Section "PhyAI Architecture", paragraphs
+// "Overview" and "Graph replay").
+#include <algorithm>
+#include <cmath>
+#include <cstdlib>
+#include <functional>
+#include <cstring>
+#include <map>
+#include <stdexcept>
+#include <string>
+#include <utility>
+#include <vector>
+
+#include "../../include/phyai.h"
+#include "kernels.hpp"
+
+using namespace phyai;
+
+namespace {
+
+thread_local std::string g_err;
+
+struct Fail {
+  int code;
+  std::string msg;
+};
+
+[[noreturn]] void fail(int code, const std::string& msg) { throw Fail{code, msg}; }
+
+void hip_check(hipError_t e, const char* what) {
+  if (e != hipSuccess) fail(PHYAI_EHIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+#define HIPC(x) hip_check((x), #x)
+
+uint16_t f2bf(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return static_cast<uint16_t>((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return static_cast<uint16_t>(u >> 16);
+}
+float bf2f(uint16_t b) {
+  const uint32_t u = static_cast<uint32_t>(b) << 16;
+  float f;
+  std::memcpy(&f, &u, 4);
+  return f;
+}
+
+struct DevMem {
+  std::vector<void*> ptrs;
+  void* alloc(size_t bytes) {
+    if (bytes == 0) bytes = 16;
+    void* p = nullptr;
+    hipError_t e = hipMalloc(&p, bytes);
+    if (e != hipSuccess) fail(PHYAI_ENOMEM, "hipMalloc(" + std::to_string(bytes) + ") failed: " + hipGetErrorString(e));
+    ptrs.push_back(p);
+    return p;
+  }
+  template <typename T> T* alloc_n(size_t n) { return static_cast<T*>(alloc(n * sizeof(T))); }
+  ~DevMem() {
+    for (void* p : ptrs) (void)hipFree(p);
+  }
+};
+
+struct Lin {
+  void* w = nullptr;
+  float* scale = nullptr;
+  int K = 0, NPT = 0, kind = W_BF16;
+};
+
+struct LayerW {
+  Lin qkv, kv_cross, o, gu, down, attn_mod, mlp_mod, ada;
+  float *attn_norm = nullptr, *mlp_norm = nullptr;
+  float *attn_mod_b = nullptr, *mlp_mod_b = nullptr, *ada_b = nullptr, *mlp_b1 = nullptr, *mlp_b2 = nullptr;
+};
+
+struct Bucket {
+  hipGraph_t graph = nullptr;
+  hipGraphExec_t exec = nullptr;
+};
+
+}  // namespace
+
+struct phyai_expert {
+  phyai_config c{};
+  bool f32 = false;
+  int L = 0, d = 0, D = 0, nq = 0, nkv = 0, H = 0, A = 0, F = 0, M = 0, off = 0, qd = 0, kd = 0;
+  int Bmax = 0, Kmax = 0, P = 0, Wpre = 0, act_bytes = 2;
+  DevMem mem;
+  // parameters
+  float *in_w = nullptr, *in_b = nullptr, *state_w = nullptr, *state_b = nullptr, *pos = nullptr;
+  float *out_w = nullptr, *out_b = nullptr, *final_norm = nullptr;
+  float *time_b1 = nullptr, *time_b2 = nullptr, *cond_b1 = nullptr, *cond_b2 = nullptr, *final_b = nullptr;
+  Lin time_w1a, time_w1t, time_w2, cond_w1, cond_w2, final_mod;
+  std::vector<LayerW> layers;
+  float* inv_freq = nullptr;
+  // working buffers
+  float *x = nullptr, *h = nullptr, *e_state = nullptr, *part = nullptr;
+  void *n = nullptr, *abuf = nullptr, *zbuf = nullptr, *q = nullptr, *ks = nullptr, *vs = nullptr;
+  void *o = nullptr, *g = nullptr, *cross = nullptr;
+  // two-term activations (hi + lo bf16) for the GEMMs fed by a norm or by GeGLU
+  bool split_act = false;
+  void *n_lo = nullptr, *g_lo = nullptr;
+  CallDesc* desc = nullptr;
+  // timestep tables
+  void *tau = nullptr, *c1 = nullptr, *cact = nullptr;
+  float *T = nullptr, *modtab = nullptr, *adatab = nullptr, *fintab = nullptr, *dt = nullptr;
+  std::vector<float> ts_cached;
+  std::map<std::pair<int, int>, Bucket> buckets;
+  hipStream_t cap = nullptr;
+
+  ~phyai_expert() {
+    for (auto& kv : buckets) {
+      if (kv.second.exec) (void)hipGraphExecDestroy(kv.second.exec);
+      if (kv.second.graph) (void)hipGraphDestroy(kv.second.graph);
+    }
+    if (cap) (void)hipStreamDestroy(cap);
+  }
+};
+
+namespace {
+
+// ---------------------------------------------------------------------------
+// parameter lookup and packing
+// ---------------------------------------------------------------------------
+struct Params {
+  std::map<std::string, const phyai_tensor*> by_name;
+  const phyai_tensor* get(const std::string& n, int rows, int cols) const {
+    auto it = by_name.find(n);
+    if (it == by_name.end()) fail(PHYAI_EINVAL, "missing tensor '" + n + "'");
+    const phyai_tensor* t = it->second;
+    if (t->rows != rows || t->cols != cols)
+      fail(PHYAI_EINVAL, "tensor '" + n + "' has shape [" + std::to_string(t->rows) + "][" +
+                             std::to_string(t->cols) + "], expected [" + std::to_string(rows) + "][" +
+                             std::to_string(cols) + "]");
+    if (!t->data) fail(PHYAI_EINVAL, "tensor '" + n + "' has no data");
+    return t;
+  }
+};
+
+float elem_f32(const phyai_tensor* t, int64_t i) {
+  if (t->dtype == PHYAI_DTYPE_F32) return static_cast<const float*>(t->data)[i];
+  if (t->dtype == PHYAI_DTYPE_BF16) return bf2f(static_cast<const uint16_t*>(t->data)[i]);
+  fail(PHYAI_EINVAL, std::string("tensor '") + t->name + "' must be F32 or BF16 here");
+}
+
+// Small parameters used by the row kernels are kept as fp32 (exact decode).
+float* upload_f32(phyai_expert& e, const phyai_tensor* t, hipStream_t s) {
+  const int64_t n = (int64_t)t->rows * t->cols;
+  std::vector<float> v(n);
+  for (int64_t i = 0; i < n; ++i) v[i] = elem_f32(t, i);
+  float* p = e.mem.alloc_n<float>(n);
+  HIPC(hipMemcpyAsync(p, v.data(), n * 4, hipMemcpyHostToDevice, s));
+  HIPC(hipStreamSynchronize(s));
+  return p;
+}
+
+// Pack the column-concatenation of `srcs` ([K][sum cols]) into MFMA operand
+// order.  perm(pc) gives the logical column of packed column pc (-1: zero).
+template <class Perm>
+Lin pack_linear(phyai_expert& e, const std::vector<const phyai_tensor*>& srcs, int Np, Perm perm, int kind,
+                hipStream_t s) {
+  const int K = srcs[0]->rows;
+  std::vector<int> src_of, col_of;
+  for (size_t i = 0; i < srcs.size(); ++i) {
+    if (srcs[i]->rows != K) fail(PHYAI_EINVAL, "fused linear sources disagree in rows");
+    const int want = kind == W_FP8 ? PHYAI_DTYPE_FP8E4M3 : (kind == W_BF16 ? PHYAI_DTYPE_BF16 : PHYAI_DTYPE_F32);
+    if (srcs[i]->dtype != want)
+      fail(PHYAI_EINVAL, std::string("tensor '") + srcs[i]->name + "' has the wrong dtype for this path");
+    if (kind == W_FP8 && !srcs[i]->scale) fail(PHYAI_EINVAL, std::string("tensor '") + srcs[i]->name + "' needs scales");
+    for (int c = 0; c < srcs[i]->cols; ++c) {
+      src_of.push_back((int)i);
+      col_of.push_back(c);
+    }
+  }
+  if (Np % 32) fail(PHYAI_EINVAL, "packed width must be a multiple of 32");
+  if (kind != W_F32 && K % 64) fail(PHYAI_EUNSUPPORTED, "MFMA linears need K % 64 == 0");
+  Lin L;
+  L.K = K;
+  L.NPT = Np / 32;
+  L.kind = kind;
+  const int nkb = K / 64;
+  if (kind == W_F32) {
+    std::vector<float> buf((size_t)K * Np, 0.f);
+    for (int pc = 0; pc < Np; ++pc) {
+      const int lc = perm(pc);
+      if (lc < 0) continue;
+      const phyai_tensor* t = srcs[src_of[lc]];
+      const int cc = col_of[lc];
+      for (int k = 0; k < K; ++k) buf[(size_t)k * Np + pc] = static_cast<const float*>(t->data)[(int64_t)k * t->cols + cc];
+    }
+    L.w = e.mem.alloc(buf.size() * 4);
+    HIPC(hipMemcpyAsync(L.w, buf.data(), buf.size() * 4, hipMemcpyHostToDevice, s));
+    HIPC(hipStreamSynchronize(s));
+    return L;
+  }
+  const size_t esz = kind == W_FP8 ? 1 : 2;
+  std::vector<uint8_t> buf((size_t)K * Np * esz, 0);
+  std::vector<float> sc(kind == W_FP8 ? Np : 0, 1.f);
+  for (int pc = 0; pc < Np; ++pc) {
+    const int lc = perm(pc);
+    const int p = pc / 32, hf = (pc % 32) / 16, c = pc % 16;
+    const phyai_tensor* t = lc >= 0 ? srcs[src_of[lc]] : nullptr;
+    const int cc = lc >= 0 ? col_of[lc] : 0;
+    if (kind == W_FP8 && t) sc[pc] = t->scale[cc];
+    for (int k = 0; k < K; ++k) {
+      const int kb = k / 64, st = (k % 64) / 32, kg = (k % 32) / 8, j = k % 8;
+      const int lane = kg * 16 + c;
+      const size_t frag = ((size_t)(p * nkb + kb) * 2 + hf) * 64 + lane;
+      if (kind == W_FP8) {
+        const uint8_t v = t ? static_cast<const uint8_t*>(t->data)[(int64_t)k * t->cols + cc] : 0;
+        buf[frag * 16 + st * 8 + j] = v;
+      } else {
+        const uint16_t v = t ? static_cast<const uint16_t*>(t->data)[(int64_t)k * t->cols + cc] : 0;
+        std::memcpy(&buf[(frag * 2 + st) * 16 + j * 2], &v, 2);
+      }
+    }
+  }
+  L.w = e.mem.alloc(buf.size());
+  HIPC(hipMemcpyAsync(L.w, buf.data(), buf.size(), hipMemcpyHostToDevice, s));
+  if (kind == W_FP8) {
+    L.scale = e.mem.alloc_n<float>(Np);
+    HIPC(hipMemcpyAsync(L.scale, sc.data(), Np * 4, hipMemcpyHostToDevice, s));
+  }
+  HIPC(hipStreamSynchronize(s));
+  return L;
+}
+
+Lin pack_identity(phyai_expert& e, const std::vector<const phyai_tensor*>& srcs, int kind, hipStream_t s) {
+  int N = 0;
+  for (auto* t : srcs) N += t->cols;
+  const int Np = (N + 31) / 32 * 32;
+  return pack_linear(e, srcs, Np, [N](int pc) { return pc < N ? pc : -1; }, kind, s);
+}
+
+// Heads [q | k | v], each D wide: pair tile j of a head holds dims 16j+c and
+// D/2 + 16j + c (the RoPE pair).
+Lin pack_heads(phyai_expert& e, const std::vector<const phyai_tensor*>& srcs, int D, int kind, hipStream_t s) {
+  int N = 0;
+  for (auto* t : srcs) N += t->cols;
+  return pack_linear(e, srcs, N, [D](int pc) {
+    const int p = pc / 32, hf = (pc % 32) / 16, c = pc % 16;
+    const int tiles = D / 32;
+    const int head = p / tiles, j = p % tiles;
+    return head * D + hf * (D / 2) + 16 * j + c;
+  }, kind, s);
+}
+
+// [gate | up], F wide each: pair tile p holds gate col 16p+c and up col 16p+c.
+Lin pack_geglu(phyai_expert& e, const phyai_tensor* gate, const phyai_tensor* up, int kind, hipStream_t s) {
+  const int F = gate->cols;
+  return pack_linear(e, {gate, up}, 2 * F, [F](int pc) {
+    const int p = pc / 32, hf = (pc % 32) / 16, c = pc % 16;
+    return hf * F + 16 * p + c;
+  }, kind, s);
+}
+
+// ---------------------------------------------------------------------------
+// launch helpers (overloads on the activation type)
+// ---------------------------------------------------------------------------
+void gemm_store(const GemmArgs& g, const EpiStore<bf16_t>& e, hipStream_t s) { gemm_store_bf16(g, e, s); }
+void gemm_store(const GemmArgs& g, const EpiStore<float>& e, hipStream_t s) { gemm_store_f32(g, e, s); }
+void gemm_geglu(const GemmArgs& g, const EpiGeglu<bf16_t>& e, hipStream_t s) { gemm_geglu_bf16(g, e, s); }
+void gemm_geglu(const GemmArgs& g, const EpiGeglu<float>& e, hipStream_t s) { gemm_geglu_f32(g, e, s); }
+void gemm_qkv(const GemmArgs& g, const EpiQkv<bf16_t>& e, hipStream_t s) { gemm_qkv_bf16(g, e, s); }
+void gemm_qkv(const GemmArgs& g, const EpiQkv<float>& e, hipStream_t s) { gemm_qkv_f32(g, e, s); }
+void norm_rows(const float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode, const float* mul,
+               const float* sh, hipStream_t s) { norm_rows_bf16(h, n, n_lo, R, d, eps, mode, mul, sh, s); }
+void norm_rows(const float* h, float* n, float*, int R, int d, float eps, int mode, const float* mul, const float* sh,
+               hipStream_t s) { norm_rows_f32(h, n, R, d, eps, mode, mul, sh, s); }
+
+GemmArgs gargs(const Lin& w, const void* A, int lda, int R) {
+  GemmArgs g{};
+  g.A = A;
+  g.lda = lda;
+  g.R = R;
+  g.K = w.K;
+  g.NPT = w.NPT;
+  g.W = w.w;
+  g.scale = w.scale;
+  g.kind = w.kind;
+  return g;
+}
+
+template <typename T> EpiStore<T> store_epi(T* out, int ldo, const float* bias, const float* rowvec, int act) {
+  EpiStore<T> e{};
+  e.out = out;
+  e.ldo = ldo;
+  e.bias = bias;
+  e.rowvec = rowvec;
+  e.act = act;
+  return e;
+}
+
+// split of the keys across blocks so that small batches still fill the chip
+int attn_splits(int B, int rows, int nkv, int keys) {
+  const int base = ((rows + 63) / 64) * B * nkv;
+  int s = (128 + base - 1) / base;
+  const int cap = keys / 64 > 1 ? keys / 64 : 1;
+  if (s > cap) s = cap;
+  return s < 1 ? 1 : s;
+}
+
+// ---------------------------------------------------------------------------
+// the K-step loop
+// ---------------------------------------------------------------------------
+template <typename T>
+void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
+  const int d = e.d, M = e.M, H = e.H, L = e.L, D = e.D;
+  const int R = B * M;
+  const int kind_act = e.f32 ? W_F32 : W_BF16;
+  (void)kind_act;
+  T* n = static_cast<T*>(e.n);
+  T* q = static_cast<T*>(e.q);
+  T* ks = static_cast<T*>(e.ks);
+  T* vs = static_cast<T*>(e.vs);
+  T* o = static_cast<T*>(e.o);
+  T* g = static_cast<T*>(e.g);
+  T* n_lo = static_cast<T*>(e.n_lo);
+  T* g_lo = static_cast<T*>(e.g_lo);
+  auto with_lo = [](GemmArgs ga, const void* lo) { ga.A_lo = lo; return ga; };
+  const int variant = e.c.variant;
+  const int S = 2 * L + 1;   // pi0.5 norm sites
+
+  copy_noise_to_state(e.desc, e.x, (int64_t)B * H * e.A, s);
+  if (e.c.state_token) embed_state(e.desc, e.state_w, e.state_b, e.e_state, B, e.A, d, s);
+  if (variant == PHYAI_VARIANT_DIT) {
+    for (int l = 0; l < L; l += 2) {
+      GemmArgs ga = gargs(e.layers[l].kv_cross, nullptr, e.c.d_feat, B * e.P);
+      ga.A_ind = reinterpret_cast<const void* const*>(&e.desc->prefix);
+      ga.a_off = 0;
+      ga.rows_per_req = e.P;
+      ga.desc = e.desc;
+      T* dst = static_cast<T*>(e.cross) + (int64_t)(l / 2) * e.Bmax * e.P * 2 * d;
+      gemm_store(ga, store_epi<T>(dst, 2 * d, nullptr, nullptr, ACT_NONE), s);
+    }
+  }
+
+  const int keys_self = (variant == PHYAI_VARIANT_DIT) ? M : e.P + M;
+  const int nsplit_main = attn_splits(B, M * (e.nq / e.nkv), e.nkv, keys_self);
+  const int nsplit_cross = attn_splits(B, M * (e.nq / e.nkv), e.nkv, e.P);
+
+  for (int k = 0; k < K; ++k) {
+    // ---- action tokens -> h
+    EmbedArgs em{};
+    em.x = e.x;
+    em.in_w = e.in_w;
+    em.in_b = e.in_b;
+    em.pos = e.pos;
+    em.e_state = e.e_state;
+    em.h = e.h;
+    em.act_out = variant == PHYAI_VARIANT_PI0 ? e.abuf : nullptr;
+    em.act_is_bf16 = e.f32 ? 0 : 1;
+    em.B = B; em.H = H; em.M = M; em.A = e.A; em.d = d; em.off = e.off;
+    embed_actions(em, s);
+    if (variant == PHYAI_VARIANT_PI0) {
+      // u = W2 swish(W1a a + (W1t tau(t_k) + b1)) + b2, written into the action rows of h
+      gemm_store(gargs(e.time_w1a, e.abuf, d, B * H),
+                 store_epi<T>(static_cast<T*>(e.zbuf), d, nullptr, e.T + (int64_t)k * d, ACT_SWISH), s);
+      EpiStore<float> ep = store_epi<float>(e.h, d, e.time_b2, nullptr, ACT_NONE);
+      ep.grp = H; ep.grp_stride = M; ep.grp_off = e.off;
+      gemm_store(gargs(e.time_w2, e.zbuf, d, B * H), ep, s);
+    }
+
+    for (int l = 0; l < L; ++l) {
+      const LayerW& w = e.layers[l];
+      if (variant != PHYAI_VARIANT_DIT) {
+        const float* mul;
+        const float* sh = nullptr;
+        if (variant == PHYAI_VARIANT_PI0) mul = w.attn_norm;
+        else { mul = e.modtab + ((int64_t)k * S + 2 * l) * 2 * d; sh = mul + d; }
+        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul, sh, s);
+        EpiQkv<T> eq{q, ks, vs, D, e.nq, e.nkv, e.c.rope, M, e.inv_freq, e.desc};
+        gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
+        AttnArgs at{};
+        at.q = q; at.ldq = e.qd;
+        at.use_seg1 = 1;
+        at.seg1_ind = reinterpret_cast<const void* const*>(&e.desc->prefix);
+        const int64_t blk = (int64_t)B * e.P * e.Wpre;
+        at.seg1_k_off = ((int64_t)l * 2 + 0) * blk;
+        at.seg1_v_off = ((int64_t)l * 2 + 1) * blk;
+        at.seg1_bstride = (int64_t)e.P * e.Wpre;
+        at.seg1_ld = e.Wpre;
+        at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = M;
+        at.mask_mode = e.c.state_token ? 1 : 0;
+        at.out = o; at.ldo = e.qd;
+        at.part = e.part; at.n_split = e.f32 ? 1 : nsplit_main;
+        at.desc = e.desc;
+        at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
+        at.scale = 1.0f / std::sqrt((float)D);
+        if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
+        gemm_resid(gargs(w.o, o, e.qd, R), EpiResid{e.h, d, nullptr, nullptr}, s);
+        if (variant == PHYAI_VARIANT_PI0) { mul = w.mlp_norm; sh = nullptr; }
+        else { mul = e.modtab + ((int64_t)k * S + 2 * l + 1) * 2 * d; sh = mul + d; }
+        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul, sh, s);
+        gemm_geglu(with_lo(gargs(w.gu, n, d, R), n_lo), EpiGeglu<T>{g, e.F, g_lo}, s);
+        gemm_resid(with_lo(gargs(w.down, g, e.F, R), g_lo), EpiResid{e.h, d, nullptr, nullptr}, s);
+      } else {
+        const float* ada = e.adatab + ((int64_t)k * L + l) * 6 * d;
+        const float *sh1 = ada, *sc1 = ada + d, *g1 = ada + 2 * d, *sh2 = ada + 3 * d, *sc2 = ada + 4 * d,
+                    *g2 = ada + 5 * d;
+        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc1, sh1, s);
+        const bool cross = (l % 2) == 0;
+        EpiQkv<T> eq{q, ks, vs, D, e.nq, e.nkv, 0, M, e.inv_freq, e.desc};
+        gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
+        AttnArgs at{};
+        at.q = q; at.ldq = e.qd;
+        if (cross) {
+          const T* cb = static_cast<const T*>(e.cross) + (int64_t)(l / 2) * e.Bmax * e.P * 2 * d;
+          at.use_seg1 = 1;
+          at.seg1_k = cb;
+          at.seg1_v = cb + d;
+          at.seg1_bstride = (int64_t)e.P * 2 * d;
+          at.seg1_ld = 2 * d;
+          at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = 0;
+        } else {
+          at.use_seg1 = 0;
+          at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = M;
+        }
+        at.mask_mode = 0;
+        at.out = o; at.ldo = e.qd;
+        at.part = e.part; at.n_split = e.f32 ? 1 : (cross ? nsplit_cross : nsplit_main);
+        at.desc = e.desc;
+        at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
+        at.scale = 1.0f / std::sqrt((float)D);
+        if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
+        gemm_resid(gargs(w.o, o, e.qd, R), EpiResid{e.h, d, nullptr, g1}, s);
+        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc2, sh2, s);
+        gemm_store(with_lo(gargs(w.gu, n, d, R), n_lo), store_epi<T>(g, e.F, w.mlp_b1, nullptr, ACT_GELU), s);
+        gemm_resid(gargs(w.down, g, e.F, R), EpiResid{e.h, d, w.mlp_b2, g2}, s);
+      }
+    }
+
+    ReadoutArgs ro{};
+    ro.h = e.h; ro.B = B; ro.H = H; ro.M = M; ro.off = e.off; ro.d = d; ro.A = e.A;
+    ro.eps = e.c.rms_eps;
+    ro.out_w = e.out_w; ro.out_b = e.out_b; ro.dt = e.dt + k; ro.x = e.x;
+    if (variant == PHYAI_VARIANT_PI0) { ro.mode = NORM_RMS; ro.mul = e.final_norm; ro.shift = nullptr; }
+    else if (variant == PHYAI_VARIANT_PI05) {
+      ro.mode = NORM_RMS;
+      ro.mul = e.modtab + ((int64_t)k * S + 2 * L) * 2 * d;
+      ro.shift = ro.mul + d;
+    } else {
+      ro.mode = NORM_LN;
+      ro.shift = e.fintab + (int64_t)k * 2 * d;
+      ro.mul = ro.shift + d;
+    }
+    readout_euler(ro, s);
+  }
+  copy_state_to_out(e.desc, e.x, (int64_t)B * H * e.A, s);
+}
+
+// Tables that depend only on the schedule (paragraph "Graph replay"):
+// sinusoid, dt, pi0 time-MLP input half, pi0.5 adaRMS scale/shift, DiT adaLN.
+template <typename T>
+void build_tables(phyai_expert& e, const float* ts, int K, hipStream_t s) {
+  const int td = e.c.time_dim, d = e.d, L = e.L;
+  std::vector<double> tau((size_t)K * td);
+  const int half = td / 2;
+  for (int k = 0; k < K; ++k)
+    for (int i = 0; i < half; ++i) {
+      const double frac = (double)i / (half - 1);
+      const double period = (double)e.c.sin_min_period * std::pow((double)e.c.sin_max_period / e.c.sin_min_period, frac);
+      const double ang = 2.0 * M_PI * (double)ts[k] / period;
+      tau[(size_t)k * td + i] = std::sin(ang);
+      tau[(size_t)k * td + half + i] = std::cos(ang);
+    }
+  std::vector<float> dts(K);
+  for (int k = 0; k < K; ++k) dts[k] = ts[k + 1] - ts[k];
+  HIPC(hipMemcpyAsync(e.dt, dts.data(), K * 4, hipMemcpyHostToDevice, s));
+  if (e.f32) {
+    std::vector<float> tf(tau.begin(), tau.end());
+    HIPC(hipMemcpyAsync(e.tau, tf.data(), tf.size() * 4, hipMemcpyHostToDevice, s));
+    HIPC(hipStreamSynchronize(s));
+  } else {
+    std::vector<uint16_t> tb(tau.size());
+    for (size_t i = 0; i < tau.size(); ++i) tb[i] = f2bf((float)tau[i]);
+    HIPC(hipMemcpyAsync(e.tau, tb.data(), tb.size() * 2, hipMemcpyHostToDevice, s));
+    HIPC(hipStreamSynchronize(s));
+  }
+  T* tau_d = static_cast<T*>(e.tau);
+  if (e.c.variant == PHYAI_VARIANT_PI0) {
+    gemm_store(gargs(e.time_w1t, tau_d, td, K), store_epi<float>(e.T, d, e.time_b1, nullptr, ACT_NONE), s);
+  } else {
+    T* c1 = static_cast<T*>(e.c1);
+    T* ca = static_cast<T*>(e.cact);
+    gemm_store(gargs(e.cond_w1, tau_d, td, K), store_epi<T>(c1, d, e.cond_b1, nullptr, ACT_SWISH), s);
+    // pi0.5: c = swish(...); DiT: the adaLN maps read SiLU(c) -- both are swish of the second layer
+    gemm_store(gargs(e.cond_w2, c1, d, K), store_epi<T>(ca, d, e.cond_b2, nullptr, ACT_SWISH), s);
+    if (e.c.variant == PHYAI_VARIANT_PI05) {
+      const int S = 2 * L + 1;
+      for (int l = 0; l < L; ++l) {
+        gemm_store(gargs(e.layers[l].attn_mod, ca, d, K),
+                   store_epi<float>(e.modtab + (int64_t)(2 * l) * 2 * d, S * 2 * d, e.layers[l].attn_mod_b, nullptr, ACT_NONE), s);
+        gemm_store(gargs(e.layers[l].mlp_mod, ca, d, K),
+                   store_epi<float>(e.modtab + (int64_t)(2 * l + 1) * 2 * d, S * 2 * d, e.layers[l].mlp_mod_b, nullptr, ACT_NONE), s);
+      }
+      gemm_store(gargs(e.final_mod, ca, d, K),
+                 store_epi<float>(e.modtab + (int64_t)(2 * L) * 2 * d, S * 2 * d, e.final_b, nullptr, ACT_NONE), s);
+    } else {
+      for (int l = 0; l < L; ++l)
+        gemm_store(gargs(e.layers[l].ada, ca, d, K),
+                   store_epi<float>(e.adatab + (int64_t)l * 6 * d, L * 6 * d, e.layers[l].ada_b, nullptr, ACT_NONE), s);
+      gemm_store(gargs(e.final_mod, ca, d, K), store_epi<float>(e.fintab, 2 * d, e.final_b, nullptr, ACT_NONE), s);
+    }
+  }
+  HIPC(hipGetLastError());
+  HIPC(hipStreamSynchronize(s));
+  e.ts_cached.assign(ts, ts + K + 1);
+}
+
+void check_config(const phyai_config& c) {
+  auto req = [](bool ok, const std::string& m) { if (!ok) fail(PHYAI_EINVAL, m); };
+  req(c.variant >= 0 && c.variant <= 2, "variant out of range");
+  req(c.n_layers >= 1 && c.d_model >= 64 && c.n_q_heads >= 1 && c.n_kv_heads >= 1, "non-positive size");
+  req(c.n_q_heads % c.n_kv_heads == 0, "n_q_heads must be a multiple of n_kv_heads");
+  req(c.head_dim == 64 || c.head_dim == 128 || c.head_dim == 256, "head_dim must be 64, 128 or 256");
+  req(c.d_model % 64 == 0 && c.d_model <= 2048, "d_model must be a multiple of 64, at most 2048");
+  req(c.d_mlp >= 64 && c.d_mlp % 64 == 0, "d_mlp must be a positive multiple of 64");
+  req(c.horizon >= 1 && c.action_dim >= 1 && c.action_dim <= 64, "horizon >= 1 and 1 <= action_dim <= 64");
+  req(c.max_steps >= 1 && c.max_steps <= 1024, "max_steps out of range");
+  req(c.max_batch >= 1 && c.max_batch <= kMaxBatch, "max_batch out of range (1..512)");
+  req(c.prefix_cap >= 0, "prefix_cap < 0");
+  req(c.time_dim >= 4 && c.time_dim % 64 == 0, "time_dim must be a multiple of 64");
+  req(c.weight_dtype >= 0 && c.weight_dtype <= 2, "weight_dtype out of range");
+  req(c.rms_eps > 0.f, "rms_eps must be positive");
+  req(c.sin_min_period > 0.f && c.sin_max_period > 0.f, "sinusoid periods must be positive");
+  const bool f32 = c.weight_dtype == PHYAI_DTYPE_F32;
+  req(c.kv_dtype == (f32 ? PHYAI_DTYPE_F32 : PHYAI_DTYPE_BF16),
+      "kv_dtype must be F32 on the fp32 path and BF16 on the bf16/fp8 path");
+  if (c.variant == PHYAI_VARIANT_DIT) {
+    req(c.d_feat >= 64 && c.d_feat % 64 == 0, "DiT needs d_feat, a multiple of 64");
+    req(c.n_kv_heads == c.n_q_heads, "DiT attention has one key/value head per query head");
+    req(c.prefix_cap >= 1, "DiT needs prefix_cap >= 1 feature rows");
+    req(c.rope == 0, "DiT has no RoPE");
+  }
+  if (c.variant == PHYAI_VARIANT_PI05) req(c.state_token == 0, "pi0.5 has no state token");
+  const int64_t qd = (int64_t)c.n_q_heads * c.head_dim;
+  req(qd % 64 == 0, "n_q_heads * head_dim must be a multiple of 64");
+}
+
+void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_tensors, hipStream_t s,
+               phyai_expert* e) {
+  const phyai_config& c = *cfg;
+  check_config(c);
+  e->c = c;
+  e->f32 = c.weight_dtype == PHYAI_DTYPE_F32;
+  e->act_bytes = e->f32 ? 4 : 2;
+  e->L = c.n_layers; e->d = c.d_model; e->D = c.head_dim; e->nq = c.n_q_heads; e->nkv = c.n_kv_heads;
+  e->H = c.horizon; e->A = c.action_dim; e->F = c.d_mlp;
+  e->off = c.state_token ? 1 : 0;
+  e->M = e->H + e->off;
+  e->qd = e->nq * e->D; e->kd = e->nkv * e->D;
+  e->Bmax = c.max_batch; e->Kmax = c.max_steps; e->P = c.prefix_cap;
+  e->Wpre = c.variant == PHYAI_VARIANT_DIT ? c.d_feat : e->kd;
+  const int d = e->d, L = e->L, D = e->D, F = e->F, A = e->A;
+
+  Params P;
+  for (int i = 0; i < n_tensors; ++i) {
+    if (!tensors[i].name) fail(PHYAI_EINVAL, "tensor with NULL name");
+    P.by_name[tensors[i].name] = &tensors[i];
+  }
+  const int wk_small = e->f32 ? W_F32 : W_BF16;
+  const int wk_trunk = e->f32 ? W_F32 : (c.weight_dtype == PHYAI_DTYPE_FP8E4M3 ? W_FP8 : W_BF16);
+  auto vec = [&](const std::string& n, int len) { return upload_f32(*e, P.get(n, 1, len), s); };
+
+  e->in_w = upload_f32(*e, P.get("in_w", A, d), s);
+  e->in_b = vec("in_b", d);
+  e->out_w = upload_f32(*e, P.get("out_w", d, A), s);
+  e->out_b = vec("out_b", A);
+  if (c.state_token) {
+    e->state_w = upload_f32(*e, P.get("state_w", A, d), s);
+    e->state_b = vec("state_b", d);
+  }
+  if (c.variant == PHYAI_VARIANT_PI0) {
+    const phyai_tensor* w1 = P.get("time_w1", d + c.time_dim, d);
+    // split W1 into the rows acting on the action embedding and on tau(t)
+    phyai_tensor ta = *w1, tt = *w1;
+    const size_t esz = w1->dtype == PHYAI_DTYPE_F32 ? 4 : 2;
+    ta.rows = d;
+    tt.rows = c.time_dim;
+    tt.data = static_cast<const char*>(w1->data) + (size_t)d * d * esz;
+    e->time_w1a = pack_identity(*e, {&ta}, wk_small, s);
+    e->time_w1t = pack_identity(*e, {&tt}, wk_small, s);
+    e->time_b1 = vec("time_b1", d);
+    e->time_w2 = pack_identity(*e, {P.get("time_w2", d, d)}, wk_small, s);
+    e->time_b2 = vec("time_b2", d);
+    e->final_norm = vec("final_norm", d);
+  } else {
+    e->cond_w1 = pack_identity(*e, {P.get("cond_w1", c.time_dim, d)}, wk_small, s);
+    e->cond_b1 = vec("cond_b1", d);
+    e->cond_w2 = pack_identity(*e, {P.get("cond_w2", d, d)}, wk_small, s);
+    e->cond_b2 = vec("cond_b2", d);
+    if (c.variant == PHYAI_VARIANT_PI05) {
+      e->final_mod = pack_identity(*e, {P.get("final_mod_w", d, 2 * d)}, wk_small, s);
+      e->final_b = vec("final_mod_b", 2 * d);
+    } else {
+      e->final_mod = pack_identity(*e, {P.get("final_ada_w", d, 2 * d)}, wk_small, s);
+      e->final_b = vec("final_ada_b", 2 * d);
+      e->pos = upload_f32(*e, P.get("pos_emb", e->H, d), s);
+    }
+  }
+  e->layers.resize(L);
+  for (int l = 0; l < L; ++l) {
+    LayerW& w = e->layers[l];
+    const std::string p = "layers." + std::to_string(l) + ".";
+    const bool cross = c.variant == PHYAI_VARIANT_DIT && (l % 2 == 0);
+    const int kin = cross ? c.d_feat : d;
+    const phyai_tensor* wq = P.get(p + "wq", d, e->qd);
+    const phyai_tensor* wkt = P.get(p + "wk", kin, e->kd);
+    const phyai_tensor* wvt = P.get(p + "wv", kin, e->kd);
+    if (cross) {
+      w.qkv = pack_heads(*e, {wq}, D, wk_trunk, s);
+      w.kv_cross = pack_identity(*e, {wkt, wvt}, wk_trunk, s);
+    } else {
+      w.qkv = pack_heads(*e, {wq, wkt, wvt}, D, wk_trunk, s);
+    }
+    w.o = pack_identity(*e, {P.get(p + "wo", e->qd, d)}, wk_trunk, s);
+    if (c.variant == PHYAI_VARIANT_DIT) {
+      w.ada = pack_identity(*e, {P.get(p + "ada_w", d, 6 * d)}, wk_small, s);
+      w.ada_b = vec(p + "ada_b", 6 * d);
+      w.gu = pack_identity(*e, {P.get(p + "mlp_w1", d, F)}, wk_trunk, s);
+      w.mlp_b1 = vec(p + "mlp_b1", F);
+      w.down = pack_identity(*e, {P.get(p + "mlp_w2", F, d)}, wk_trunk, s);
+      w.mlp_b2 = vec(p + "mlp_b2", d);
+    } else {
+      w.gu = pack_geglu(*e, P.get(p + "w_gate", d, F), P.get(p + "w_up", d, F), wk_trunk, s);
+      w.down = pack_identity(*e, {P.get(p + "w_down", F, d)}, wk_trunk, s);
+      if (c.variant == PHYAI_VARIANT_PI0) {
+        w.attn_norm = vec(p + "attn_norm", d);
+        w.mlp_norm = vec(p + "mlp_norm", d);
+      } else {
+        w.attn_mod = pack_identity(*e, {P.get(p + "attn_mod_w", d, 2 * d)}, wk_small, s);
+        w.attn_mod_b = vec(p + "attn_mod_b", 2 * d);
+        w.mlp_mod = pack_identity(*e, {P.get(p + "mlp_mod_w", d, 2 * d)}, wk_small, s);
+        w.mlp_mod_b = vec(p + "mlp_mod_b", 2 * d);
+      }
+    }
+  }
+  // RoPE inverse frequencies
+  {
+    std::vector<float> inv(D / 2);
+    for (int i = 0; i < D / 2; ++i) inv[i] = (float)std::pow((double)c.rope_base, -2.0 * i / D);
+    e->inv_freq = e->mem.alloc_n<float>(D / 2);
+    HIPC(hipMemcpyAsync(e->inv_freq, inv.data(), inv.size() * 4, hipMemcpyHostToDevice, s));
+  }
+  // working buffers sized for max_batch
+  const int64_t Bm = e->Bmax, M = e->M, ab = e->act_bytes;
+  e->x = e->mem.alloc_n<float>(Bm * e->H * A);
+  e->h = e->mem.alloc_n<float>(Bm * M * d);
+  e->e_state = e->mem.alloc_n<float>(Bm * d);
+  e->n = e->mem.alloc(Bm * M * d * ab);
+  e->abuf = e->mem.alloc(Bm * e->H * d * ab);
+  e->zbuf = e->mem.alloc(Bm * e->H * d * ab);
+  e->q = e->mem.alloc(Bm * M * e->qd * ab);
+  e->ks = e->mem.alloc(Bm * M * e->kd * ab);
+  e->vs = e->mem.alloc(Bm * M * e->kd * ab);
+  e->o = e->mem.alloc(Bm * M * e->qd * ab);
+  e->g = e->mem.alloc(Bm * M * F * ab);
+  // pi0.5's adaRMS path amplifies the bf16 rounding of the normalised
+  // activations and of the GeGLU output; those GEMM operands carry a second
+  // bf16 term there (weights are still read once).
+  e->split_act = !e->f32 && c.variant == PHYAI_VARIANT_PI05;
+  if (e->split_act) {
+    e->n_lo = e->mem.alloc(Bm * M * d * ab);
+    e->g_lo = e->mem.alloc(Bm * M * F * ab);
+  }
+  if (c.variant == PHYAI_VARIANT_DIT) e->cross = e->mem.alloc((int64_t)((L + 1) / 2) * Bm * e->P * 2 * d * ab);
+  int64_t part = 0;
+  if (!e->f32) {
+    const int keys_main = c.variant == PHYAI_VARIANT_DIT ? e->M : e->P + e->M;
+    for (int B = 1; B <= e->Bmax; ++B) {
+      const int rows = e->M * (e->nq / e->nkv);
+      const int s1 = attn_splits(B, rows, e->nkv, keys_main);
+      const int s2 = attn_splits(B, rows, e->nkv, e->P);
+      int64_t need = attention_partial_floats(B, e->M, e->nq, e->nkv, D, s1);
+      if (c.variant == PHYAI_VARIANT_DIT)
+        need = std::max(need, attention_partial_floats(B, e->M, e->nq, e->nkv, D, s2));
+      part = std::max(part, need);
+    }
+  }
+  e->part = e->mem.alloc_n<float>(part > 0 ? part : 4);
+  e->desc = static_cast<CallDesc*>(e->mem.alloc(sizeof(CallDesc)));
+  // tables
+  const int64_t Km = e->Kmax;
+  e->tau = e->mem.alloc(Km * c.time_dim * ab);
+  e->c1 = e->mem.alloc(Km * d * ab);
+  e->cact = e->mem.alloc(Km * d * ab);
+  e->dt = e->mem.alloc_n<float>(Km);
+  if (c.variant == PHYAI_VARIANT_PI0) e->T = e->mem.alloc_n<float>(Km * d);
+  if (c.variant == PHYAI_VARIANT_PI05) e->modtab = e->mem.alloc_n<float>(Km * (2 * L + 1) * 2 * d);
+  if (c.variant == PHYAI_VARIANT_DIT) {
+    e->adatab = e->mem.alloc_n<float>(Km * L * 6 * d);
+    e->fintab = e->mem.alloc_n<float>(Km * 2 * d);
+  }
+  HIPC(hipStreamCreateWithFlags(&e->cap, hipStreamNonBlocking));
+  std::vector<float> ts(e->Kmax + 1);
+  for (int k = 0; k <= e->Kmax; ++k) ts[k] = (float)(1.0 - (double)k / e->Kmax);
+  if (e->f32) build_tables<float>(*e, ts.data(), e->Kmax, s);
+  else build_tables<bf16_t>(*e, ts.data(), e->Kmax, s);
+}
+
+Bucket& get_bucket(phyai_expert& e, int B, int K) {
+  auto key = std::make_pair(B, K);
+  auto it = e.buckets.find(key);
+  if (it != e.buckets.end()) return it->second;
+  Bucket bk;
+  HIPC(hipStreamBeginCapture(e.cap, hipStreamCaptureModeThreadLocal));
+  try {
+    if (e.f32) enqueue_loop<float>(e, B, K, e.cap);
+    else enqueue_loop<bf16_t>(e, B, K, e.cap);
+  } catch (...) {
+    hipGraph_t junk = nullptr;
+    (void)hipStreamEndCapture(e.cap, &junk);
+    if (junk) (void)hipGraphDestroy(junk);
+    throw;
+  }
+  HIPC(hipStreamEndCapture(e.cap, &bk.graph));
+  hipError_t ie = hipGraphInstantiate(&bk.exec, bk.graph, nullptr, nullptr, 0);
+  if (ie != hipSuccess) {
+    (void)hipGraphDestroy(bk.graph);
+    fail(PHYAI_EHIP, std::string("hipGraphInstantiate: ") + hipGetErrorString(ie));
+  }
+  return e.buckets.emplace(key, bk).first->second;
+}
+
+bool use_graphs() {
+  const char* v = std::getenv("PHYAI_NO_GRAPH");
+  return !(v && v[0] == '1');
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// C ABI
+// ---------------------------------------------------------------------------
+namespace {
+int run_guarded(const std::function<void()>& f) {
+  try {
+    f();
+    g_err.clear();
+    return PHYAI_OK;
+  } catch (const Fail& x) {
+    g_err = x.msg;
+    return x.code;
+  } catch (const std::bad_alloc&) {
+    g_err = "host allocation failed";
+    return PHYAI_ENOMEM;
+  } catch (const std::exception& x) {
+    g_err = x.what();
+    return PHYAI_EINVAL;
+  }
+}
+}  // namespace
+
+extern "C" {
+
+int phyai_version(void) { return 100; }
+
+const char* phyai_last_error(void) { return g_err.c_str(); }
+
+int phyai_load_expert(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_tensors, void* stream,
+                      phyai_expert** out) {
+  if (out) *out = nullptr;
+  return run_guarded([&] {
+    if (!cfg || !out) fail(PHYAI_EINVAL, "cfg and out must not be NULL");
+    if (n_tensors < 0 || (n_tensors > 0 && !tensors)) fail(PHYAI_EINVAL, "bad tensor list");
+    phyai_expert* e = new phyai_expert();
+    try {
+      load_impl(cfg, tensors, n_tensors, static_cast<hipStream_t>(stream), e);
+    } catch (...) {
+      delete e;
+      throw;
+    }
+    *out = e;
+  });
+}
+
+int phyai_prepare(phyai_expert* e, int32_t batch, int32_t n_steps, void* stream) {
+  (void)stream;
+  return run_guarded([&] {
+    if (!e) fail(PHYAI_EINVAL, "NULL handle");
+    if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range");
+    if (n_steps < 1 || n_steps > e->Kmax) fail(PHYAI_EINVAL, "n_steps out of range");
+    if (use_graphs()) get_bucket(*e, batch, n_steps);
+  });
+}
+
+int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len, const float* noise,
+                  const float* timesteps, int32_t n_steps, int32_t batch, const float* state, float* out_actions,
+                  void* stream) {
+  return run_guarded([&] {
+    if (!e) fail(PHYAI_EINVAL, "NULL handle");
+    if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range 1..max_batch");
+    if (n_steps < 1 || n_steps > e->Kmax) fail(PHYAI_EINVAL, "n_steps out of range 1..max_steps");
+    if (!prefix_len || !noise || !timesteps || !out_actions) fail(PHYAI_EINVAL, "NULL argument");
+    if (!prefix && e->P > 0) fail(PHYAI_EINVAL, "NULL prefix");
+    if (e->c.state_token && !state) fail(PHYAI_EINVAL, "state is required when state_token = 1");
+    for (int b = 0; b < batch; ++b) {
+      if (prefix_len[b] < 0 || prefix_len[b] > e->P)
+        fail(PHYAI_EINVAL, "prefix_len[" + std::to_string(b) + "] = " + std::to_string(prefix_len[b]) +
+                               " outside 0..prefix_cap");
+      if (e->c.variant == PHYAI_VARIANT_DIT && prefix_len[b] < 1)
+        fail(PHYAI_EINVAL, "DiT requests need at least one feature row");
+    }
+    for (int k = 0; k <= n_steps; ++k)
+      if (!std::isfinite(timesteps[k])) fail(PHYAI_EINVAL, "non-finite timestep");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    const bool same = (int)e->ts_cached.size() >= n_steps + 1 &&
+                      std::memcmp(e->ts_cached.data(), timesteps, (n_steps + 1) * 4) == 0;
+    if (!same) {
+      if (e->f32) build_tables<float>(*e, timesteps, n_steps, s);
+      else build_tables<bf16_t>(*e, timesteps, n_steps, s);
+    }
+    Bucket* bk = use_graphs() ? &get_bucket(*e, batch, n_steps) : nullptr;
+    CallDesc hd;
+    std::memset(&hd, 0, sizeof(hd));
+    hd.prefix = prefix;
+    hd.noise = noise;
+    hd.state = state;
+    hd.out = out_actions;
+    for (int b = 0; b < batch; ++b) hd.prefix_len[b] = prefix_len[b];
+    set_call_desc(hd, e->desc, s);
+    HIPC(hipGetLastError());
+    if (bk) {
+      HIPC(hipGraphLaunch(bk->exec, s));
+    } else {
+      if (e->f32) enqueue_loop<float>(*e, batch, n_steps, s);
+      else enqueue_loop<bf16_t>(*e, batch, n_steps, s);
+      HIPC(hipGetLastError());
+    }
+  });
+}
+
+int phyai_debug_hidden(phyai_expert* e, float* dst, int32_t batch, void* stream) {
+  return run_guarded([&] {
+    if (!e || !dst) fail(PHYAI_EINVAL, "NULL argument");
+    if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range");
+    HIPC(hipMemcpyAsync(dst, e->h, (size_t)batch * e->M * e->d * 4, hipMemcpyDeviceToDevice,
+                        static_cast<hipStream_t>(stream)));
+  });
+}
+
+int phyai_fp8_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, void* stream) {
+  return run_guarded([&] {
+    if (n < 0) fail(PHYAI_EINVAL, "n < 0");
+    if (n == 0) return;
+    if (!codes || !out) fail(PHYAI_EINVAL, "NULL argument");
+    fp8_to_bf16(codes, out, n, static_cast<hipStream_t>(stream));
+    HIPC(hipGetLastError());
+  });
+}
+
+void phyai_free_expert(phyai_expert* e) { delete e; }
+
+}  // extern "C"

@@ -1,0 +1,70 @@
+"""Host-only checks of the C ABI library: it loads, exports every symbol the
+header declares, reports its version and rejects bad arguments without a
+GPU (validation happens before any device work)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2608_03682_amd as px
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared():
+    src = open(os.path.join(ROOT, "include", "phyai.h")).read()
+    return sorted(set(re.findall(r"\b(phyai_[a-z0-9_]+)\s*\(", src)))
+
+
+def test_library_is_built():
+    assert os.path.exists(px.LIB_PATH), "run __graft_entry__.build() first"
+
+
+def test_exports_every_declared_symbol():
+    L = px.lib()
+    names = _declared()
+    assert set(names) == set(px.EXPORTS)
+    for n in names:
+        assert hasattr(L, n), n
+
+
+def test_version():
+    assert px.version() == 100
+
+
+def test_null_arguments_are_rejected():
+    L = px.lib()
+    h = ctypes.c_void_p()
+    assert L.phyai_load_expert(None, None, 0, None, ctypes.byref(h)) == px.PHYAI_EINVAL
+    assert b"NULL" in L.phyai_last_error()
+    assert L.phyai_denoise(None, None, None, None, None, 1, 1, None, None, None) == px.PHYAI_EINVAL
+    assert L.phyai_prepare(None, 1, 1, None) == px.PHYAI_EINVAL
+    assert L.phyai_fp8_to_bf16(None, None, -1, None) == px.PHYAI_EINVAL
+    L.phyai_free_expert(None)
+
+
+@pytest.mark.parametrize("field,value,needle", [
+    ("head_dim", 96, b"head_dim"),
+    ("d_model", 100, b"d_model"),
+    ("action_dim", 65, b"action_dim"),
+    ("max_batch", 513, b"max_batch"),
+    ("n_kv_heads", 3, b"multiple"),
+])
+def test_bad_config_rejected_before_device_work(field, value, needle):
+    import workloads as wl
+    cfg = px.make_config(wl.CONFIGS["pi0_bf16_b1"])
+    setattr(cfg, field, value)
+    h = ctypes.c_void_p()
+    rc = px.lib().phyai_load_expert(ctypes.byref(cfg), None, 0, None, ctypes.byref(h))
+    assert rc == px.PHYAI_EINVAL and not h.value
+    assert needle in px.lib().phyai_last_error()
+
+
+def test_missing_tensor_rejected():
+    import workloads as wl
+    cfg = px.make_config(wl.CONFIGS["tiny_fp32"])
+    h = ctypes.c_void_p()
+    rc = px.lib().phyai_load_expert(ctypes.byref(cfg), (px.Tensor * 1)(), 0, None, ctypes.byref(h))
+    assert rc == px.PHYAI_EINVAL
+    assert b"missing tensor 'in_w'" in px.lib().phyai_last_error()

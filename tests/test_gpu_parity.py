@@ -1,0 +1,89 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
+same seeded inputs.  Bars: max-abs <= tol * max(1, rms(oracle)) with tol
+1e-4 (fp32 path), 2e-2 (bf16), 5e-2 (fp8 weights)."""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from gpu_helpers import compare, run_gpu, small_cfg, to_device
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+def _expert(cfg, case, **kw):
+    import paper_2608_03682_amd as px
+    return px.Expert(cfg, case.weights, **kw)
+
+
+def _oracle(cfg, case):
+    return oracle.denoise(cfg, case.weights, case.prefix, case.prefix_len, case.noise, case.timesteps,
+                          case.state)
+
+
+def test_fp8_decode_all_codes_bit_exact():
+    import paper_2608_03682_amd as px
+    codes = torch.arange(256, dtype=torch.uint8, device="cuda")
+    bits = px.fp8_to_bf16(codes).cpu().numpy().view(np.uint16)
+    vals = oracle.decode_bf16(bits)
+    ref = oracle.E4M3FN_TABLE
+    nan = np.isnan(ref)
+    assert np.array_equal(np.isnan(vals), nan)
+    assert np.array_equal(vals[~nan], ref[~nan])
+    assert np.array_equal(np.signbit(vals[~nan]), np.signbit(ref[~nan]))
+
+
+@pytest.mark.parametrize("variant,kw", [
+    ("pi0", {}),
+    ("pi0", dict(head_dim=256, n_q_heads=2)),
+    ("pi0", dict(weight_dtype="fp8", batch=4)),
+    ("pi05", {}),
+    ("dit", {}),
+    ("pi0", dict(weight_dtype="f32", kv_dtype="f32", state_token=False, rope=False)),
+])
+def test_small_parity(variant, kw):
+    cfg = small_cfg(variant, **kw)
+    print(f"[case] small {variant} {kw}", flush=True)
+    case = wl.make_case(cfg, seed=3)
+    ex = _expert(cfg, case)
+    gpu = run_gpu(ex, case)
+    compare(f"small_{variant}_{kw}", gpu, _oracle(cfg, case), cfg)
+
+
+def test_tiny_fp32_full_config():
+    cfg = wl.CONFIGS["tiny_fp32"]
+    print("[case] tiny_fp32", flush=True)
+    case = wl.make_case(cfg, seed=0)
+    ex = _expert(cfg, case)
+    compare("tiny_fp32", run_gpu(ex, case), _oracle(cfg, case), cfg)
+
+
+@pytest.mark.parametrize("name", ["pi0_bf16_b1", "pi05_bf16_b1", "dit_bf16_b1"])
+def test_full_size_batch1(name):
+    cfg = wl.CONFIGS[name]
+    print(f"[case] {name}", flush=True)
+    case = wl.make_case(cfg, seed=0)
+    ex = _expert(cfg, case)
+    gpu = run_gpu(ex, case)
+    compare(name, gpu, _oracle(cfg, case), cfg)
+
+
+def test_full_size_batch64_fp8_sampled():
+    """The rollout batch: all 64 requests run on the GPU in the benchmark's
+    launch configuration; the oracle checks a sample of requests one by one
+    (the shortest and the longest prefix, plus the first and last slots)."""
+    cfg = wl.CONFIGS["pi0_fp8_b64"]
+    print("[case] pi0_fp8_b64 sampled", flush=True)
+    case = wl.make_case(cfg, seed=0)
+    ex = _expert(cfg, case)
+    gpu = run_gpu(ex, case)
+    assert np.isfinite(gpu).all()
+    pl = case.prefix_len
+    sample = sorted({0, cfg.batch - 1, int(np.argmin(pl)), int(np.argmax(pl))})
+    W = oracle.DecodedWeights(case.weights)
+    pre = wl.make_prefix(cfg, pl, 0, requests=sample)
+    ref = oracle.denoise(cfg, case.weights, pre, pl[sample], case.noise[sample], case.timesteps,
+                         case.state[sample], decoded=W, slots=list(range(len(sample))))
+    compare(f"pi0_fp8_b64 requests {sample}", gpu[sample], ref, cfg)
