@@ -1,0 +1,247 @@
+#!/usr/bin/env python3
+"""Benchmark of the action-expert denoising loop on one MI355X.
+
+One "step" is one phyai_denoise call: the whole K-step Euler loop of one
+batch (all transformer layers, attention over the frozen prefix, readout and
+Euler update), i.e. one action chunk per request.
+
+Headline (value): pi0-shaped expert, bf16 weights, batch 1 -- ms per chunk.
+Also measured in the same run and reported in the same JSON line:
+  * batch64: the pi0-shaped expert at rollout batch 64 with ragged prefixes
+    and fp8 weights -- chunks/s = B / T_sync (the paper's Q(B)).
+  * roofline: the dominant kernel of each leg, its algorithmic bytes (B=1,
+    HBM-bound) or FLOPs (B=64, MFMA-bound) per launch over its average
+    duration, timed with HIP events on the stream it runs on.
+  * cpu_baseline: the fp64 oracle on this host's cores, one chunk.
+
+Inputs are seeded synthetic tensors resident in HBM before the timed region.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
+
+
+def _log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def _upload(case):
+    import torch
+    pre = case.prefix
+    prefix = torch.from_numpy(pre.view(np.int16) if pre.dtype == np.uint16 else pre).cuda()
+    noise = torch.from_numpy(case.noise).cuda()
+    state = None if case.state is None else torch.from_numpy(case.state).cuda()
+    return prefix, noise, state
+
+
+def stage_bytes_flops(cfg, B, plen_sum):
+    """Algorithmic HBM bytes and FLOPs of one launch of each block stage
+    (one layer), following the phase-roofline accounting of weights +
+    activations + K/V + boundary I/O.  Rows: the B*M suffix tokens."""
+    d, F, D, nq, nkv = cfg.d_model, cfg.d_mlp, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
+    M = cfg.tokens
+    R = B * M
+    wb = 1 if cfg.weight_dtype == "fp8" else 2
+    scale = 4 if cfg.weight_dtype == "fp8" else 0
+    qd, kd = nq * D, nkv * D
+    Nqkv = qd + 2 * kd
+    rows_alg = B * cfg.horizon            # state-token recompute excluded from FLOPs
+    out = {
+        "norm1": (R * d * 4 + R * d * 2, 0.0),
+        "qkv": (d * Nqkv * wb + Nqkv * scale + R * d * 2 + R * Nqkv * 2, 2.0 * rows_alg * d * Nqkv),
+        "attn": (plen_sum * 2 * kd * 2 + R * 2 * kd * 2 + 2 * R * qd * 2,
+                 4.0 * rows_alg * nq * (plen_sum / B + M) * D),
+        "oproj": (qd * d * wb + d * scale + R * qd * 2 + 2 * R * d * 4, 2.0 * rows_alg * qd * d),
+        "norm2": (R * d * 4 + R * d * 2, 0.0),
+        "mlp_up": (d * 2 * F * wb + 2 * F * scale + R * d * 2 + R * F * 2, 2.0 * rows_alg * d * 2 * F),
+        "mlp_down": (F * d * wb + d * scale + R * F * 2 + 2 * R * d * 4, 2.0 * rows_alg * F * d),
+    }
+    return out
+
+
+def chunk_bytes(cfg, B, plen_sum):
+    """Algorithmic bytes of one phyai_denoise call (K steps): every step
+    streams all trunk weights, the prefix K/V of every layer and the
+    activations; per-step small weights (embedding, time MLP, readout)."""
+    per_layer = stage_bytes_flops(cfg, B, plen_sum)
+    step = sum(v[0] for v in per_layer.values()) * cfg.n_layers
+    d, A = cfg.d_model, cfg.action_dim
+    small = (2 * d * d * 2 if cfg.variant == "pi0" else 0) + (A * d + d * A) * 4
+    return (step + small) * cfg.n_steps
+
+
+def time_calls(fn, steps, warmup):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    evs[0].record()
+    for i in range(steps):
+        fn()
+        evs[i + 1].record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    per = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)])
+    return wall, per
+
+
+def time_stages(ex, reps=5):
+    """Average duration of one launch of each block stage (events around
+    `reps` passes over all layers, eager, on the current stream)."""
+    import torch
+    res = {}
+    L = ex.cfg.n_layers
+    for st in ("norm1", "qkv", "attn", "oproj", "norm2", "mlp_up", "mlp_down"):
+        ex.profile_stage(st, 1)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        ex.profile_stage(st, reps)
+        b.record()
+        torch.cuda.synchronize()
+        res[st] = a.elapsed_time(b) * 1e3 / (reps * L)     # microseconds per launch
+    return res
+
+
+def cpu_baseline(cfg, case):
+    import oracle
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+    except Exception:
+        cores = os.cpu_count() or 1
+    W = oracle.DecodedWeights(case.weights)
+    runs = []
+    t_total = 0.0
+    while len(runs) < 3 and (t_total < 10.0 or not runs):
+        t0 = time.perf_counter()
+        oracle.denoise(cfg, case.weights, case.prefix, case.prefix_len, case.noise, case.timesteps,
+                       case.state, decoded=W)
+        dt = time.perf_counter() - t0
+        runs.append(dt)
+        t_total += dt
+    ms = float(np.median(runs)) * 1e3
+    return {"value": ms, "unit": "ms/chunk", "cores": int(cores), "kind": "oracle",
+            "sample": f"{len(runs)} full chunk(s) of the batch-1 pi0 workload (K={cfg.n_steps} Euler steps, "
+                      f"L={cfg.n_layers}), float64 NumPy oracle, median"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-batch64", action="store_true")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (the expert loop shards as independent "
+              f"requests per GPU, with no cross-GPU step); --gpus {args.gpus} is not run.", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2608_03682_amd as px
+    import workloads as wl
+
+    torch.cuda.set_device(0)
+    K, W = args.steps, args.warmup
+
+    # ---------------- batch 1, pi0-shaped, bf16 ----------------
+    cfg = wl.CONFIGS["pi0_bf16_b1"]
+    _log(f"generating {cfg.name}")
+    case = wl.make_case(cfg, seed=args.seed)
+    ex = px.Expert(cfg, case.weights)
+    prefix, noise, state = _upload(case)
+    out = torch.empty_like(noise)
+    ex.prepare(1, cfg.n_steps)
+    fn = lambda: ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=out)
+    _log(f"timing {cfg.name}: {W} warmup + {K} timed")
+    wall, per = time_calls(fn, K, W)
+    ms = wall * 1e3 / K
+    assert np.isfinite(out.cpu().numpy()).all()
+    stages = time_stages(ex)
+    plen_sum = int(case.prefix_len.sum())
+    sb = stage_bytes_flops(cfg, 1, plen_sum)
+    dom = max(("qkv", "attn", "oproj", "mlp_up", "mlp_down"), key=lambda s: stages[s])
+    dom_bytes = sb[dom][0]
+    ach = dom_bytes / (stages[dom] * 1e-6) / 1e9
+    cb = chunk_bytes(cfg, 1, plen_sum)
+    rec = {
+        "metric": "pi0-shape action-chunk latency ms @B=1 + chunks/s @B=64; % HBM / MFMA peak",
+        "value": round(ms, 4), "unit": "ms/chunk", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(ms, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded N(0,0.02) weights, N(0,1) prefix K/V and noise)",
+        "config": {"workload": "pi0_bf16_b1: 18 layers, width 1024, 8 q heads + 1 kv head, head_dim 256, "
+                               "GeGLU 4096, RoPE, prefix 816, H=50 + state token, A=32, K=10 Euler steps, B=1",
+                   "batch": 1, "prefix_len": int(case.prefix_len[0]), "euler_steps": cfg.n_steps},
+        "latency_ms": {"mean": round(float(per.mean()), 4), "p50": round(float(np.median(per)), 4),
+                       "p99": round(float(np.percentile(per, 99)), 4)},
+        "stage_us_per_launch": {k: round(v, 2) for k, v in stages.items()},
+        "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": None,
+                     "kernel": dom, "bytes_per_launch": int(dom_bytes), "avg_us": round(stages[dom], 2)},
+        "chunk_roofline": {"bytes_per_chunk": int(cb), "achieved_GBs": round(cb / (ms * 1e-3) / 1e9, 1),
+                           "frac_of_hbm_peak": round(cb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+    }
+    if not args.no_cpu_baseline:
+        _log("timing the CPU oracle baseline")
+        rec["cpu_baseline"] = cpu_baseline(cfg, case)
+    ex.close()
+    del prefix, noise, state, out, case
+    torch.cuda.empty_cache()
+
+    # ---------------- batch 64, ragged prefixes, fp8 weights ----------------
+    if not args.no_batch64:
+        cfg = wl.CONFIGS["pi0_fp8_b64"]
+        _log(f"generating {cfg.name}")
+        case = wl.make_case(cfg, seed=args.seed)
+        ex = px.Expert(cfg, case.weights)
+        prefix, noise, state = _upload(case)
+        out = torch.empty_like(noise)
+        ex.prepare(cfg.batch, cfg.n_steps)
+        fn = lambda: ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=out)
+        K64, W64 = max(5, K // 5), max(2, W // 5)
+        _log(f"timing {cfg.name}: {W64} warmup + {K64} timed")
+        wall, per = time_calls(fn, K64, W64)
+        ms64 = wall * 1e3 / K64
+        assert np.isfinite(out.cpu().numpy()).all()
+        stages = time_stages(ex, reps=2)
+        plen_sum = int(case.prefix_len.sum())
+        sb = stage_bytes_flops(cfg, cfg.batch, plen_sum)
+        dom = max(("qkv", "attn", "oproj", "mlp_up", "mlp_down"), key=lambda s: stages[s])
+        fl = sb[dom][1]
+        ach = fl / (stages[dom] * 1e-6) / 1e12
+        chunk_flops = sum(v[1] for v in sb.values()) * cfg.n_layers * cfg.n_steps
+        rec["batch64"] = {
+            "workload": "pi0_fp8_b64: pi0 shape, B=64, ragged prefixes U[600,1000], fp8 e4m3 trunk weights "
+                        "(per-output-channel scales), bf16 prefix K/V, K=10",
+            "steps": K64, "warmup": W64, "ms_per_batch": round(ms64, 3),
+            "chunks_per_s": round(cfg.batch / (ms64 * 1e-3), 1),
+            "stage_us_per_launch": {k: round(v, 2) for k, v in stages.items()},
+            "roofline": {"bound": "mfma", "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+                         "flops_per_launch": int(fl), "avg_us": round(stages[dom], 2)},
+            "batch_TFLOPs": round(chunk_flops / (ms64 * 1e-3) / 1e12, 1),
+        }
+        ex.close()
+    print(json.dumps(rec), flush=True)
+
+
+if __name__ == "__main__":
+    main()

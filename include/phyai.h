@@ -159,6 +159,19 @@ int phyai_prepare(phyai_expert* e, int32_t batch, int32_t n_steps, void* stream)
  * norm) into `dst` (device).  Diagnostic for layer-by-layer parity tests. */
 int phyai_debug_hidden(phyai_expert* e, float* dst, int32_t batch, void* stream);
 
+/* Measurement aid: enqueue `reps` passes over all L layers of one stage of
+ * the transformer block, exactly as the graph launches it (step 0 of the
+ * current schedule, the batch of the last phyai_denoise call), eagerly on
+ * `stream`, so that a caller can time a single kernel with events.
+ * Stages: 0 norm before attention, 1 QKV GEMM (+RoPE, KV write),
+ * 2 attention (+split combine), 3 O-projection GEMM + residual, 4 norm
+ * before the MLP, 5 gate/up GEMM + GeGLU (DiT: MLP-in + GELU), 6 down GEMM
+ * + residual.  Requires a previous phyai_denoise on this handle (the stage
+ * reads the buffers it left); it overwrites working buffers only, never the
+ * caller's.  Loop semantics (Section "PhyAI Architecture", paragraph
+ * "Kernel fusion", lists these fused operators). */
+int phyai_profile_stage(phyai_expert* e, int32_t stage, int32_t reps, void* stream);
+
 /* Decode `n` OCP e4m3fn codes (device uint8) to bfloat16 bit patterns (device
  * uint16) with the same conversion the GEMM kernels use when they expand fp8
  * weights (the W8A16 path of the paper's quantised GEMMs, paragraph

@@ -22,7 +22,9 @@ _DTYPE = {"f32": 0, "bf16": 1, "fp8": 2}
 
 # Every symbol include/phyai.h declares.
 EXPORTS = ("phyai_load_expert", "phyai_denoise", "phyai_prepare", "phyai_debug_hidden",
-           "phyai_fp8_to_bf16", "phyai_free_expert", "phyai_last_error", "phyai_version")
+           "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_free_expert", "phyai_last_error",
+           "phyai_version")
+STAGES = {"norm1": 0, "qkv": 1, "attn": 2, "oproj": 3, "norm2": 4, "mlp_up": 5, "mlp_down": 6}
 
 
 class PhyaiError(RuntimeError):
@@ -61,11 +63,12 @@ def lib() -> ctypes.CDLL:
         L.phyai_prepare.argtypes = [vp, i32, i32, vp]
         L.phyai_debug_hidden.argtypes = [vp, vp, i32, vp]
         L.phyai_fp8_to_bf16.argtypes = [vp, vp, i64, vp]
+        L.phyai_profile_stage.argtypes = [vp, i32, i32, vp]
         L.phyai_free_expert.argtypes = [vp]
         L.phyai_free_expert.restype = None
         L.phyai_last_error.restype = ctypes.c_char_p
         for f in ("phyai_load_expert", "phyai_denoise", "phyai_prepare", "phyai_debug_hidden",
-                  "phyai_fp8_to_bf16", "phyai_version"):
+                  "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_version"):
             getattr(L, f).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -153,6 +156,10 @@ class Expert:
         dst = torch.empty((batch * M, c.d_model), dtype=torch.float32, device="cuda")
         _check(lib().phyai_debug_hidden(self._h, _ptr(dst), batch, _stream(stream)))
         return dst
+
+    def profile_stage(self, stage: str, reps: int, stream=None):
+        """Enqueue `reps` passes over all layers of one block stage (for timing)."""
+        _check(lib().phyai_profile_stage(self._h, STAGES[stage], reps, _stream(stream)))
 
     def close(self):
         if getattr(self, "_h", None):

@@ -111,6 +111,7 @@ struct phyai_expert {
   void *tau = nullptr, *c1 = nullptr, *cact = nullptr;
   float *T = nullptr, *modtab = nullptr, *adatab = nullptr, *fintab = nullptr, *dt = nullptr;
   std::vector<float> ts_cached;
+  int last_batch = 0;       // batch of the last phyai_denoise (0: none yet)
   std::map<std::pair<int, int>, Bucket> buckets;
   hipStream_t cap = nullptr;
 
@@ -309,12 +310,14 @@ int attn_splits(int B, int rows, int nkv, int keys) {
 // ---------------------------------------------------------------------------
 // the K-step loop
 // ---------------------------------------------------------------------------
+// One stage of transformer block l at step k (the graph records them in
+// order; phyai_profile_stage replays a single one).
+enum Stage { ST_NORM1 = 0, ST_QKV, ST_ATTN, ST_OPROJ, ST_NORM2, ST_MLP_UP, ST_MLP_DOWN, kStages };
+
 template <typename T>
-void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
-  const int d = e.d, M = e.M, H = e.H, L = e.L, D = e.D;
+void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s) {
+  const int d = e.d, M = e.M, L = e.L, D = e.D;
   const int R = B * M;
-  const int kind_act = e.f32 ? W_F32 : W_BF16;
-  (void)kind_act;
   T* n = static_cast<T*>(e.n);
   T* q = static_cast<T*>(e.q);
   T* ks = static_cast<T*>(e.ks);
@@ -326,6 +329,108 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
   auto with_lo = [](GemmArgs ga, const void* lo) { ga.A_lo = lo; return ga; };
   const int variant = e.c.variant;
   const int S = 2 * L + 1;   // pi0.5 norm sites
+  const LayerW& w = e.layers[l];
+  const float inv_sqrt_d = 1.0f / std::sqrt((float)D);
+  const int keys_self = (variant == PHYAI_VARIANT_DIT) ? M : e.P + M;
+  const int rows = M * (e.nq / e.nkv);
+
+  if (variant != PHYAI_VARIANT_DIT) {
+    const float* mul1 = w.attn_norm;
+    const float* sh1 = nullptr;
+    const float* mul2 = w.mlp_norm;
+    const float* sh2 = nullptr;
+    if (variant == PHYAI_VARIANT_PI05) {
+      mul1 = e.modtab + ((int64_t)k * S + 2 * l) * 2 * d;
+      sh1 = mul1 + d;
+      mul2 = e.modtab + ((int64_t)k * S + 2 * l + 1) * 2 * d;
+      sh2 = mul2 + d;
+    }
+    switch (stage) {
+      case ST_NORM1: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul1, sh1, s); break;
+      case ST_QKV: {
+        EpiQkv<T> eq{q, ks, vs, D, e.nq, e.nkv, e.c.rope, M, e.inv_freq, e.desc};
+        gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
+        break;
+      }
+      case ST_ATTN: {
+        AttnArgs at{};
+        at.q = q; at.ldq = e.qd;
+        at.use_seg1 = 1;
+        at.seg1_ind = reinterpret_cast<const void* const*>(&e.desc->prefix);
+        const int64_t blk = (int64_t)B * e.P * e.Wpre;
+        at.seg1_k_off = ((int64_t)l * 2 + 0) * blk;
+        at.seg1_v_off = ((int64_t)l * 2 + 1) * blk;
+        at.seg1_bstride = (int64_t)e.P * e.Wpre;
+        at.seg1_ld = e.Wpre;
+        at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = M;
+        at.mask_mode = e.c.state_token ? 1 : 0;
+        at.out = o; at.ldo = e.qd;
+        at.part = e.part; at.n_split = e.f32 ? 1 : attn_splits(B, rows, e.nkv, keys_self);
+        at.desc = e.desc;
+        at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
+        at.scale = inv_sqrt_d;
+        if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
+        break;
+      }
+      case ST_OPROJ: gemm_resid(gargs(w.o, o, e.qd, R), EpiResid{e.h, d, nullptr, nullptr}, s); break;
+      case ST_NORM2: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul2, sh2, s); break;
+      case ST_MLP_UP: gemm_geglu(with_lo(gargs(w.gu, n, d, R), n_lo), EpiGeglu<T>{g, e.F, g_lo}, s); break;
+      case ST_MLP_DOWN:
+        gemm_resid(with_lo(gargs(w.down, g, e.F, R), g_lo), EpiResid{e.h, d, nullptr, nullptr}, s);
+        break;
+    }
+    return;
+  }
+  // DiT block: adaLN-zero modulation from the per-step table
+  const float* ada = e.adatab + ((int64_t)k * L + l) * 6 * d;
+  const float *sh1 = ada, *sc1 = ada + d, *g1 = ada + 2 * d, *sh2 = ada + 3 * d, *sc2 = ada + 4 * d,
+              *g2 = ada + 5 * d;
+  const bool cross = (l % 2) == 0;
+  switch (stage) {
+    case ST_NORM1: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc1, sh1, s); break;
+    case ST_QKV: {
+      EpiQkv<T> eq{q, ks, vs, D, e.nq, e.nkv, 0, M, e.inv_freq, e.desc};
+      gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
+      break;
+    }
+    case ST_ATTN: {
+      AttnArgs at{};
+      at.q = q; at.ldq = e.qd;
+      if (cross) {
+        const T* cb = static_cast<const T*>(e.cross) + (int64_t)(l / 2) * e.Bmax * e.P * 2 * d;
+        at.use_seg1 = 1;
+        at.seg1_k = cb;
+        at.seg1_v = cb + d;
+        at.seg1_bstride = (int64_t)e.P * 2 * d;
+        at.seg1_ld = 2 * d;
+        at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = 0;
+      } else {
+        at.use_seg1 = 0;
+        at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = M;
+      }
+      at.mask_mode = 0;
+      at.out = o; at.ldo = e.qd;
+      at.part = e.part;
+      at.n_split = e.f32 ? 1 : attn_splits(B, rows, e.nkv, cross ? e.P : keys_self);
+      at.desc = e.desc;
+      at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
+      at.scale = inv_sqrt_d;
+      if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
+      break;
+    }
+    case ST_OPROJ: gemm_resid(gargs(w.o, o, e.qd, R), EpiResid{e.h, d, nullptr, g1}, s); break;
+    case ST_NORM2: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc2, sh2, s); break;
+    case ST_MLP_UP:
+      gemm_store(with_lo(gargs(w.gu, n, d, R), n_lo), store_epi<T>(g, e.F, w.mlp_b1, nullptr, ACT_GELU), s);
+      break;
+    case ST_MLP_DOWN: gemm_resid(gargs(w.down, g, e.F, R), EpiResid{e.h, d, w.mlp_b2, g2}, s); break;
+  }
+}
+
+template <typename T>
+void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
+  const int d = e.d, M = e.M, H = e.H, L = e.L;
+  const int variant = e.c.variant;
 
   copy_noise_to_state(e.desc, e.x, (int64_t)B * H * e.A, s);
   if (e.c.state_token) embed_state(e.desc, e.state_w, e.state_b, e.e_state, B, e.A, d, s);
@@ -340,10 +445,6 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
       gemm_store(ga, store_epi<T>(dst, 2 * d, nullptr, nullptr, ACT_NONE), s);
     }
   }
-
-  const int keys_self = (variant == PHYAI_VARIANT_DIT) ? M : e.P + M;
-  const int nsplit_main = attn_splits(B, M * (e.nq / e.nkv), e.nkv, keys_self);
-  const int nsplit_cross = attn_splits(B, M * (e.nq / e.nkv), e.nkv, e.P);
 
   for (int k = 0; k < K; ++k) {
     // ---- action tokens -> h
@@ -367,74 +468,8 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
       gemm_store(gargs(e.time_w2, e.zbuf, d, B * H), ep, s);
     }
 
-    for (int l = 0; l < L; ++l) {
-      const LayerW& w = e.layers[l];
-      if (variant != PHYAI_VARIANT_DIT) {
-        const float* mul;
-        const float* sh = nullptr;
-        if (variant == PHYAI_VARIANT_PI0) mul = w.attn_norm;
-        else { mul = e.modtab + ((int64_t)k * S + 2 * l) * 2 * d; sh = mul + d; }
-        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul, sh, s);
-        EpiQkv<T> eq{q, ks, vs, D, e.nq, e.nkv, e.c.rope, M, e.inv_freq, e.desc};
-        gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
-        AttnArgs at{};
-        at.q = q; at.ldq = e.qd;
-        at.use_seg1 = 1;
-        at.seg1_ind = reinterpret_cast<const void* const*>(&e.desc->prefix);
-        const int64_t blk = (int64_t)B * e.P * e.Wpre;
-        at.seg1_k_off = ((int64_t)l * 2 + 0) * blk;
-        at.seg1_v_off = ((int64_t)l * 2 + 1) * blk;
-        at.seg1_bstride = (int64_t)e.P * e.Wpre;
-        at.seg1_ld = e.Wpre;
-        at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = M;
-        at.mask_mode = e.c.state_token ? 1 : 0;
-        at.out = o; at.ldo = e.qd;
-        at.part = e.part; at.n_split = e.f32 ? 1 : nsplit_main;
-        at.desc = e.desc;
-        at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
-        at.scale = 1.0f / std::sqrt((float)D);
-        if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
-        gemm_resid(gargs(w.o, o, e.qd, R), EpiResid{e.h, d, nullptr, nullptr}, s);
-        if (variant == PHYAI_VARIANT_PI0) { mul = w.mlp_norm; sh = nullptr; }
-        else { mul = e.modtab + ((int64_t)k * S + 2 * l + 1) * 2 * d; sh = mul + d; }
-        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul, sh, s);
-        gemm_geglu(with_lo(gargs(w.gu, n, d, R), n_lo), EpiGeglu<T>{g, e.F, g_lo}, s);
-        gemm_resid(with_lo(gargs(w.down, g, e.F, R), g_lo), EpiResid{e.h, d, nullptr, nullptr}, s);
-      } else {
-        const float* ada = e.adatab + ((int64_t)k * L + l) * 6 * d;
-        const float *sh1 = ada, *sc1 = ada + d, *g1 = ada + 2 * d, *sh2 = ada + 3 * d, *sc2 = ada + 4 * d,
-                    *g2 = ada + 5 * d;
-        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc1, sh1, s);
-        const bool cross = (l % 2) == 0;
-        EpiQkv<T> eq{q, ks, vs, D, e.nq, e.nkv, 0, M, e.inv_freq, e.desc};
-        gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
-        AttnArgs at{};
-        at.q = q; at.ldq = e.qd;
-        if (cross) {
-          const T* cb = static_cast<const T*>(e.cross) + (int64_t)(l / 2) * e.Bmax * e.P * 2 * d;
-          at.use_seg1 = 1;
-          at.seg1_k = cb;
-          at.seg1_v = cb + d;
-          at.seg1_bstride = (int64_t)e.P * 2 * d;
-          at.seg1_ld = 2 * d;
-          at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = 0;
-        } else {
-          at.use_seg1 = 0;
-          at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = M;
-        }
-        at.mask_mode = 0;
-        at.out = o; at.ldo = e.qd;
-        at.part = e.part; at.n_split = e.f32 ? 1 : (cross ? nsplit_cross : nsplit_main);
-        at.desc = e.desc;
-        at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
-        at.scale = 1.0f / std::sqrt((float)D);
-        if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
-        gemm_resid(gargs(w.o, o, e.qd, R), EpiResid{e.h, d, nullptr, g1}, s);
-        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc2, sh2, s);
-        gemm_store(with_lo(gargs(w.gu, n, d, R), n_lo), store_epi<T>(g, e.F, w.mlp_b1, nullptr, ACT_GELU), s);
-        gemm_resid(gargs(w.down, g, e.F, R), EpiResid{e.h, d, w.mlp_b2, g2}, s);
-      }
-    }
+    for (int l = 0; l < L; ++l)
+      for (int st = 0; st < kStages; ++st) layer_stage<T>(e, st, l, k, B, s);
 
     ReadoutArgs ro{};
     ro.h = e.h; ro.B = B; ro.H = H; ro.M = M; ro.off = e.off; ro.d = d; ro.A = e.A;
@@ -443,7 +478,7 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
     if (variant == PHYAI_VARIANT_PI0) { ro.mode = NORM_RMS; ro.mul = e.final_norm; ro.shift = nullptr; }
     else if (variant == PHYAI_VARIANT_PI05) {
       ro.mode = NORM_RMS;
-      ro.mul = e.modtab + ((int64_t)k * S + 2 * L) * 2 * d;
+      ro.mul = e.modtab + ((int64_t)k * (2 * L + 1) + 2 * L) * 2 * d;
       ro.shift = ro.mul + d;
     } else {
       ro.mode = NORM_LN;
@@ -827,6 +862,7 @@ int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len
     for (int b = 0; b < batch; ++b) hd.prefix_len[b] = prefix_len[b];
     set_call_desc(hd, e->desc, s);
     HIPC(hipGetLastError());
+    e->last_batch = batch;
     if (bk) {
       HIPC(hipGraphLaunch(bk->exec, s));
     } else {
@@ -852,6 +888,22 @@ int phyai_fp8_to_bf16(const uint8_t* codes, uint16_t* out, int64_t n, void* stre
     if (n == 0) return;
     if (!codes || !out) fail(PHYAI_EINVAL, "NULL argument");
     fp8_to_bf16(codes, out, n, static_cast<hipStream_t>(stream));
+    HIPC(hipGetLastError());
+  });
+}
+
+int phyai_profile_stage(phyai_expert* e, int32_t stage, int32_t reps, void* stream) {
+  return run_guarded([&] {
+    if (!e) fail(PHYAI_EINVAL, "NULL handle");
+    if (stage < 0 || stage >= kStages) fail(PHYAI_EINVAL, "stage out of range 0..6");
+    if (reps < 1) fail(PHYAI_EINVAL, "reps < 1");
+    if (e->last_batch < 1) fail(PHYAI_EINVAL, "call phyai_denoise first (the stage reads its inputs)");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    for (int r = 0; r < reps; ++r)
+      for (int l = 0; l < e->L; ++l) {
+        if (e->f32) layer_stage<float>(*e, stage, l, 0, e->last_batch, s);
+        else layer_stage<bf16_t>(*e, stage, l, 0, e->last_batch, s);
+      }
     HIPC(hipGetLastError());
   });
 }

@@ -159,27 +159,21 @@ def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
 
 def e4m3fn_encode(v: np.ndarray) -> np.ndarray:
     """Encode float values as OCP e4m3fn codes: saturate to +-448, then round
-    to nearest with ties to even.  (No NaN/inf inputs.)"""
-    v = np.asarray(v, dtype=np.float64)
+    to nearest with ties to even.  (No NaN/inf inputs.)
+
+    With a = |v| in the binade [2^E, 2^(E+1)) (E clamped below at -6, where
+    the subnormals share the quantum of the lowest binade), the representable
+    values are n * 2^(E-3); n = rint(a / 2^(E-3)) lies in [8, 16] for normals
+    (n = 16 is the next binade) and in [0, 8] below 2^-6, and in every case
+    the code is 8*E + 48 + n."""
+    v = np.asarray(v, dtype=np.float32)
     sign = np.signbit(v)
-    a = np.minimum(np.abs(v), 448.0)
-    # Exponent of the binade; subnormals share the quantum of the lowest binade.
-    with np.errstate(divide="ignore"):
-        e = np.floor(np.log2(np.where(a > 0, a, 1.0)))
-    e = np.clip(e, -6, 8)
-    q = np.exp2(e - 3)                         # spacing of representable values
-    n = np.round(a / q)                        # numpy rounds half to even
-    val = np.minimum(n * q, 448.0)
-    # value -> code
-    code = np.zeros(v.shape, dtype=np.int64)
-    sub = val < 2.0 ** -6
-    code[sub] = np.round(val[sub] / 2.0 ** -9).astype(np.int64)
-    nrm = ~sub
-    en = np.floor(np.log2(val[nrm]))
-    mant = np.round((val[nrm] / np.exp2(en) - 1.0) * 8.0).astype(np.int64)
-    code[nrm] = ((en.astype(np.int64) + 7) << 3) | mant
-    code = code | (sign.astype(np.int64) << 7)
-    return code.astype(np.uint8)
+    a = np.minimum(np.abs(v), np.float32(448.0))
+    _, e = np.frexp(a)                                  # a = m * 2^e, m in [0.5, 1)
+    E = np.maximum(np.where(a > 0, e - 1, -6), -6).astype(np.int32)
+    n = np.rint(np.ldexp(a, 3 - E)).astype(np.int32)   # exact scaling by a power of two
+    code = 8 * E + 48 + n
+    return (code | (sign.astype(np.int32) << 7)).astype(np.uint8)
 
 
 def quantize_fp8_per_column(w: np.ndarray):
@@ -191,7 +185,7 @@ def quantize_fp8_per_column(w: np.ndarray):
     w = np.asarray(w, dtype=np.float32)
     amax = np.abs(w).max(axis=0).astype(np.float32)
     scale = np.where(amax > 0, amax / np.float32(448.0), np.float32(1.0)).astype(np.float32)
-    codes = e4m3fn_encode(w.astype(np.float64) / scale.astype(np.float64)[None, :])
+    codes = e4m3fn_encode(w / scale[None, :])
     return codes, scale
 
 
