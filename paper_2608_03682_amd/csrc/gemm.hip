@@ -184,5 +184,7 @@ void gemm_geglu_bf16(const GemmArgs& g, const EpiGeglu<bf16_t>& e, hipStream_t s
 void gemm_geglu_f32(const GemmArgs& g, const EpiGeglu<float>& e, hipStream_t s) { launch(g, e, s); }
 void gemm_qkv_bf16(const GemmArgs& g, const EpiQkv<bf16_t>& e, hipStream_t s) { launch(g, e, s); }
 void gemm_qkv_f32(const GemmArgs& g, const EpiQkv<float>& e, hipStream_t s) { launch(g, e, s); }
+void gemm_kv_bf16(const GemmArgs& g, const EpiKV<bf16_t>& e, hipStream_t s) { launch(g, e, s); }
+void gemm_kv_f32(const GemmArgs& g, const EpiKV<float>& e, hipStream_t s) { launch(g, e, s); }
 
 }  // namespace phyai

@@ -106,35 +106,69 @@ struct EpiGeglu {
 // Fused QKV.  Heads are ordered [n_q query | n_kv key | n_kv value], each
 // head_dim wide; head h owns pair tiles h*D/32 .. (h+1)*D/32-1, and pair tile
 // j of a head holds dimension i = 16j+c (half 0) and i + D/2 (half 1), the
-// two halves that RoPE rotates together.
+// two halves that RoPE rotates together.  q goes to [R][nq*D]; k and v go
+// into the layer's key range (K [b][kvh][key][D], V transposed
+// [b][kvh][D][key]) at key = (prefix_len[b] if keys_after_prefix) + token.
 template <typename OutT>
 struct EpiQkv {
-  OutT* q; OutT* k; OutT* v;
+  OutT* q; OutT* kall; OutT* vt;
   int D, nq, nkv;
   int rope;
   int M;                    // suffix tokens per request
+  int ldk;                  // key capacity of a key range
+  int keys_after_prefix;
   const float* inv_freq;    // [D/2]: base^(-2i/D)
   const CallDesc* desc;     // positions start at prefix_len[b]
   __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
     const int tiles = D / 32;
     const int head = p / tiles;
     const int i = 16 * (p % tiles) + c;
+    const int b = r / M, tok = r % M;
+    const int plen = desc->prefix_len[b];
     if (rope && head < nq + nkv) {
-      const int b = r / M;
-      const float pos = (float)(desc->prefix_len[b] + (r % M));
+      const float pos = (float)(plen + tok);
       float s, co;
       sincosf(pos * inv_freq[i], &s, &co);
       const float x1 = a0, x2 = a1;
       a0 = x1 * co - x2 * s;
       a1 = x2 * co + x1 * s;
     }
-    OutT* dst;
-    int64_t base;
-    if (head < nq) { dst = q; base = (int64_t)r * nq * D + head * D; }
-    else if (head < nq + nkv) { dst = k; base = (int64_t)r * nkv * D + (head - nq) * D; }
-    else { dst = v; base = (int64_t)r * nkv * D + (head - nq - nkv) * D; }
-    ActIO<OutT>::store(dst + base + i, a0);
-    ActIO<OutT>::store(dst + base + i + D / 2, a1);
+    if (head < nq) {
+      OutT* dst = q + (int64_t)r * nq * D + head * D + i;
+      ActIO<OutT>::store(dst, a0);
+      ActIO<OutT>::store(dst + D / 2, a1);
+      return;
+    }
+    const int key = (keys_after_prefix ? plen : 0) + tok;
+    if (head < nq + nkv) {
+      OutT* dst = kall + (((int64_t)b * nkv + (head - nq)) * ldk + key) * D + i;
+      ActIO<OutT>::store(dst, a0);
+      ActIO<OutT>::store(dst + D / 2, a1);
+    } else {
+      OutT* dst = vt + (((int64_t)b * nkv + (head - nq - nkv)) * D + i) * ldk + key;
+      ActIO<OutT>::store(dst, a0);
+      ActIO<OutT>::store(dst + (int64_t)(D / 2) * ldk, a1);
+    }
+  }
+};
+
+// K|V projection of feature rows r = b*P + key (identity packing): columns
+// [0, nkv*D) are K heads, [nkv*D, 2*nkv*D) V heads, stored like EpiQkv's k/v.
+template <typename OutT>
+struct EpiKV {
+  OutT* kall; OutT* vt;
+  int D, nkv, P, ldk;
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    const int b = r / P, key = r % P;
+    float v[2] = {a0, a1};
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int col = 32 * p + 16 * hf + c;
+      const int kv = col / (nkv * D), rem = col % (nkv * D);
+      const int h = rem / D, i = rem % D;
+      if (kv == 0) ActIO<OutT>::store(kall + (((int64_t)b * nkv + h) * ldk + key) * D + i, v[hf]);
+      else ActIO<OutT>::store(vt + (((int64_t)b * nkv + h) * D + i) * ldk + key, v[hf]);
+    }
   }
 };
 
@@ -145,26 +179,28 @@ void gemm_geglu_bf16(const GemmArgs&, const EpiGeglu<bf16_t>&, hipStream_t);
 void gemm_geglu_f32(const GemmArgs&, const EpiGeglu<float>&, hipStream_t);
 void gemm_qkv_bf16(const GemmArgs&, const EpiQkv<bf16_t>&, hipStream_t);
 void gemm_qkv_f32(const GemmArgs&, const EpiQkv<float>&, hipStream_t);
+void gemm_kv_bf16(const GemmArgs&, const EpiKV<bf16_t>&, hipStream_t);
+void gemm_kv_f32(const GemmArgs&, const EpiKV<float>&, hipStream_t);
 
 // ---------------------------------------------------------------------------
-// Attention of suffix queries over two key segments:
-//   segment 1 (prefix K/V cache, or projected DiT features): per request,
-//     rows 0 .. len1(b)-1 at seg1_k/v + b*seg1_bstride + row*seg1_ld;
-//   segment 2 (the suffix tokens' own K/V): rows b*M .. b*M+len2-1 of sk/sv.
-// Query rows of (request b, kv head h) are token*G + g for the G = nq/nkv
-// query heads that share kv head h.
+// Attention of suffix queries over one key range per (request, kv head):
+// K [key][D] and V^T [D][key] at grp * ldk * D (grp = b * nkv + kvh).  The
+// range holds n_keys(b) = (keys_from_prefix ? prefix_len[b] : 0) + n_suffix
+// keys.  Query rows of (b, kv head h) are token*G + g for the G = nq/nkv
+// query heads sharing kv head h.  mask_mode 1 is the pi0 block mask: the
+// state token (suffix token 0, key prefix_len[b]) sees the prefix and
+// itself only.
 // ---------------------------------------------------------------------------
 struct AttnArgs {
   const void* q; int ldq;
-  const void* const* seg1_ind;  // if set, segment-1 base = *seg1_ind (+ offsets)
-  const void* seg1_k; const void* seg1_v;
-  int64_t seg1_k_off, seg1_v_off;
-  int64_t seg1_bstride; int seg1_ld;
-  int use_seg1;
-  const void* sk; const void* sv; int ld2; int len2;
-  int mask_mode;            // 0: all keys; 1: block mask (suffix token 0 is the state token)
+  const void* K; const void* Vt;
+  int ldk;
+  int keys_from_prefix, n_suffix;
+  int mask_mode;
   void* out; int ldo;
-  float* part;              // split-KV partials (n_split > 1)
+  float* part;              // split partials (n_split > 1)
+  int64_t part_ml_off;      // set by the launcher
+  int* counters;            // one per (group, row tile), zero between launches
   int n_split;
   const CallDesc* desc;
   int B, M, nq, nkv, D;
@@ -174,6 +210,19 @@ struct AttnArgs {
 void attention_bf16(const AttnArgs&, hipStream_t);
 void attention_f32(const AttnArgs&, hipStream_t);
 int64_t attention_partial_floats(int B, int M, int nq, int nkv, int D, int n_split);
+int64_t attention_counters(int B, int M, int nq, int nkv);
+
+// Copy the caller's prefix K and transpose its V ([L][2][B][P][nkv*D]) into
+// the per-layer key ranges (layer l at K/Vt + l * layer_stride).
+struct RelayoutArgs {
+  const CallDesc* desc;
+  void* K; void* Vt;
+  int64_t layer_stride;
+  int ldk, L, B, P, nkv, D;
+  int n_suffix;             // suffix keys that follow the prefix (zero-fill starts after them)
+};
+void prefix_relayout_bf16(const RelayoutArgs&, hipStream_t);
+void prefix_relayout_f32(const RelayoutArgs&, hipStream_t);
 
 // ---------------------------------------------------------------------------
 // Row kernels

@@ -101,8 +101,13 @@ struct phyai_expert {
   float* inv_freq = nullptr;
   // working buffers
   float *x = nullptr, *h = nullptr, *e_state = nullptr, *part = nullptr;
-  void *n = nullptr, *abuf = nullptr, *zbuf = nullptr, *q = nullptr, *ks = nullptr, *vs = nullptr;
-  void *o = nullptr, *g = nullptr, *cross = nullptr;
+  void *n = nullptr, *abuf = nullptr, *zbuf = nullptr, *q = nullptr;
+  void *o = nullptr, *g = nullptr;
+  // per-layer key ranges: K [L][Bmax][nkv][ldk][D], V transposed [L][Bmax][nkv][D][ldk]
+  void *kall = nullptr, *vt = nullptr;
+  int ldk = 0;
+  int64_t kv_layer = 0;     // elements per layer
+  int* counters = nullptr;
   // two-term activations (hi + lo bf16) for the GEMMs fed by a norm or by GeGLU
   bool split_act = false;
   void *n_lo = nullptr, *g_lo = nullptr;
@@ -270,6 +275,10 @@ void gemm_geglu(const GemmArgs& g, const EpiGeglu<bf16_t>& e, hipStream_t s) { g
 void gemm_geglu(const GemmArgs& g, const EpiGeglu<float>& e, hipStream_t s) { gemm_geglu_f32(g, e, s); }
 void gemm_qkv(const GemmArgs& g, const EpiQkv<bf16_t>& e, hipStream_t s) { gemm_qkv_bf16(g, e, s); }
 void gemm_qkv(const GemmArgs& g, const EpiQkv<float>& e, hipStream_t s) { gemm_qkv_f32(g, e, s); }
+void gemm_kv(const GemmArgs& g, const EpiKV<bf16_t>& e, hipStream_t s) { gemm_kv_bf16(g, e, s); }
+void gemm_kv(const GemmArgs& g, const EpiKV<float>& e, hipStream_t s) { gemm_kv_f32(g, e, s); }
+void prefix_relayout(const RelayoutArgs& r, bf16_t*, hipStream_t s) { prefix_relayout_bf16(r, s); }
+void prefix_relayout(const RelayoutArgs& r, float*, hipStream_t s) { prefix_relayout_f32(r, s); }
 void norm_rows(const float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode, const float* mul,
                const float* sh, hipStream_t s) { norm_rows_bf16(h, n, n_lo, R, d, eps, mode, mul, sh, s); }
 void norm_rows(const float* h, float* n, float*, int R, int d, float eps, int mode, const float* mul, const float* sh,
@@ -300,9 +309,9 @@ template <typename T> EpiStore<T> store_epi(T* out, int ldo, const float* bias, 
 
 // split of the keys across blocks so that small batches still fill the chip
 int attn_splits(int B, int rows, int nkv, int keys) {
-  const int base = ((rows + 63) / 64) * B * nkv;
-  int s = (128 + base - 1) / base;
-  const int cap = keys / 64 > 1 ? keys / 64 : 1;
+  const int base = ((rows + 127) / 128) * B * nkv;     // blocks without a split
+  int s = (256 + base - 1) / base;
+  const int cap = (keys + 127) / 128;                   // keep >= two 64-key tiles per split
   if (s > cap) s = cap;
   return s < 1 ? 1 : s;
 }
@@ -320,8 +329,8 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   const int R = B * M;
   T* n = static_cast<T*>(e.n);
   T* q = static_cast<T*>(e.q);
-  T* ks = static_cast<T*>(e.ks);
-  T* vs = static_cast<T*>(e.vs);
+  T* kl = static_cast<T*>(e.kall) + (int64_t)l * e.kv_layer;
+  T* vl = static_cast<T*>(e.vt) + (int64_t)l * e.kv_layer;
   T* o = static_cast<T*>(e.o);
   T* g = static_cast<T*>(e.g);
   T* n_lo = static_cast<T*>(e.n_lo);
@@ -331,8 +340,15 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   const int S = 2 * L + 1;   // pi0.5 norm sites
   const LayerW& w = e.layers[l];
   const float inv_sqrt_d = 1.0f / std::sqrt((float)D);
-  const int keys_self = (variant == PHYAI_VARIANT_DIT) ? M : e.P + M;
   const int rows = M * (e.nq / e.nkv);
+  AttnArgs at{};
+  at.q = q; at.ldq = e.qd;
+  at.K = kl; at.Vt = vl; at.ldk = e.ldk;
+  at.out = o; at.ldo = e.qd;
+  at.part = e.part; at.counters = e.counters;
+  at.desc = e.desc;
+  at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
+  at.scale = inv_sqrt_d;
 
   if (variant != PHYAI_VARIANT_DIT) {
     const float* mul1 = w.attn_norm;
@@ -348,27 +364,15 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
     switch (stage) {
       case ST_NORM1: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul1, sh1, s); break;
       case ST_QKV: {
-        EpiQkv<T> eq{q, ks, vs, D, e.nq, e.nkv, e.c.rope, M, e.inv_freq, e.desc};
+        EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, e.c.rope, M, e.ldk, 1, e.inv_freq, e.desc};
         gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
         break;
       }
       case ST_ATTN: {
-        AttnArgs at{};
-        at.q = q; at.ldq = e.qd;
-        at.use_seg1 = 1;
-        at.seg1_ind = reinterpret_cast<const void* const*>(&e.desc->prefix);
-        const int64_t blk = (int64_t)B * e.P * e.Wpre;
-        at.seg1_k_off = ((int64_t)l * 2 + 0) * blk;
-        at.seg1_v_off = ((int64_t)l * 2 + 1) * blk;
-        at.seg1_bstride = (int64_t)e.P * e.Wpre;
-        at.seg1_ld = e.Wpre;
-        at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = M;
+        at.keys_from_prefix = 1;
+        at.n_suffix = M;
         at.mask_mode = e.c.state_token ? 1 : 0;
-        at.out = o; at.ldo = e.qd;
-        at.part = e.part; at.n_split = e.f32 ? 1 : attn_splits(B, rows, e.nkv, keys_self);
-        at.desc = e.desc;
-        at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
-        at.scale = inv_sqrt_d;
+        at.n_split = e.f32 ? 1 : attn_splits(B, rows, e.nkv, e.P + M);
         if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
         break;
       }
@@ -389,32 +393,16 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   switch (stage) {
     case ST_NORM1: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc1, sh1, s); break;
     case ST_QKV: {
-      EpiQkv<T> eq{q, ks, vs, D, e.nq, e.nkv, 0, M, e.inv_freq, e.desc};
+      // cross blocks project only Q here (their K/V come from the features)
+      EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, 0, M, e.ldk, 0, e.inv_freq, e.desc};
       gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
       break;
     }
     case ST_ATTN: {
-      AttnArgs at{};
-      at.q = q; at.ldq = e.qd;
-      if (cross) {
-        const T* cb = static_cast<const T*>(e.cross) + (int64_t)(l / 2) * e.Bmax * e.P * 2 * d;
-        at.use_seg1 = 1;
-        at.seg1_k = cb;
-        at.seg1_v = cb + d;
-        at.seg1_bstride = (int64_t)e.P * 2 * d;
-        at.seg1_ld = 2 * d;
-        at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = 0;
-      } else {
-        at.use_seg1 = 0;
-        at.sk = ks; at.sv = vs; at.ld2 = e.kd; at.len2 = M;
-      }
+      at.keys_from_prefix = cross ? 1 : 0;
+      at.n_suffix = cross ? 0 : M;
       at.mask_mode = 0;
-      at.out = o; at.ldo = e.qd;
-      at.part = e.part;
-      at.n_split = e.f32 ? 1 : attn_splits(B, rows, e.nkv, cross ? e.P : keys_self);
-      at.desc = e.desc;
-      at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
-      at.scale = inv_sqrt_d;
+      at.n_split = e.f32 ? 1 : attn_splits(B, rows, e.nkv, cross ? e.P : M);
       if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
       break;
     }
@@ -435,15 +423,20 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
   copy_noise_to_state(e.desc, e.x, (int64_t)B * H * e.A, s);
   if (e.c.state_token) embed_state(e.desc, e.state_w, e.state_b, e.e_state, B, e.A, d, s);
   if (variant == PHYAI_VARIANT_DIT) {
+    // request-local cross-attention K/V: project the VLM features once per call
     for (int l = 0; l < L; l += 2) {
       GemmArgs ga = gargs(e.layers[l].kv_cross, nullptr, e.c.d_feat, B * e.P);
       ga.A_ind = reinterpret_cast<const void* const*>(&e.desc->prefix);
       ga.a_off = 0;
       ga.rows_per_req = e.P;
       ga.desc = e.desc;
-      T* dst = static_cast<T*>(e.cross) + (int64_t)(l / 2) * e.Bmax * e.P * 2 * d;
-      gemm_store(ga, store_epi<T>(dst, 2 * d, nullptr, nullptr, ACT_NONE), s);
+      EpiKV<T> ek{static_cast<T*>(e.kall) + (int64_t)l * e.kv_layer, static_cast<T*>(e.vt) + (int64_t)l * e.kv_layer,
+                  e.D, e.nkv, e.P, e.ldk};
+      gemm_kv(ga, ek, s);
     }
+  } else if (e.P > 0) {
+    RelayoutArgs ra{e.desc, e.kall, e.vt, e.kv_layer, e.ldk, L, B, e.P, e.nkv, e.D, M};
+    prefix_relayout(ra, static_cast<T*>(nullptr), s);
   }
 
   for (int k = 0; k < K; ++k) {
@@ -693,9 +686,16 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
   e->abuf = e->mem.alloc(Bm * e->H * d * ab);
   e->zbuf = e->mem.alloc(Bm * e->H * d * ab);
   e->q = e->mem.alloc(Bm * M * e->qd * ab);
-  e->ks = e->mem.alloc(Bm * M * e->kd * ab);
-  e->vs = e->mem.alloc(Bm * M * e->kd * ab);
   e->o = e->mem.alloc(Bm * M * e->qd * ab);
+  {
+    const int keys = c.variant == PHYAI_VARIANT_DIT ? std::max(e->P, e->M) : e->P + e->M;
+    e->ldk = (keys + 63) / 64 * 64;
+    e->kv_layer = Bm * e->nkv * (int64_t)e->ldk * D;
+    e->kall = e->mem.alloc(L * e->kv_layer * ab);
+    e->vt = e->mem.alloc(L * e->kv_layer * ab);
+    HIPC(hipMemsetAsync(e->kall, 0, L * e->kv_layer * ab, s));
+    HIPC(hipMemsetAsync(e->vt, 0, L * e->kv_layer * ab, s));
+  }
   e->g = e->mem.alloc(Bm * M * F * ab);
   // pi0.5's adaRMS path amplifies the bf16 rounding of the normalised
   // activations and of the GeGLU output; those GEMM operands carry a second
@@ -705,7 +705,6 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     e->n_lo = e->mem.alloc(Bm * M * d * ab);
     e->g_lo = e->mem.alloc(Bm * M * F * ab);
   }
-  if (c.variant == PHYAI_VARIANT_DIT) e->cross = e->mem.alloc((int64_t)((L + 1) / 2) * Bm * e->P * 2 * d * ab);
   int64_t part = 0;
   if (!e->f32) {
     const int keys_main = c.variant == PHYAI_VARIANT_DIT ? e->M : e->P + e->M;
@@ -720,6 +719,12 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     }
   }
   e->part = e->mem.alloc_n<float>(part > 0 ? part : 4);
+  {
+    const int64_t nc = attention_counters(e->Bmax, e->M, e->nq, e->nkv);
+    e->counters = e->mem.alloc_n<int>(nc);
+    HIPC(hipMemsetAsync(e->counters, 0, nc * sizeof(int), s));
+    HIPC(hipStreamSynchronize(s));
+  }
   e->desc = static_cast<CallDesc*>(e->mem.alloc(sizeof(CallDesc)));
   // tables
   const int64_t Km = e->Kmax;
