@@ -157,11 +157,158 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, Epi epi) {
   epi(row, p, c, s0, s1);
 }
 
+// ---------------------------------------------------------------------------
+// Tiled GEMM for many rows (rollout batches): 128 x 128 output tiles, 4 waves
+// in a 2 x 2 arrangement of 64 x 64.  Per k-block of 64 the activation tile
+// (128 x 64 bf16, 16-byte chunks XOR-swizzled against bank conflicts) and
+// the block's 8 packed weight fragments are copied into LDS by direct
+// global->LDS loads, double-buffered; fp8 codes are expanded to bf16 after
+// the LDS read.  A grid-stride loop walks the output tiles.
+// ---------------------------------------------------------------------------
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ void dma16(const void* src, lds_void_t* lds) {
+  const uint32_t m = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(lds));
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" :: "s"(m), "v"(src) : "memory", "m0");
+}
+#define GEMM_WAIT_VMCNT(n) __builtin_amdgcn_s_waitcnt(((n) & 15) | (((n) >> 4) << 14) | 0x70 | 0xF00)
+__device__ __forceinline__ void bare_barrier() {
+  __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
+  __builtin_amdgcn_s_barrier();
+}
+__device__ __forceinline__ int aswz(int row) { return (row >> 1) & 7; }
+
+template <bool FP8>
+struct TiledSmem {
+  bf16_t A[128 * 64];
+  uint8_t B[8 * (FP8 ? 1024 : 2048)];
+};
+
+template <class Epi, bool FP8>
+__global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi) {
+  __shared__ __attribute__((aligned(1024))) TiledSmem<FP8> s0;
+  __shared__ __attribute__((aligned(1024))) TiledSmem<FP8> s1;
+  constexpr int FB = FP8 ? 1024 : 2048;          // bytes per weight fragment
+  constexpr int NB = 8 * FB / 1024 / 4;          // weight DMA blocks per wave per k-block
+  constexpr int NOPS = 4 + NB;                   // DMA ops per thread per k-block
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lc = lane % 16, lg = lane / 16;
+  const int nkb = g.K / 64;
+  const int mtiles = (g.R + 127) / 128, ntiles = g.NPT / 4;
+  const bf16_t* A = static_cast<const bf16_t*>(g.A);
+  const uint8_t* W = static_cast<const uint8_t*>(g.W);
+
+  // per-thread A source offsets (row within tile, swizzled chunk) for loads i = 0..3
+  int arow[4], acol[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int pos = (4 * i + wave) * 64 + lane;
+    arow[i] = pos / 8;
+    acol[i] = 8 * ((pos % 8) ^ aswz(pos / 8));
+  }
+
+  for (int tile = blockIdx.x; tile < mtiles * ntiles; tile += gridDim.x) {
+    const int mt0 = (tile % mtiles) * 128;
+    const int pt0 = (tile / mtiles) * 4;
+    const bf16_t* arp[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) arp[i] = A + (int64_t)min(mt0 + arow[i], g.R - 1) * g.lda + acol[i];
+
+    auto issue = [&](TiledSmem<FP8>& S, int kb) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) dma16(arp[i] + kb * 64, (lds_void_t*)(S.A + (4 * i + wv) * 512));
+#pragma unroll
+      for (int i = 0; i < NB; ++i) {
+        const int blk = 4 * i + wv;                  // 1 KiB block of the k-block's weights
+        const int f = blk / (FB / 1024), part = blk % (FB / 1024);
+        const int p = pt0 + f / 2, hf = f % 2;
+        const uint8_t* src = W + ((int64_t)(p * nkb + kb) * 2 + hf) * FB + part * 1024 + lane * 16;
+        dma16(src, (lds_void_t*)(S.B + blk * 1024));
+      }
+    };
+
+    f32x4 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+    auto compute = [&](const TiledSmem<FP8>& S) {
+      bf16x8 af[4][2];
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int row = 64 * wm + 16 * mt + lc;
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+          af[mt][st] = *reinterpret_cast<const bf16x8*>(S.A + row * 64 + 8 * ((4 * st + lg) ^ aswz(row)));
+      }
+      bf16x8 bfr[4][2];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        const int f = (2 * wn + nt / 2) * 2 + nt % 2;
+        if (FP8) {
+          const uint4 v = *reinterpret_cast<const uint4*>(S.B + f * FB + lane * 16);
+          bfr[nt][0] = fp8x8_to_bf16x8(v.x, v.y);
+          bfr[nt][1] = fp8x8_to_bf16x8(v.z, v.w);
+        } else {
+          const uint4* src = reinterpret_cast<const uint4*>(S.B + f * FB + lane * 32);
+          bfr[nt][0] = as_bf16x8(src[0]);
+          bfr[nt][1] = as_bf16x8(src[1]);
+        }
+      }
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma16x16x32(af[mt][st], bfr[nt][st], acc[mt][nt]);
+    };
+
+    issue(s0, 0);
+    for (int kb = 0; kb < nkb; kb += 2) {
+      if (kb + 1 < nkb) { issue(s1, kb + 1); GEMM_WAIT_VMCNT(NOPS); } else { GEMM_WAIT_VMCNT(0); }
+      bare_barrier();
+      compute(s0);
+      bare_barrier();
+      if (kb + 1 >= nkb) break;
+      if (kb + 2 < nkb) { issue(s0, kb + 2); GEMM_WAIT_VMCNT(NOPS); } else { GEMM_WAIT_VMCNT(0); }
+      bare_barrier();
+      compute(s1);
+      bare_barrier();
+    }
+
+    // epilogue: wave (wm, wn) holds rows mt0+64wm.., pair tiles pt0+2wn, +1
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) {
+      const int p = pt0 + 2 * wn + pp;
+      float s0c = 1.f, s1c = 1.f;
+      if (g.scale) {
+        s0c = g.scale[32 * p + lc];
+        s1c = g.scale[32 * p + 16 + lc];
+      }
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = mt0 + 64 * wm + 16 * mt + 4 * lg + v;
+          if (row < g.R) epi(row, p, lc, acc[mt][2 * pp][v] * s0c, acc[mt][2 * pp + 1][v] * s1c);
+        }
+    }
+  }
+}
+
 template <class Epi>
 void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
   if (g.kind == W_F32) {
     dim3 grid(g.NPT, (g.R + 15) / 16);
     hipLaunchKernelGGL(gemm_f32_kernel<Epi>, grid, dim3(256), 0, s, g, epi);
+  } else if (g.R >= 256 && g.A_lo == nullptr && g.A_ind == nullptr && g.rows_per_req == 0 && g.NPT % 4 == 0) {
+    const int tiles = ((g.R + 127) / 128) * (g.NPT / 4);
+    dim3 grid(tiles < 512 ? tiles : 512);
+    if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_tiled_kernel<Epi, true>), grid, dim3(256), 0, s, g, epi);
+    else hipLaunchKernelGGL((gemm_tiled_kernel<Epi, false>), grid, dim3(256), 0, s, g, epi);
   } else {
     dim3 grid((g.NPT + kNP - 1) / kNP, (g.R + 16 * kMT - 1) / (16 * kMT));
     const bool split = g.A_lo != nullptr;
