@@ -14,21 +14,26 @@ namespace phyai {
 namespace {
 
 constexpr int kMT = 4;           // 16-row MFMA tiles per block (64 rows)
-constexpr int kNP = 2;           // pair tiles per block (64 columns)
-constexpr int kNT = 2 * kNP;     // 16-column MFMA tiles per block
 
-// One block = 4 waves computing a 64 x 64 output tile; the K range is split
-// between the 4 waves and their partial sums are added through LDS.
-template <class Epi, bool FP8, bool SPLIT>
+// Small-row GEMM (batch-1 style): one block = 4 waves computing 64 rows x
+// 32*NP columns; the block's K range is split between the 4 waves, whose
+// partial sums are added through LDS.  With g.split_out set, blockIdx.z
+// selects a slice of K and the block writes its raw partial sums to
+// split_out[z] (fp32 [R][32*NPT]) instead of running the epilogue; the
+// consumer adds the slices in a fixed order.
+template <class Epi, bool FP8, bool SPLIT, int NP>
 __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
-  __shared__ float red[4][kMT * kNT * 4][kWave];
+  constexpr int NT = 2 * NP;
+  __shared__ float red[4][kMT * NT * 4][kWave];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int pt0 = blockIdx.x * kNP;
+  const int pt0 = blockIdx.x * NP;
   const int m0 = blockIdx.y * 16 * kMT;
   const bf16_t* A = g.A_ind ? static_cast<const bf16_t*>(*g.A_ind) + g.a_off
                             : static_cast<const bf16_t*>(g.A);
   const int nkb = g.K / 64;
-  const int kb0 = wave * nkb / 4, kb1 = (wave + 1) * nkb / 4;
+  const int nz = gridDim.z, z = blockIdx.z;
+  const int zb0 = z * nkb / nz, zb1 = (z + 1) * nkb / nz;
+  const int kb0 = zb0 + wave * (zb1 - zb0) / 4, kb1 = zb0 + (wave + 1) * (zb1 - zb0) / 4;
   const int arow = lane % 16, akg = lane / 16;
 
   // rows this lane loads A for, with validity
@@ -48,16 +53,16 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
     alp[mt] = SPLIT ? static_cast<const bf16_t*>(g.A_lo) + (int64_t)(ok ? row : 0) * g.lda + akg * 8 : nullptr;
   }
 
-  f32x4 acc[kMT][kNT];
+  f32x4 acc[kMT][NT];
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
-    for (int t = 0; t < kNT; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int t = 0; t < NT; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   for (int kb = kb0; kb < kb1; ++kb) {
-    bf16x8 b[kNT][2];
+    bf16x8 b[NT][2];
 #pragma unroll
-    for (int t = 0; t < kNT; ++t) {
+    for (int t = 0; t < NT; ++t) {
       const int p = pt0 + t / 2, hf = t % 2;
       const int64_t frag = ((int64_t)(p * nkb + kb) * 2 + hf) * kWave + lane;
       if (p >= g.NPT) {
@@ -92,7 +97,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
 #pragma unroll
       for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
-        for (int t = 0; t < kNT; ++t) {
+        for (int t = 0; t < NT; ++t) {
           acc[mt][t] = mfma16x16x32(a[mt][s], b[t][s], acc[mt][t]);
           if (SPLIT) acc[mt][t] = mfma16x16x32(al[mt][s], b[t][s], acc[mt][t]);
         }
@@ -101,16 +106,18 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
-    for (int t = 0; t < kNT; ++t)
+    for (int t = 0; t < NT; ++t)
 #pragma unroll
-      for (int v = 0; v < 4; ++v) red[wave][(mt * kNT + t) * 4 + v][lane] = acc[mt][t][v];
+      for (int v = 0; v < 4; ++v) red[wave][(mt * NT + t) * 4 + v][lane] = acc[mt][t][v];
   __syncthreads();
 
   // wave w finishes row tile w
   const int mt = wave;
   const int c = lane % 16;
+  const int N = 32 * g.NPT;
+  float* sp = g.split_out ? g.split_out + (int64_t)z * g.split_stride : nullptr;
 #pragma unroll
-  for (int pp = 0; pp < kNP; ++pp) {
+  for (int pp = 0; pp < NP; ++pp) {
     const int p = pt0 + pp;
     if (p >= g.NPT) break;
 #pragma unroll
@@ -119,14 +126,21 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
       float s0 = 0.f, s1 = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        s0 += red[w][(mt * kNT + 2 * pp) * 4 + v][lane];
-        s1 += red[w][(mt * kNT + 2 * pp + 1) * 4 + v][lane];
+        s0 += red[w][(mt * NT + 2 * pp) * 4 + v][lane];
+        s1 += red[w][(mt * NT + 2 * pp + 1) * 4 + v][lane];
       }
       if (g.scale) {
         s0 *= g.scale[32 * p + c];
         s1 *= g.scale[32 * p + 16 + c];
       }
-      if (row < g.R) epi(row, p, c, s0, s1);
+      if (row < g.R) {
+        if (sp) {
+          sp[(int64_t)row * N + 32 * p + c] = s0;
+          sp[(int64_t)row * N + 32 * p + 16 + c] = s1;
+        } else {
+          epi(row, p, c, s0, s1);
+        }
+      }
     }
   }
 }
@@ -212,13 +226,13 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
   for (int tile = blockIdx.x; tile < mtiles * ntiles; tile += gridDim.x) {
     const int mt0 = (tile % mtiles) * 128;
     const int pt0 = (tile / mtiles) * 4;
-    const bf16_t* arp[4];
+    int aoff[4];       // element offsets of this thread's A chunks (rows clamped into range)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) arp[i] = A + (int64_t)min(mt0 + arow[i], g.R - 1) * g.lda + acol[i];
+    for (int i = 0; i < 4; ++i) aoff[i] = min(mt0 + arow[i], g.R - 1) * g.lda + acol[i];
 
     auto issue = [&](TiledSmem<FP8>& S, int kb) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) dma16(arp[i] + kb * 64, (lds_void_t*)(S.A + (4 * i + wv) * 512));
+      for (int i = 0; i < 4; ++i) dma16(A + aoff[i] + kb * 64, (lds_void_t*)(S.A + (4 * i + wv) * 512));
 #pragma unroll
       for (int i = 0; i < NB; ++i) {
         const int blk = 4 * i + wv;                  // 1 KiB block of the k-block's weights
@@ -299,6 +313,20 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
   }
 }
 
+}  // namespace
+
+int gemm_split_k(int R, int NPT, int K) {
+  if (R >= 256) return 1;                     // the tiled kernel has enough blocks
+  const int blocks = NPT * ((R + 63) / 64);
+  int s = (256 + blocks - 1) / blocks;
+  const int cap = (K / 64) / 4;               // keep >= one k-block per wave
+  if (s > cap) s = cap;
+  if (s > 8) s = 8;
+  return s < 1 ? 1 : s;
+}
+
+namespace {
+
 template <class Epi>
 void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
   if (g.kind == W_F32) {
@@ -310,14 +338,17 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
     if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_tiled_kernel<Epi, true>), grid, dim3(256), 0, s, g, epi);
     else hipLaunchKernelGGL((gemm_tiled_kernel<Epi, false>), grid, dim3(256), 0, s, g, epi);
   } else {
-    dim3 grid((g.NPT + kNP - 1) / kNP, (g.R + 16 * kMT - 1) / (16 * kMT));
-    const bool split = g.A_lo != nullptr;
+    // 32 columns per block; K split over blockIdx.z only when the caller
+    // provides a partial-sum buffer (linear epilogues)
+    const int nz = g.split_out ? g.split_k : 1;
+    dim3 grid(g.NPT, (g.R + 16 * kMT - 1) / (16 * kMT), nz);
+    const bool two = g.A_lo != nullptr;
     if (g.kind == W_FP8) {
-      if (split) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, true>), grid, dim3(256), 0, s, g, epi);
-      else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, false>), grid, dim3(256), 0, s, g, epi);
+      if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, true, 1>), grid, dim3(256), 0, s, g, epi);
+      else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, false, 1>), grid, dim3(256), 0, s, g, epi);
     } else {
-      if (split) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, true>), grid, dim3(256), 0, s, g, epi);
-      else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, false>), grid, dim3(256), 0, s, g, epi);
+      if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, true, 1>), grid, dim3(256), 0, s, g, epi);
+      else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, false, 1>), grid, dim3(256), 0, s, g, epi);
     }
   }
 }

@@ -46,6 +46,25 @@ struct GemmArgs {
   // read as zero (used for feature rows beyond a request's length)
   int rows_per_req;
   const CallDesc* desc;
+  // optional split over K (small row counts): raw partial sums go to
+  // split_out + z * split_stride ([R][32*NPT] fp32 each) and the epilogue is
+  // not run; the consumer adds the split_k slices in order
+  float* split_out;
+  int64_t split_stride;
+  int split_k;
+};
+
+// Split factor gemm launches use for a small-row GEMM (1 = no split).
+int gemm_split_k(int R, int NPT, int K);
+
+// Residual contribution left pending by split GEMMs, folded in by the next
+// row kernel: h += gate * (sum_s part[s] + bias) (gate/bias optional).
+struct PendingResid {
+  const float* part;
+  int n;
+  int64_t stride;
+  const float* gate;
+  const float* bias;
 };
 
 template <typename OutT>
@@ -231,10 +250,12 @@ enum NormMode { NORM_RMS = 0, NORM_LN = 1 };
 
 // n = normalise(h) * (1 + mul) + shift ; RMS or mean-centred LayerNorm.
 // With n_lo set, n_lo receives the bf16 rounding residue of n (two-term operand).
-void norm_rows_bf16(const float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode,
-                    const float* mul, const float* shift, hipStream_t);
-void norm_rows_f32(const float* h, float* n, int R, int d, float eps, int mode,
-                   const float* mul, const float* shift, hipStream_t);
+// With pend.n > 0 the pending residual is first added into h (written back):
+// the fused residual-add + norm.
+void norm_rows_bf16(float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode,
+                    const float* mul, const float* shift, const PendingResid& pend, hipStream_t);
+void norm_rows_f32(float* h, float* n, int R, int d, float eps, int mode,
+                   const float* mul, const float* shift, const PendingResid& pend, hipStream_t);
 
 struct EmbedArgs {
   const float* x;           // solver state [B][H][A]
@@ -254,7 +275,8 @@ void embed_state(const CallDesc* desc, const float* w, const float* b, float* e,
                  hipStream_t);
 
 struct ReadoutArgs {
-  const float* h; int B, H, M, off, d, A;
+  float* h; int B, H, M, off, d, A;
+  PendingResid pend;        // residual still pending from the last block
   float eps; int mode;
   const float* mul; const float* shift;   // final norm: * (1 + mul) + shift
   const float* out_w;       // [d][A] fp32

@@ -11,22 +11,43 @@ constexpr int kMaxPer = 8;   // d <= 2048 with 256 threads
 
 // n = normalise(h) * (1 + mul) + shift.  RMS: h / sqrt(mean(h^2) + eps);
 // LN: (h - mean) / sqrt(var + eps).  Statistics in fp32.
-template <typename OutT>
-__global__ __launch_bounds__(256) void norm_rows_kernel(const float* __restrict__ h, OutT* __restrict__ n,
-                                                        OutT* __restrict__ n_lo, int d, float eps, int mode,
-                                                        const float* __restrict__ mul,
-                                                        const float* __restrict__ shift) {
-  __shared__ float scratch[4];
-  const int row = blockIdx.x;
-  const float* hr = h + (int64_t)row * d;
-  float v[kMaxPer];
-  float s = 0.f;
+// h row += gate * (sum of pending slices + bias), written back; returns the row in v.
+__device__ __forceinline__ void load_row_with_pending(float* hr, int64_t row, int d, const PendingResid& pd,
+                                                      float (&v)[kMaxPer]) {
 #pragma unroll
   for (int i = 0; i < kMaxPer; ++i) {
     const int c = threadIdx.x + 256 * i;
     v[i] = c < d ? hr[c] : 0.f;
-    s += v[i];
   }
+  if (pd.n > 0) {
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      if (c < d) {
+        float t = 0.f;
+        for (int s = 0; s < pd.n; ++s) t += pd.part[s * pd.stride + row * d + c];
+        if (pd.bias) t += pd.bias[c];
+        if (pd.gate) t *= pd.gate[c];
+        v[i] += t;
+        hr[c] = v[i];
+      }
+    }
+  }
+}
+
+template <typename OutT>
+__global__ __launch_bounds__(256) void norm_rows_kernel(float* __restrict__ h, OutT* __restrict__ n,
+                                                        OutT* __restrict__ n_lo, int d, float eps, int mode,
+                                                        const float* __restrict__ mul,
+                                                        const float* __restrict__ shift, PendingResid pend) {
+  __shared__ float scratch[4];
+  const int row = blockIdx.x;
+  float* hr = h + (int64_t)row * d;
+  float v[kMaxPer];
+  load_row_with_pending(hr, row, d, pend, v);
+  float s = 0.f;
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) s += v[i];
   float mu = 0.f;
   if (mode == NORM_LN) mu = block_sum<256>(s, scratch) / d;
   float ss = 0.f;
@@ -96,15 +117,13 @@ __global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs r) {
   __shared__ float scratch[4];
   const int ar = blockIdx.x;                 // b*H + j
   const int b = ar / r.H, j = ar % r.H;
-  const float* hr = r.h + ((int64_t)b * r.M + r.off + j) * r.d;
+  const int64_t hrow = (int64_t)b * r.M + r.off + j;
+  float* hr = r.h + hrow * r.d;
   float v[kMaxPer];
+  load_row_with_pending(hr, hrow, r.d, r.pend, v);
   float s = 0.f;
 #pragma unroll
-  for (int i = 0; i < kMaxPer; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    v[i] = c < r.d ? hr[c] : 0.f;
-    s += v[i];
-  }
+  for (int i = 0; i < kMaxPer; ++i) s += v[i];
   float mu = 0.f;
   if (r.mode == NORM_LN) mu = block_sum<256>(s, scratch) / r.d;
   float ss = 0.f;
@@ -167,13 +186,14 @@ __global__ void fp8_decode_kernel(const uint8_t* codes, bf16_t* out, int64_t n) 
 
 }  // namespace
 
-void norm_rows_bf16(const float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode, const float* mul,
-                    const float* shift, hipStream_t s) {
-  hipLaunchKernelGGL(norm_rows_kernel<bf16_t>, dim3(R), dim3(256), 0, s, h, n, n_lo, d, eps, mode, mul, shift);
+void norm_rows_bf16(float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode, const float* mul,
+                    const float* shift, const PendingResid& pend, hipStream_t s) {
+  hipLaunchKernelGGL(norm_rows_kernel<bf16_t>, dim3(R), dim3(256), 0, s, h, n, n_lo, d, eps, mode, mul, shift, pend);
 }
-void norm_rows_f32(const float* h, float* n, int R, int d, float eps, int mode, const float* mul,
-                   const float* shift, hipStream_t s) {
-  hipLaunchKernelGGL(norm_rows_kernel<float>, dim3(R), dim3(256), 0, s, h, n, nullptr, d, eps, mode, mul, shift);
+void norm_rows_f32(float* h, float* n, int R, int d, float eps, int mode, const float* mul,
+                   const float* shift, const PendingResid& pend, hipStream_t s) {
+  hipLaunchKernelGGL(norm_rows_kernel<float>, dim3(R), dim3(256), 0, s, h, n, nullptr, d, eps, mode, mul, shift,
+                     pend);
 }
 void embed_actions(const EmbedArgs& e, hipStream_t s) {
   hipLaunchKernelGGL(embed_kernel, dim3(e.B * e.M), dim3(256), 0, s, e);

@@ -105,6 +105,7 @@ struct phyai_expert {
   void *o = nullptr, *g = nullptr;
   // per-layer key ranges: K [L][Bmax][nkv][ldk][D], V transposed [L][Bmax][nkv][D][ldk]
   void *kall = nullptr, *vt = nullptr;
+  float* pend = nullptr;    // split-K partial sums of the residual GEMMs (small batches)
   int ldk = 0;
   int64_t kv_layer = 0;     // elements per layer
   int* counters = nullptr;
@@ -279,10 +280,14 @@ void gemm_kv(const GemmArgs& g, const EpiKV<bf16_t>& e, hipStream_t s) { gemm_kv
 void gemm_kv(const GemmArgs& g, const EpiKV<float>& e, hipStream_t s) { gemm_kv_f32(g, e, s); }
 void prefix_relayout(const RelayoutArgs& r, bf16_t*, hipStream_t s) { prefix_relayout_bf16(r, s); }
 void prefix_relayout(const RelayoutArgs& r, float*, hipStream_t s) { prefix_relayout_f32(r, s); }
-void norm_rows(const float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode, const float* mul,
-               const float* sh, hipStream_t s) { norm_rows_bf16(h, n, n_lo, R, d, eps, mode, mul, sh, s); }
-void norm_rows(const float* h, float* n, float*, int R, int d, float eps, int mode, const float* mul, const float* sh,
-               hipStream_t s) { norm_rows_f32(h, n, R, d, eps, mode, mul, sh, s); }
+void norm_rows(float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode, const float* mul,
+               const float* sh, const PendingResid& p, hipStream_t s) {
+  norm_rows_bf16(h, n, n_lo, R, d, eps, mode, mul, sh, p, s);
+}
+void norm_rows(float* h, float* n, float*, int R, int d, float eps, int mode, const float* mul, const float* sh,
+               const PendingResid& p, hipStream_t s) {
+  norm_rows_f32(h, n, R, d, eps, mode, mul, sh, p, s);
+}
 
 GemmArgs gargs(const Lin& w, const void* A, int lda, int R) {
   GemmArgs g{};
@@ -316,6 +321,31 @@ int attn_splits(int B, int rows, int nkv, int keys) {
   return s < 1 ? 1 : s;
 }
 
+// Split over K used for a residual GEMM of block l (which: 0 = O projection,
+// 1 = down / MLP-out projection) at batch B; 1 means the epilogue adds into h
+// directly.
+int resid_split(const phyai_expert& e, int which, int l, int B) {
+  if (e.f32) return 1;
+  const Lin& w = which == 0 ? e.layers[l].o : e.layers[l].down;
+  return gemm_split_k(B * e.M, w.NPT, w.K);
+}
+
+// The residual contribution a split GEMM left pending, for its consumer.
+PendingResid pending_of(const phyai_expert& e, int which, int l, int k, int B) {
+  PendingResid p{};
+  const int S = resid_split(e, which, l, B);
+  if (S <= 1) return p;
+  p.part = e.pend;
+  p.n = S;
+  p.stride = (int64_t)B * e.M * e.d;
+  if (e.c.variant == PHYAI_VARIANT_DIT) {
+    const float* ada = e.adatab + ((int64_t)k * e.L + l) * 6 * e.d;
+    p.gate = which == 0 ? ada + 2 * e.d : ada + 5 * e.d;
+    p.bias = which == 0 ? nullptr : e.layers[l].mlp_b2;
+  }
+  return p;
+}
+
 // ---------------------------------------------------------------------------
 // the K-step loop
 // ---------------------------------------------------------------------------
@@ -336,6 +366,15 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   T* n_lo = static_cast<T*>(e.n_lo);
   T* g_lo = static_cast<T*>(e.g_lo);
   auto with_lo = [](GemmArgs ga, const void* lo) { ga.A_lo = lo; return ga; };
+  auto with_split = [&](GemmArgs ga, int which) {
+    const int sk = resid_split(e, which, l, B);
+    if (sk > 1) {
+      ga.split_out = e.pend;
+      ga.split_stride = (int64_t)R * d;
+      ga.split_k = sk;
+    }
+    return ga;
+  };
   const int variant = e.c.variant;
   const int S = 2 * L + 1;   // pi0.5 norm sites
   const LayerW& w = e.layers[l];
@@ -362,7 +401,11 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
       sh2 = mul2 + d;
     }
     switch (stage) {
-      case ST_NORM1: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul1, sh1, s); break;
+      case ST_NORM1: {
+        const PendingResid pd = l > 0 ? pending_of(e, 1, l - 1, k, B) : PendingResid{};
+        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul1, sh1, pd, s);
+        break;
+      }
       case ST_QKV: {
         EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, e.c.rope, M, e.ldk, 1, e.inv_freq, e.desc};
         gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
@@ -376,11 +419,13 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
         if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
         break;
       }
-      case ST_OPROJ: gemm_resid(gargs(w.o, o, e.qd, R), EpiResid{e.h, d, nullptr, nullptr}, s); break;
-      case ST_NORM2: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul2, sh2, s); break;
+      case ST_OPROJ: gemm_resid(with_split(gargs(w.o, o, e.qd, R), 0), EpiResid{e.h, d, nullptr, nullptr}, s); break;
+      case ST_NORM2:
+        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul2, sh2, pending_of(e, 0, l, k, B), s);
+        break;
       case ST_MLP_UP: gemm_geglu(with_lo(gargs(w.gu, n, d, R), n_lo), EpiGeglu<T>{g, e.F, g_lo}, s); break;
       case ST_MLP_DOWN:
-        gemm_resid(with_lo(gargs(w.down, g, e.F, R), g_lo), EpiResid{e.h, d, nullptr, nullptr}, s);
+        gemm_resid(with_split(with_lo(gargs(w.down, g, e.F, R), g_lo), 1), EpiResid{e.h, d, nullptr, nullptr}, s);
         break;
     }
     return;
@@ -391,7 +436,11 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
               *g2 = ada + 5 * d;
   const bool cross = (l % 2) == 0;
   switch (stage) {
-    case ST_NORM1: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc1, sh1, s); break;
+    case ST_NORM1: {
+      const PendingResid pd = l > 0 ? pending_of(e, 1, l - 1, k, B) : PendingResid{};
+      norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc1, sh1, pd, s);
+      break;
+    }
     case ST_QKV: {
       // cross blocks project only Q here (their K/V come from the features)
       EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, 0, M, e.ldk, 0, e.inv_freq, e.desc};
@@ -406,12 +455,12 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
       if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
       break;
     }
-    case ST_OPROJ: gemm_resid(gargs(w.o, o, e.qd, R), EpiResid{e.h, d, nullptr, g1}, s); break;
-    case ST_NORM2: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc2, sh2, s); break;
+    case ST_OPROJ: gemm_resid(with_split(gargs(w.o, o, e.qd, R), 0), EpiResid{e.h, d, nullptr, g1}, s); break;
+    case ST_NORM2: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc2, sh2, pending_of(e, 0, l, k, B), s); break;
     case ST_MLP_UP:
       gemm_store(with_lo(gargs(w.gu, n, d, R), n_lo), store_epi<T>(g, e.F, w.mlp_b1, nullptr, ACT_GELU), s);
       break;
-    case ST_MLP_DOWN: gemm_resid(gargs(w.down, g, e.F, R), EpiResid{e.h, d, w.mlp_b2, g2}, s); break;
+    case ST_MLP_DOWN: gemm_resid(with_split(gargs(w.down, g, e.F, R), 1), EpiResid{e.h, d, w.mlp_b2, g2}, s); break;
   }
 }
 
@@ -468,6 +517,7 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
     ro.h = e.h; ro.B = B; ro.H = H; ro.M = M; ro.off = e.off; ro.d = d; ro.A = e.A;
     ro.eps = e.c.rms_eps;
     ro.out_w = e.out_w; ro.out_b = e.out_b; ro.dt = e.dt + k; ro.x = e.x;
+    ro.pend = pending_of(e, 1, L - 1, k, B);
     if (variant == PHYAI_VARIANT_PI0) { ro.mode = NORM_RMS; ro.mul = e.final_norm; ro.shift = nullptr; }
     else if (variant == PHYAI_VARIANT_PI05) {
       ro.mode = NORM_RMS;
@@ -719,6 +769,19 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     }
   }
   e->part = e->mem.alloc_n<float>(part > 0 ? part : 4);
+  {
+    int64_t pend = 4;
+    if (!e->f32)
+      for (int B = 1; B <= e->Bmax; ++B) {
+        const int R = B * e->M;
+        for (int l = 0; l < L; ++l)
+          for (int which = 0; which < 2; ++which) {
+            const int sk = resid_split(*e, which, l, B);
+            if (sk > 1) pend = std::max(pend, (int64_t)sk * R * d);
+          }
+      }
+    e->pend = e->mem.alloc_n<float>(pend);
+  }
   {
     const int64_t nc = attention_counters(e->Bmax, e->M, e->nq, e->nkv);
     e->counters = e->mem.alloc_n<int>(nc);
