@@ -22,8 +22,8 @@
 // fragment read from LDS feeds two MFMAs); 64-key tiles double-buffered in
 // LDS and filled by direct global->LDS loads, the next tile in flight while
 // the current one is computed.
-// With n_split > 1 the key range is split over blocks; the last block of a
-// row tile to finish (atomic counter) merges the partials in a fixed order.
+// With n_split > 1 the key range is split over blocks, whose partials a
+// second kernel merges in a fixed order.
 #include "kernels.hpp"
 
 namespace phyai {
@@ -187,7 +187,6 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   // are visibly independent
   __shared__ __attribute__((aligned(1024))) AttnTile<D> smA;
   __shared__ __attribute__((aligned(1024))) AttnTile<D> smB;
-  __shared__ int s_last;
   constexpr int CPR = D / 8;                  // 16-byte chunks per K row
   constexpr int NLD = kKT * D / 8 / 256;      // loads per thread per operand per tile
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -332,7 +331,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   }
 
   // ---- split: write this block's partial (O normalised by its own l, as
-  // bf16, plus m and l), the last block of the row tile merges them
+  // bf16, plus m and l); attn_combine_kernel merges the splits
   const int64_t tile_id = (int64_t)grp * ntiles + rt;
   bf16_t* obase = reinterpret_cast<bf16_t*>(a.part) + tile_id * a.n_split * (int64_t)kRows * D;
   float* mlbase = a.part + (a.part_ml_off) + tile_id * a.n_split * (int64_t)kRows * 2;
@@ -353,46 +352,59 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
       mlbase[((int64_t)split * kRows + lrow) * 2 + 1] = l_run[c];
     }
   }
-  __threadfence();
-  __syncthreads();
-  if (threadIdx.x == 0) s_last = (atomicAdd(&a.counters[tile_id], 1) == a.n_split - 1);
-  __syncthreads();
-  if (!s_last) return;
-  __threadfence();
-  // merge: thread t handles row t/2 and half of D; weights w_s = l_s 2^(m_s - M)
-  const int lrow = threadIdx.x / 2, half = threadIdx.x % 2;
-  const int gr = rt * kRows + lrow;
-  if (gr < rows) {
-    float mmax = -1e30f;
-    for (int s2 = 0; s2 < a.n_split; ++s2) mmax = fmaxf(mmax, mlbase[((int64_t)s2 * kRows + lrow) * 2]);
-    float acc[D / 2];
+}
+
+// Merge the key splits of one query row per wave: o = sum_s w_s o_s / sum_s w_s
+// with w_s = l_s 2^(m_s - max m); every split's data is requested at once.
+// Lane i merges elements 4i .. 4i+3 (lanes >= D/4 idle).
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int G = a.nq / a.nkv;
+  const int rows = a.M * G;
+  const int ntiles = (rows + kRows - 1) / kRows;
+  const int grp = blockIdx.y;
+  const int r = blockIdx.x * 4 + wave;
+  if (r >= rows || lane >= D / 4) return;
+  const int b = grp / a.nkv, kvh = grp % a.nkv;
+  const int rt = r / kRows, lrow = r % kRows;
+  const int64_t tile_id = (int64_t)grp * ntiles + rt;
+  const bf16_t* obase = reinterpret_cast<const bf16_t*>(a.part) + tile_id * a.n_split * (int64_t)kRows * D;
+  const float* mlbase = a.part + a.part_ml_off + tile_id * a.n_split * (int64_t)kRows * 2;
+  constexpr int SMAX = 16;
+  float m[SMAX], l[SMAX];
+  uint2 v[SMAX];
+  float mmax = -1e30f;
 #pragma unroll
-    for (int i = 0; i < D / 2; ++i) acc[i] = 0.f;
-    float lsum = 0.f;
-    for (int s2 = 0; s2 < a.n_split; ++s2) {
-      const float* ml = mlbase + ((int64_t)s2 * kRows + lrow) * 2;
-      const float w = ml[1] * exp2f(ml[0] - mmax);
-      lsum += w;
-      const bf16_t* pp = obase + ((int64_t)s2 * kRows + lrow) * D + half * (D / 2);
-#pragma unroll
-      for (int i = 0; i < D / 2; i += 8) {
-        const uint4 v = *reinterpret_cast<const uint4*>(pp + i);
-        const uint32_t u[4] = {v.x, v.y, v.z, v.w};
-#pragma unroll
-        for (int k = 0; k < 4; ++k) {
-          acc[i + 2 * k] += w * __uint_as_float(u[k] << 16);
-          acc[i + 2 * k + 1] += w * __uint_as_float(u[k] & 0xffff0000u);
-        }
-      }
+  for (int s = 0; s < SMAX; ++s) {
+    if (s < a.n_split) {
+      const float* ml = mlbase + ((int64_t)s * kRows + lrow) * 2;
+      m[s] = ml[0];
+      l[s] = ml[1];
+      v[s] = *reinterpret_cast<const uint2*>(obase + ((int64_t)s * kRows + lrow) * D + 4 * lane);
+      mmax = fmaxf(mmax, m[s]);
     }
-    const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
-    const int tok = gr / G, qhead = kvh * G + gr % G;
-    bf16_t* op = static_cast<bf16_t*>(a.out) + (int64_t)(b * a.M + tok) * a.ldo + qhead * D + half * (D / 2);
-#pragma unroll
-    for (int i = 0; i < D / 2; i += 2)
-      *reinterpret_cast<uint32_t*>(op + i) = pack_bf16x2(acc[i] * inv, acc[i + 1] * inv);
   }
-  if (threadIdx.x == 0) a.counters[tile_id] = 0;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  float lsum = 0.f;
+#pragma unroll
+  for (int s = 0; s < SMAX; ++s) {
+    if (s < a.n_split) {
+      const float w = l[s] * exp2f(m[s] - mmax);
+      lsum += w;
+      acc[0] += w * __uint_as_float(v[s].x << 16);
+      acc[1] += w * __uint_as_float(v[s].x & 0xffff0000u);
+      acc[2] += w * __uint_as_float(v[s].y << 16);
+      acc[3] += w * __uint_as_float(v[s].y & 0xffff0000u);
+    }
+  }
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  const int tok = r / G, qhead = kvh * G + r % G;
+  bf16_t* op = static_cast<bf16_t*>(a.out) + (int64_t)(b * a.M + tok) * a.ldo + qhead * D + 4 * lane;
+  uint2 w;
+  w.x = pack_bf16x2(acc[0] * inv, acc[1] * inv);
+  w.y = pack_bf16x2(acc[2] * inv, acc[3] * inv);
+  *reinterpret_cast<uint2*>(op) = w;
 }
 
 // fp32 path: one wave per (request, token, query head), keys one at a time.
@@ -521,6 +533,12 @@ void attention_bf16(const AttnArgs& a0, hipStream_t s) {
   if (a.D == 256) hipLaunchKernelGGL(attn_mfma_kernel<256>, grid, dim3(256), 0, s, a);
   else if (a.D == 128) hipLaunchKernelGGL(attn_mfma_kernel<128>, grid, dim3(256), 0, s, a);
   else if (a.D == 64) hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, s, a);
+  if (a.n_split > 1) {
+    dim3 g2((rows + 3) / 4, a.B * a.nkv);
+    if (a.D == 256) hipLaunchKernelGGL(attn_combine_kernel<256>, g2, dim3(256), 0, s, a);
+    else if (a.D == 128) hipLaunchKernelGGL(attn_combine_kernel<128>, g2, dim3(256), 0, s, a);
+    else if (a.D == 64) hipLaunchKernelGGL(attn_combine_kernel<64>, g2, dim3(256), 0, s, a);
+  }
 }
 
 void attention_f32(const AttnArgs& a, hipStream_t s) {

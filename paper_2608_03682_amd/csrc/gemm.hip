@@ -59,48 +59,58 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  for (int kb = kb0; kb < kb1; ++kb) {
-    bf16x8 b[NT][2];
+  // up to KU k-blocks per trip, every load of the trip issued before its
+  // MFMAs (blocks past the wave's range re-read a valid block with a zero A)
+  constexpr int KU = 4;
+  for (int kb = kb0; kb < kb1; kb += KU) {
+    bf16x8 b[KU][NT][2];
+    bf16x8 a[KU][kMT][2], al[KU][kMT][2];
 #pragma unroll
-    for (int t = 0; t < NT; ++t) {
-      const int p = pt0 + t / 2, hf = t % 2;
-      const int64_t frag = ((int64_t)(p * nkb + kb) * 2 + hf) * kWave + lane;
-      if (p >= g.NPT) {
-        b[t][0] = as_bf16x8(make_uint4(0, 0, 0, 0));
-        b[t][1] = b[t][0];
-      } else if (FP8) {
-        const uint4 v = static_cast<const uint4*>(g.W)[frag];
-        b[t][0] = fp8x8_to_bf16x8(v.x, v.y);
-        b[t][1] = fp8x8_to_bf16x8(v.z, v.w);
-      } else {
-        const uint4* src = static_cast<const uint4*>(g.W) + frag * 2;
-        b[t][0] = as_bf16x8(src[0]);
-        b[t][1] = as_bf16x8(src[1]);
+    for (int u = 0; u < KU; ++u) {
+      const bool live = kb + u < kb1;
+      const int kk = live ? kb + u : kb;
+#pragma unroll
+      for (int t = 0; t < NT; ++t) {
+        const int p = pt0 + t / 2, hf = t % 2;
+        const int64_t frag = ((int64_t)(p * nkb + kk) * 2 + hf) * kWave + lane;
+        if (p >= g.NPT) {
+          b[u][t][0] = as_bf16x8(make_uint4(0, 0, 0, 0));
+          b[u][t][1] = b[u][t][0];
+        } else if (FP8) {
+          const uint4 v = static_cast<const uint4*>(g.W)[frag];
+          b[u][t][0] = fp8x8_to_bf16x8(v.x, v.y);
+          b[u][t][1] = fp8x8_to_bf16x8(v.z, v.w);
+        } else {
+          const uint4* src = static_cast<const uint4*>(g.W) + frag * 2;
+          b[u][t][0] = as_bf16x8(src[0]);
+          b[u][t][1] = as_bf16x8(src[1]);
+        }
+      }
+#pragma unroll
+      for (int mt = 0; mt < kMT; ++mt) {
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          uint4 v = make_uint4(0, 0, 0, 0), w = make_uint4(0, 0, 0, 0);
+          if (aval[mt] && live) {
+            v = *reinterpret_cast<const uint4*>(arp[mt] + kk * 64 + s * 32);
+            if (SPLIT) w = *reinterpret_cast<const uint4*>(alp[mt] + kk * 64 + s * 32);
+          }
+          a[u][mt][s] = as_bf16x8(v);
+          al[u][mt][s] = as_bf16x8(w);
+        }
       }
     }
-    bf16x8 a[kMT][2], al[kMT][2];
 #pragma unroll
-    for (int mt = 0; mt < kMT; ++mt) {
+    for (int u = 0; u < KU; ++u)
 #pragma unroll
-      for (int s = 0; s < 2; ++s) {
-        uint4 v = make_uint4(0, 0, 0, 0), w = make_uint4(0, 0, 0, 0);
-        if (aval[mt]) {
-          v = *reinterpret_cast<const uint4*>(arp[mt] + kb * 64 + s * 32);
-          if (SPLIT) w = *reinterpret_cast<const uint4*>(alp[mt] + kb * 64 + s * 32);
-        }
-        a[mt][s] = as_bf16x8(v);
-        al[mt][s] = as_bf16x8(w);
-      }
-    }
+      for (int s = 0; s < 2; ++s)
 #pragma unroll
-    for (int s = 0; s < 2; ++s)
+        for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
-      for (int mt = 0; mt < kMT; ++mt)
-#pragma unroll
-        for (int t = 0; t < NT; ++t) {
-          acc[mt][t] = mfma16x16x32(a[mt][s], b[t][s], acc[mt][t]);
-          if (SPLIT) acc[mt][t] = mfma16x16x32(al[mt][s], b[t][s], acc[mt][t]);
-        }
+          for (int t = 0; t < NT; ++t) {
+            acc[mt][t] = mfma16x16x32(a[u][mt][s], b[u][t][s], acc[mt][t]);
+            if (SPLIT) acc[mt][t] = mfma16x16x32(al[u][mt][s], b[u][t][s], acc[mt][t]);
+          }
   }
 
 #pragma unroll

@@ -318,6 +318,7 @@ int attn_splits(int B, int rows, int nkv, int keys) {
   int s = (256 + base - 1) / base;
   const int cap = (keys + 127) / 128;                   // keep >= two 64-key tiles per split
   if (s > cap) s = cap;
+  if (s > 16) s = 16;                                   // the merge kernel takes up to 16
   return s < 1 ? 1 : s;
 }
 
