@@ -141,6 +141,40 @@ def cpu_baseline(cfg, case):
                       f"L={cfg.n_layers}), float64 NumPy oracle, median"}
 
 
+def measured_roofs():
+    """The paper's roof measurement, on this GPU: best of 50 after 10 warm-up
+    iterations of a 4 GiB device copy (memory roof) and an 8192^2 bf16 GEMM
+    (compute roof, torch/hipBLASLt used only as a measuring stick)."""
+    import torch
+    n = (4 << 30) // 4
+    src = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    a = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+    b = torch.randn(8192, 8192, dtype=torch.bfloat16, device="cuda")
+
+    def best(fn):
+        for _ in range(10):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(50):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1) * 1e-3)
+        return min(ts)
+
+    t_copy = best(lambda: dst.copy_(src))
+    t_gemm = best(lambda: torch.matmul(a, b))
+    out = {"copy_GBs": round(2 * n * 4 / t_copy / 1e9, 1), "copy_bytes_per_launch": 2 * n * 4,
+           "bf16_gemm_TFLOPs": round(2 * 8192 ** 3 / t_gemm / 1e12, 1)}
+    del src, dst, a, b
+    torch.cuda.empty_cache()
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -149,6 +183,7 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-batch64", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-roofs", action="store_true")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (the expert loop shards as independent "
@@ -199,6 +234,9 @@ def main():
         "chunk_roofline": {"bytes_per_chunk": int(cb), "achieved_GBs": round(cb / (ms * 1e-3) / 1e9, 1),
                            "frac_of_hbm_peak": round(cb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
     }
+    if not args.no_roofs:
+        _log("measuring the copy and GEMM roofs")
+        rec["measured_roofs"] = measured_roofs()
     if not args.no_cpu_baseline:
         _log("timing the CPU oracle baseline")
         rec["cpu_baseline"] = cpu_baseline(cfg, case)

@@ -20,12 +20,18 @@ __device__ __forceinline__ void load_row_with_pending(float* hr, int64_t row, in
     v[i] = c < d ? hr[c] : 0.f;
   }
   if (pd.n > 0) {
+    // all slices of a column are requested before they are summed (in order)
+    constexpr int kMaxSplit = 8;
 #pragma unroll
     for (int i = 0; i < kMaxPer; ++i) {
       const int c = threadIdx.x + 256 * i;
       if (c < d) {
+        float sl[kMaxSplit];
+#pragma unroll
+        for (int s = 0; s < kMaxSplit; ++s) sl[s] = s < pd.n ? pd.part[s * pd.stride + row * d + c] : 0.f;
         float t = 0.f;
-        for (int s = 0; s < pd.n; ++s) t += pd.part[s * pd.stride + row * d + c];
+#pragma unroll
+        for (int s = 0; s < kMaxSplit; ++s) t += sl[s];
         if (pd.bias) t += pd.bias[c];
         if (pd.gate) t *= pd.gate[c];
         v[i] += t;
@@ -85,6 +91,7 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs e) {
   __syncthreads();
   for (int c = threadIdx.x; c < e.d; c += 256) {
     float y = e.in_b[c];
+#pragma unroll 16
     for (int a = 0; a < e.A; ++a) y = fmaf(xs[a], e.in_w[(int64_t)a * e.d + c], y);
     if (e.pos) y += e.pos[(int64_t)j * e.d + c];
     if (e.act_out) {
@@ -105,6 +112,7 @@ __global__ __launch_bounds__(256) void state_embed_kernel(const CallDesc* desc, 
   __syncthreads();
   for (int c = threadIdx.x; c < d; c += 256) {
     float y = bias[c];
+#pragma unroll 16
     for (int a = 0; a < A; ++a) y = fmaf(xs[a], w[(int64_t)a * d + c], y);
     e[(int64_t)b * d + c] = y;
   }
@@ -144,10 +152,21 @@ __global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs r) {
     }
   }
   __syncthreads();
+  // v = n W_out: thread (group gq of 4, column a) sums rows c = gq (mod 4);
+  // eight independent partial sums keep the W_out loads in flight
   const int a = threadIdx.x % 64, gq = threadIdx.x / 64;
   float part = 0.f;
-  if (a < r.A)
-    for (int c = gq; c < r.d; c += 4) part = fmaf(nrm[c], r.out_w[(int64_t)c * r.A + a], part);
+  if (a < r.A) {
+    float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int c = gq;
+    for (; c + 28 < r.d; c += 32) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc8[u] = fmaf(nrm[c + 4 * u], r.out_w[(int64_t)(c + 4 * u) * r.A + a], acc8[u]);
+    }
+    for (; c < r.d; c += 4) acc8[0] = fmaf(nrm[c], r.out_w[(int64_t)c * r.A + a], acc8[0]);
+#pragma unroll
+    for (int u = 0; u < 8; ++u) part += acc8[u];
+  }
   red[gq][a] = part;
   __syncthreads();
   if (threadIdx.x < r.A) {
