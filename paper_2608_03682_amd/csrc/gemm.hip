@@ -9,6 +9,9 @@
 // K therefore reads whole contiguous 2 KiB (bf16) / 1 KiB (fp8) blocks.
 #include "kernels.hpp"
 
+#include <cstdlib>
+#include <cstring>
+
 namespace phyai {
 
 namespace {
@@ -323,6 +326,130 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
   }
 }
 
+// ---------------------------------------------------------------------------
+// Ring-pipelined 128 x 128 GEMM for many rows and short K.  4 waves in a
+// 2 x 2 arrangement of 64 x 64; per k-block of 64 the activation tile and
+// the block's 8 packed weight fragments go through a 2-stage LDS ring (48
+// KiB per block for fp8 weights, so three blocks share a compute unit and
+// cover each other's barrier and load stalls); one barrier per k-block;
+// every fragment of a k-block is requested before its first MFMA.
+// Measured against the grid-strided kernel above on the rollout-batch
+// shapes (3264 rows, fp8 weights): faster for K = 1024 (QKV 28.5 vs 39 us,
+// GeGLU 65 vs 77 us), slower for K >= 2048, where the other one is used.
+// ---------------------------------------------------------------------------
+template <bool FP8>
+struct RingCfg {
+  static constexpr int FB = FP8 ? 1024 : 2048;   // bytes per (pair, half) fragment per k-block
+  static constexpr int A_KB = 16, B_KB = 8 * FB / 1024;
+  static constexpr int STAGE = (A_KB + B_KB) * 1024;
+  static constexpr int A_LD = A_KB / 4, B_LD = B_KB / 4;
+};
+
+template <class Epi, bool FP8>
+__global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g, Epi epi) {
+  typedef RingCfg<FP8> C;
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[2 * C::STAGE];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int wv = __builtin_amdgcn_readfirstlane(wave);
+  const int wm = wave >> 1, wn = wave & 1;
+  const int lc = lane % 16, lg = lane / 16;
+  const int nkb = g.K / 64;
+  const int mtiles = (g.R + 127) / 128;
+  const int m0 = (blockIdx.x % mtiles) * 128;
+  const int pt0 = (blockIdx.x / mtiles) * 4;
+  const bf16_t* A = static_cast<const bf16_t*>(g.A);
+  const uint8_t* W = static_cast<const uint8_t*>(g.W);
+
+  int aoff[C::A_LD];
+#pragma unroll
+  for (int i = 0; i < C::A_LD; ++i) {
+    const int row = 8 * (4 * i + wave) + lane / 8;       // 1 KiB block 4i + wave = rows 8 blk ..
+    aoff[i] = min(m0 + row, g.R - 1) * g.lda + 8 * ((lane % 8) ^ aswz(row));
+  }
+  const uint8_t* bsrc[C::B_LD];
+#pragma unroll
+  for (int i = 0; i < C::B_LD; ++i) {
+    const int blk = 4 * i + wave;
+    const int f = blk / (C::FB / 1024), part = blk % (C::FB / 1024);
+    bsrc[i] = W + ((int64_t)(pt0 + f / 2) * nkb * 2 + f % 2) * C::FB + part * 1024 + lane * 16;
+  }
+  auto issue = [&](int slot, int kb) {
+    uint8_t* base = ring + slot * C::STAGE;
+#pragma unroll
+    for (int i = 0; i < C::A_LD; ++i) dma16(A + aoff[i] + kb * 64, (lds_void_t*)(base + (4 * i + wv) * 1024));
+#pragma unroll
+    for (int i = 0; i < C::B_LD; ++i)
+      dma16(bsrc[i] + (int64_t)kb * 2 * C::FB, (lds_void_t*)(base + (C::A_KB + 4 * i + wv) * 1024));
+  };
+
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](int slot) {
+    const bf16_t* As = reinterpret_cast<const bf16_t*>(ring + slot * C::STAGE);
+    const uint8_t* Bs = ring + slot * C::STAGE + C::A_KB * 1024;
+    constexpr int BW = FP8 ? 1 : 2;
+    uint4 braw[4][BW];
+#pragma unroll
+    for (int nt = 0; nt < 4; ++nt) {
+      const int f = 2 * (2 * wn + nt / 2) + nt % 2;
+#pragma unroll
+      for (int w = 0; w < BW; ++w) braw[nt][w] = *reinterpret_cast<const uint4*>(Bs + f * C::FB + lane * 16 * BW + 16 * w);
+    }
+    bf16x8 af[2][4];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        const int row = 64 * wm + 16 * mt + lc;
+        af[st][mt] = *reinterpret_cast<const bf16x8*>(As + row * 64 + 8 * ((4 * st + lg) ^ aswz(row)));
+      }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+      bf16x8 bfr[4];
+#pragma unroll
+      for (int nt = 0; nt < 4; ++nt) {
+        if (FP8) bfr[nt] = st == 0 ? fp8x8_to_bf16x8(braw[nt][0].x, braw[nt][0].y)
+                                   : fp8x8_to_bf16x8(braw[nt][0].z, braw[nt][0].w);
+        else bfr[nt] = as_bf16x8(braw[nt][BW - 1 < st ? 0 : st]);
+      }
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma16x16x32(af[st][mt], bfr[nt], acc[mt][nt]);
+    }
+  };
+
+  issue(0, 0);
+  for (int kb = 0; kb < nkb; ++kb) {
+    GEMM_WAIT_VMCNT(0);                      // this wave's loads of k-block kb have landed
+    bare_barrier();                          // ... everyone's, and k-block kb-1 is consumed
+    if (kb + 1 < nkb) issue((kb + 1) & 1, kb + 1);
+    compute(kb & 1);
+  }
+
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    const int p = pt0 + 2 * wn + pp;
+    float s0c = 1.f, s1c = 1.f;
+    if (g.scale) {
+      s0c = g.scale[32 * p + lc];
+      s1c = g.scale[32 * p + 16 + lc];
+    }
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = m0 + 64 * wm + 16 * mt + 4 * lg + v;
+        if (row < g.R) epi(row, p, lc, acc[mt][2 * pp][v] * s0c, acc[mt][2 * pp + 1][v] * s1c);
+      }
+  }
+}
+
 }  // namespace
 
 int gemm_split_k(int R, int NPT, int K) {
@@ -344,9 +471,16 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
     hipLaunchKernelGGL(gemm_f32_kernel<Epi>, grid, dim3(256), 0, s, g, epi);
   } else if (g.R >= 256 && g.A_lo == nullptr && g.A_ind == nullptr && g.rows_per_req == 0 && g.NPT % 4 == 0) {
     const int tiles = ((g.R + 127) / 128) * (g.NPT / 4);
-    dim3 grid(tiles < 512 ? tiles : 512);
-    if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_tiled_kernel<Epi, true>), grid, dim3(256), 0, s, g, epi);
-    else hipLaunchKernelGGL((gemm_tiled_kernel<Epi, false>), grid, dim3(256), 0, s, g, epi);
+    const char* force = getenv("PHYAI_GEMM_TILE");   // tests: "ring" / "strided" (read at enqueue time)
+    const bool ring = force ? strcmp(force, "ring") == 0 : g.K <= 1024;
+    if (ring) {
+      if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true>), dim3(tiles), dim3(256), 0, s, g, epi);
+      else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false>), dim3(tiles), dim3(256), 0, s, g, epi);
+    } else {
+      dim3 grid(tiles < 512 ? tiles : 512);
+      if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_tiled_kernel<Epi, true>), grid, dim3(256), 0, s, g, epi);
+      else hipLaunchKernelGGL((gemm_tiled_kernel<Epi, false>), grid, dim3(256), 0, s, g, epi);
+    }
   } else {
     // 32 columns per block; K split over blockIdx.z only when the caller
     // provides a partial-sum buffer (linear epilogues)

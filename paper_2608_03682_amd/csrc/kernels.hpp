@@ -136,7 +136,7 @@ struct EpiQkv {
   int M;                    // suffix tokens per request
   int ldk;                  // key capacity of a key range
   int keys_after_prefix;
-  const float* inv_freq;    // [D/2]: base^(-2i/D)
+  const float2* rope_cs;    // [rows][D/2]: (cos, sin) of position * base^(-2i/D)
   const CallDesc* desc;     // positions start at prefix_len[b]
   __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
     const int tiles = D / 32;
@@ -145,12 +145,10 @@ struct EpiQkv {
     const int b = r / M, tok = r % M;
     const int plen = desc->prefix_len[b];
     if (rope && head < nq + nkv) {
-      const float pos = (float)(plen + tok);
-      float s, co;
-      sincosf(pos * inv_freq[i], &s, &co);
+      const float2 cs = rope_cs[(int64_t)r * (D / 2) + i];
       const float x1 = a0, x2 = a1;
-      a0 = x1 * co - x2 * s;
-      a1 = x2 * co + x1 * s;
+      a0 = x1 * cs.x - x2 * cs.y;
+      a1 = x2 * cs.x + x1 * cs.y;
     }
     if (head < nq) {
       OutT* dst = q + (int64_t)r * nq * D + head * D + i;
@@ -289,6 +287,9 @@ void readout_euler(const ReadoutArgs&, hipStream_t);
 void copy_noise_to_state(const CallDesc* desc, float* x, int64_t n, hipStream_t);
 void copy_state_to_out(const CallDesc* desc, const float* x, int64_t n, hipStream_t);
 void set_call_desc(const CallDesc& host_desc, CallDesc* dev, hipStream_t);
+// RoPE table of one call: tab[b*M + t][i] = (cos, sin)((prefix_len[b] + t) * inv_freq[i]),
+// i < D/2 (positions of the suffix tokens follow their request's prefix).
+void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B, int M, int D, hipStream_t);
 void fp8_to_bf16(const uint8_t* codes, bf16_t* out, int64_t n, hipStream_t);
 
 }  // namespace phyai

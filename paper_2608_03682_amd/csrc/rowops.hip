@@ -175,6 +175,18 @@ __global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs r) {
   }
 }
 
+__global__ __launch_bounds__(128) void rope_table_kernel(const CallDesc* desc, const float* inv_freq, float2* tab,
+                                                        int M, int half) {
+  const int row = blockIdx.x;                    // b*M + t
+  const int b = row / M, t = row % M;
+  const float pos = (float)(desc->prefix_len[b] + t);
+  for (int i = threadIdx.x; i < half; i += blockDim.x) {
+    float sn, cs;
+    sincosf(pos * inv_freq[i], &sn, &cs);
+    tab[(int64_t)row * half + i] = make_float2(cs, sn);
+  }
+}
+
 __global__ void copy_in_kernel(const CallDesc* desc, float* x, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) x[i] = desc->noise[i];
@@ -229,6 +241,9 @@ void copy_noise_to_state(const CallDesc* desc, float* x, int64_t n, hipStream_t 
 }
 void copy_state_to_out(const CallDesc* desc, const float* x, int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(copy_out_kernel, dim3((n + 255) / 256), dim3(256), 0, s, desc, x, n);
+}
+void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B, int M, int D, hipStream_t s) {
+  hipLaunchKernelGGL(rope_table_kernel, dim3(B * M), dim3(128), 0, s, desc, inv_freq, tab, M, D / 2);
 }
 void set_call_desc(const CallDesc& d, CallDesc* dev, hipStream_t s) {
   hipLaunchKernelGGL(set_desc_kernel, dim3(1), dim3(256), 0, s, d, dev);

@@ -99,6 +99,7 @@ struct phyai_expert {
   Lin time_w1a, time_w1t, time_w2, cond_w1, cond_w2, final_mod;
   std::vector<LayerW> layers;
   float* inv_freq = nullptr;
+  float2* rope_cs = nullptr;   // per-call RoPE table [max_batch * M][D/2]
   // working buffers
   float *x = nullptr, *h = nullptr, *e_state = nullptr, *part = nullptr;
   void *n = nullptr, *abuf = nullptr, *zbuf = nullptr, *q = nullptr;
@@ -408,7 +409,7 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
         break;
       }
       case ST_QKV: {
-        EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, e.c.rope, M, e.ldk, 1, e.inv_freq, e.desc};
+        EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, e.c.rope, M, e.ldk, 1, e.rope_cs, e.desc};
         gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
         break;
       }
@@ -444,7 +445,7 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
     }
     case ST_QKV: {
       // cross blocks project only Q here (their K/V come from the features)
-      EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, 0, M, e.ldk, 0, e.inv_freq, e.desc};
+      EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, 0, M, e.ldk, 0, e.rope_cs, e.desc};
       gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
       break;
     }
@@ -471,6 +472,7 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
   const int variant = e.c.variant;
 
   copy_noise_to_state(e.desc, e.x, (int64_t)B * H * e.A, s);
+  if (e.c.rope) rope_table(e.desc, e.inv_freq, e.rope_cs, B, M, e.D, s);
   if (e.c.state_token) embed_state(e.desc, e.state_w, e.state_b, e.e_state, B, e.A, d, s);
   if (variant == PHYAI_VARIANT_DIT) {
     // request-local cross-attention K/V: project the VLM features once per call
@@ -727,6 +729,7 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     for (int i = 0; i < D / 2; ++i) inv[i] = (float)std::pow((double)c.rope_base, -2.0 * i / D);
     e->inv_freq = e->mem.alloc_n<float>(D / 2);
     HIPC(hipMemcpyAsync(e->inv_freq, inv.data(), inv.size() * 4, hipMemcpyHostToDevice, s));
+    if (c.rope) e->rope_cs = static_cast<float2*>(e->mem.alloc((size_t)c.max_batch * e->M * (D / 2) * sizeof(float2)));
   }
   // working buffers sized for max_batch
   const int64_t Bm = e->Bmax, M = e->M, ab = e->act_bytes;

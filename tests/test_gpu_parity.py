@@ -1,6 +1,8 @@
 """GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
 same seeded inputs.  Bars: max-abs <= tol * max(1, rms(oracle)) with tol
 1e-4 (fp32 path), 2e-2 (bf16), 5e-2 (fp8 weights)."""
+import os
+
 import numpy as np
 import pytest
 
@@ -89,3 +91,21 @@ def test_full_size_batch64_fp8_sampled():
     ref = oracle.denoise(cfg, case.weights, pre, pl[sample], case.noise[sample], case.timesteps,
                          case.state[sample], decoded=W, slots=list(range(len(sample))))
     compare(f"pi0_fp8_b64 requests {sample}", gpu[sample], ref, cfg)
+
+
+@pytest.mark.parametrize("wdt", ["bf16", "fp8"])
+@pytest.mark.parametrize("tile", ["ring", "strided"])
+def test_many_row_gemm_tiles(tile, wdt):
+    """Both many-row GEMM kernels, forced in turn for every projection: 357
+    rows (a ragged last row tile), QKV 512 columns, GeGLU 2 x 512, output and
+    down projections 256 columns."""
+    cfg = small_cfg("pi0", n_q_heads=6, batch=7, weight_dtype=wdt)
+    print(f"[case] gemm tile {tile} {wdt}", flush=True)
+    case = wl.make_case(cfg, seed=4)
+    os.environ["PHYAI_GEMM_TILE"] = tile
+    try:
+        ex = _expert(cfg, case)
+        gpu = run_gpu(ex, case)
+    finally:
+        del os.environ["PHYAI_GEMM_TILE"]
+    compare(f"gemm tile {tile} {wdt}", gpu, _oracle(cfg, case), cfg)
