@@ -12,16 +12,18 @@
 // contiguous range with 16-byte loads, and V arrives already in the
 // key-contiguous order the P.V product needs.
 //
-// MFMA formulation: S^T = K Q^T and O^T = V^T P^T, so a query is always
-// the MFMA column (lane % 16): its softmax statistics live in the four lanes
-// l%16 == q (two cross-lane steps), and the probabilities leave the S^T
-// accumulators already laid out as the B operand of the P.V product (the
-// key order inside k is permuted identically on both operands).
+// MFMA formulation: S^T = K Q^T and O^T = V^T P^T on 32x32x16 bf16 MFMAs,
+// so a query is always the MFMA column (lane % 32): its softmax statistics
+// live in lanes l and l^32 (one cross-lane step), and the probabilities
+// leave the S^T accumulators already laid out as the B operand of the P.V
+// product (the key order inside a tile is permuted identically on both
+// operands).  The 32x32 shape issues half as many MFMA instructions per flop
+// as 16x16, which is what a single wave per SIMD needs to keep the matrix
+// core busy.
 //
-// Block: 4 waves x 32 query rows (two 16-row groups per wave, so every K/V
-// fragment read from LDS feeds two MFMAs); 64-key tiles double-buffered in
-// LDS and filled by direct global->LDS loads, the next tile in flight while
-// the current one is computed.
+// Block: 4 waves x 32 query rows; 64-key tiles double-buffered in LDS and
+// filled by direct global->LDS loads, the next tile in flight while the
+// current one is computed.
 // With n_split > 1 the key range is split over blocks, whose partials a
 // second kernel merges in a fixed order.
 #include "kernels.hpp"
@@ -57,9 +59,25 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_s_barrier();
 }
 
+// MFMA formulation (32x32x16 bf16): S^T = K Q^T and O^T = V^T P^T.  A wave
+// owns 32 query rows, one per MFMA column (lane % 32), so each lane keeps the
+// softmax state of one query; lanes l and l^32 share it.
+//
+// Key order inside a tile.  The S^T MFMA of key block kb (0, 1: 32 keys
+// each) reads its A-operand (K) row i = 8u + 4h + w (u < 4, h < 2, w < 4) from
+// key 32kb + 16(u/2) + 8h + 4(u%2) + w.  Accumulator v = 8t + j of lane l
+// (h = l/32) then holds key 32kb + 16t + 8h + j: the 8 consecutive keys that
+// lane supplies as the k-slice of the P.V MFMA for key step 2kb + t.  So P
+// needs no shuffle and each V^T fragment is one 16-byte LDS read.
+__device__ __forceinline__ int perm_row(int i) {
+  const int u = i >> 3, h = (i >> 2) & 1, w = i & 3;
+  return 16 * (u >> 1) + 8 * h + 4 * (u & 1) + w;
+}
+
 // LDS tiles, 16-byte chunks XOR-swizzled so that the MFMA fragment reads of
-// 16 lanes (16 rows, same column) fall in 16 different bank groups:
-//   K  [64 keys][D]:   chunk c of key row r sits at position c ^ (r & 15)
+// 16 lanes fall in 16 different bank groups (a 16-lane group reads 16
+// consecutive keys (K) or 16 consecutive d (V^T) at one chunk):
+//   K  [64 keys][D]:   chunk c of key row r sits at position c ^ kswz(r)
 //   Vt [D][64 keys]:   chunk c of row d sits at position c ^ ((d >> 1) & 7)
 template <int D>
 struct AttnTile {
@@ -67,117 +85,106 @@ struct AttnTile {
   bf16_t Vt[D * kKT];
 };
 
+// D >= 128: a chunk's bank group is its position mod 16; D == 64: two rows
+// share 256 bytes, the row's low bit separates them.
 template <int D>
-__device__ __forceinline__ int kswz(int r) { return (D / 8 >= 16) ? (r & 15) : (r & (D / 8 - 1)); }
+__device__ __forceinline__ int kswz(int r) { return D >= 128 ? (r & 15) : ((r >> 1) & 7); }
 __device__ __forceinline__ int vswz(int d) { return (d >> 1) & 7; }
 
-// One 64-key tile of the online-softmax attention for the wave's two query
-// groups, reading K and V^T from the LDS tile T.
+// The value of lane l ^ 32 combined with this lane's (gfx950 permlane32
+// swap: the two results are this lane's and its partner's value).
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// One 64-key tile of the online-softmax attention for the wave's 32 query
+// rows, reading K and V^T from the LDS tile T.
 template <int D>
-__device__ __forceinline__ void attn_tile(const AttnTile<D>& T, const bf16x8 (&qf)[2][D / 32],
-                                          f32x4 (&o)[2][D / 16], float (&m_run)[2], float (&l_run)[2],
-                                          int kt0, int kend, int plen, bool state0, bool state1, float sl2,
-                                          int lc, int lg) {
-  f32x4 st[2][4];
+__device__ __forceinline__ void attn_tile(const AttnTile<D>& T, const bf16x8 (&qf)[D / 16], f32x16 (&o)[D / 32],
+                                          float& m_run, float& l_run, int kt0, int kend, int plen, bool state_q,
+                                          float sl2, int lr, int hl) {
+  // S^T of the two 32-key blocks as two interleaved accumulator chains
+  f32x16 st[2];
 #pragma unroll
-  for (int kt = 0; kt < 4; ++kt) {
-    const int r = 16 * kt + lc;
-    bf16x8 kf[D / 32];
+  for (int v = 0; v < 16; ++v) { st[0][v] = 0.f; st[1][v] = 0.f; }
+  const int r0 = perm_row(lr), r1 = 32 + r0;
 #pragma unroll
-    for (int s = 0; s < D / 32; ++s)
-      kf[s] = *reinterpret_cast<const bf16x8*>(T.K + r * D + 8 * ((4 * s + lg) ^ kswz<D>(r)));
-    st[0][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-    st[1][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int s = 0; s < D / 32; ++s) {
-      st[0][kt] = mfma16x16x32(kf[s], qf[0][s], st[0][kt]);
-      st[1][kt] = mfma16x16x32(kf[s], qf[1][s], st[1][kt]);
-    }
+  for (int s = 0; s < D / 16; ++s) {
+    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(T.K + r0 * D + 8 * ((2 * s + hl) ^ kswz<D>(r0)));
+    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(T.K + r1 * D + 8 * ((2 * s + hl) ^ kswz<D>(r1)));
+    st[0] = mfma32x32x16(k0, qf[s], st[0]);
+    st[1] = mfma32x32x16(k1, qf[s], st[1]);
   }
   // Scores are masked only where a mask can bite: the tile holding the end
-  // of the key range, and state-token queries (wave-uniform test).
-  const bool need_mask = !(kt0 + kKT <= kend) || state0 || state1;
-  bf16x8 pf[2][2];
+  // of the key range, and state-token queries (wave-uniform test).  The
+  // scale (> 0) is applied after the max, inside the exponent.
+  const bool need_mask = !(kt0 + kKT <= kend) || state_q;
+  if (__ballot(need_mask)) {
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const bool state_q = c == 0 ? state0 : state1;
-    float sc[16];
-    float tmax = -INFINITY;
-    if (__ballot(need_mask)) {
+    for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int key = kt0 + 16 * kt + 4 * lg + v;
-          const bool ok = key < kend && (!state_q || key <= plen);
-          const float s = ok ? st[c][kt][v] * sl2 : -INFINITY;
-          sc[kt * 4 + v] = s;
-          tmax = fmaxf(tmax, s);
-        }
-    } else {
-#pragma unroll
-      for (int kt = 0; kt < 4; ++kt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const float s = st[c][kt][v] * sl2;
-          sc[kt * 4 + v] = s;
-          tmax = fmaxf(tmax, s);
-        }
-    }
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 16, kWave));
-    tmax = fmaxf(tmax, __shfl_xor(tmax, 32, kWave));
-    // Lazy rescaling: the running reference m only moves when the tile max
-    // exceeds it by more than 8 (log2 units), so exp2(s - m) <= 256 and the
-    // accumulators are rescaled only a few times per key range.
-    if (__ballot(tmax > m_run[c] + 8.f)) {
-      const float m_new = fmaxf(m_run[c], tmax);
-      const float alpha = __builtin_amdgcn_exp2f(m_run[c] - m_new);
-      m_run[c] = m_new;
-      l_run[c] *= alpha;
-#pragma unroll
-      for (int i = 0; i < D / 16; ++i) o[c][i] *= alpha;
-    }
-    float p[16], psum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      p[i] = __builtin_amdgcn_exp2f(sc[i] - m_run[c]);
-      psum += p[i];
-    }
-    l_run[c] += psum;
-#pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      uint4 w;
-      w.x = pack_bf16x2(p[8 * h + 0], p[8 * h + 1]);
-      w.y = pack_bf16x2(p[8 * h + 2], p[8 * h + 3]);
-      w.z = pack_bf16x2(p[8 * h + 4], p[8 * h + 5]);
-      w.w = pack_bf16x2(p[8 * h + 6], p[8 * h + 7]);
-      pf[c][h] = as_bf16x8(w);
-    }
+      for (int v = 0; v < 16; ++v) {
+        const int key = kt0 + 32 * kb + 16 * (v >> 3) + 8 * hl + (v & 7);
+        const bool ok = key < kend && (!state_q || key <= plen);
+        st[kb][v] = ok ? st[kb][v] : -INFINITY;
+      }
   }
-  // V^T fragments, four d-tiles per batch
-  const int vo = 4 * (lg & 1);
+  float mx[8];
 #pragma unroll
-  for (int d0 = 0; d0 < D / 16; d0 += 4) {
-    bf16x8 vf[4][2];
+  for (int i = 0; i < 8; ++i)
+    mx[i] = fmaxf(fmaxf(st[0][2 * i], st[0][2 * i + 1]), fmaxf(st[1][2 * i], st[1][2 * i + 1]));
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int d = 16 * (d0 + j) + lc;
-      const bf16_t* vrow = T.Vt + d * kKT + vo;
+  for (int w = 4; w > 0; w >>= 1)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        const int c0 = 4 * h + (lg >> 1);
-        const uint2 lo = *reinterpret_cast<const uint2*>(vrow + 8 * (c0 ^ vswz(d)));
-        const uint2 hi = *reinterpret_cast<const uint2*>(vrow + 8 * ((c0 + 2) ^ vswz(d)));
-        vf[j][h] = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-      }
+    for (int i = 0; i < w; ++i) mx[i] = fmaxf(mx[i], mx[i + w]);
+  const float tmax = pair_max(mx[0]) * sl2;
+  // Lazy rescaling: the running reference m only moves when the tile max
+  // exceeds it by more than 8 (log2 units), so exp2(s - m) <= 256 and the
+  // accumulators are rescaled only a few times per key range.
+  if (__ballot(tmax > m_run + 8.f)) {
+    const float m_new = fmaxf(m_run, tmax);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    l_run *= alpha;
+#pragma unroll
+    for (int i = 0; i < D / 32; ++i) o[i] *= alpha;
+  }
+  // P^T fragment of key step t (0..3): keys 16t + 8h + j = accumulator
+  // 8(t%2) + j of key block t/2
+  bf16x8 pf[4];
+  float ps[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    float pv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) pv[j] = __builtin_amdgcn_exp2f(fmaf(st[t >> 1][8 * (t & 1) + j], sl2, -m_run));
+    ps[t] = ((pv[0] + pv[1]) + (pv[2] + pv[3])) + ((pv[4] + pv[5]) + (pv[6] + pv[7]));
+    uint4 w;
+    w.x = pack_bf16x2(pv[0], pv[1]);
+    w.y = pack_bf16x2(pv[2], pv[3]);
+    w.z = pack_bf16x2(pv[4], pv[5]);
+    w.w = pack_bf16x2(pv[6], pv[7]);
+    pf[t] = as_bf16x8(w);
+  }
+  l_run += (ps[0] + ps[1]) + (ps[2] + ps[3]);
+  // O^T += V^T P^T: V^T fragment (d-block db, key step t) = row d = 32 db + lr,
+  // keys 16t + 8h .. +7, one 16-byte read; consecutive MFMAs go to different
+  // d-blocks
+#pragma unroll
+  for (int t = 0; t < 4; ++t) {
+    bf16x8 vf[D / 32];
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const int d = 32 * db + lr;
+      vf[db] = *reinterpret_cast<const bf16x8*>(T.Vt + d * kKT + 8 * ((2 * t + hl) ^ vswz(d)));
     }
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-      for (int h = 0; h < 2; ++h) {
-        o[0][d0 + j] = mfma16x16x32(vf[j][h], pf[0][h], o[0][d0 + j]);
-        o[1][d0 + j] = mfma16x16x32(vf[j][h], pf[1][h], o[1][d0 + j]);
-      }
+    for (int db = 0; db < D / 32; ++db) o[db] = mfma32x32x16(vf[db], pf[t], o[db]);
   }
 }
 
@@ -190,7 +197,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   constexpr int CPR = D / 8;                  // 16-byte chunks per K row
   constexpr int NLD = kKT * D / 8 / 256;      // loads per thread per operand per tile
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
-  const int lg = lane / 16, lc = lane % 16;
+  const int lr = lane % 32, hl = lane / 32;
   const int G = a.nq / a.nkv;
   const int rows = a.M * G;
   // 1-D grid, XCD-aware: blocks are dealt to the 8 XCDs round-robin, so the
@@ -215,21 +222,19 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   const bf16_t* Kb = static_cast<const bf16_t*>(a.K) + (int64_t)grp * a.ldk * D;
   const bf16_t* Vb = static_cast<const bf16_t*>(a.Vt) + (int64_t)grp * a.ldk * D;
 
-  int qr[2], qtok[2];
-  bool qv[2];
-  bf16x8 qf[2][D / 32];
+  // this lane's query row: B operand of S^T, Q[row][16s + 8h .. +7]
+  const int qr = rt * kRows + wave * 32 + lr;
+  const bool qv = qr < rows;
+  const int qtok = qv ? qr / G : 0;
+  const int qhead = kvh * G + (qv ? qr % G : 0);
+  bf16x8 qf[D / 16];
+  {
+    const bf16_t* qp = static_cast<const bf16_t*>(a.q) + (int64_t)(b * a.M + qtok) * a.ldq + qhead * D + 8 * hl;
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    qr[c] = rt * kRows + wave * 32 + c * 16 + lc;
-    qv[c] = qr[c] < rows;
-    qtok[c] = qv[c] ? qr[c] / G : 0;
-    const int qhead = kvh * G + (qv[c] ? qr[c] % G : 0);
-    const bf16_t* qp = static_cast<const bf16_t*>(a.q) + (int64_t)(b * a.M + qtok[c]) * a.ldq + qhead * D + 8 * lg;
-#pragma unroll
-    for (int s = 0; s < D / 32; ++s) {
+    for (int s = 0; s < D / 16; ++s) {
       uint4 v = make_uint4(0, 0, 0, 0);
-      if (qv[c]) v = *reinterpret_cast<const uint4*>(qp + 32 * s);
-      qf[c][s] = as_bf16x8(v);
+      if (qv) v = *reinterpret_cast<const uint4*>(qp + 16 * s);
+      qf[s] = as_bf16x8(v);
     }
   }
   // Direct global->LDS loads of one tile (the key range always holds whole,
@@ -264,15 +269,14 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     PHYAI_WAIT_VMCNT(0);
   }
   const bool wave_active = rt * kRows + wave * 32 < rows;
-  const bool state0 = a.mask_mode == 1 && qtok[0] == 0;
-  const bool state1 = a.mask_mode == 1 && qtok[1] == 0;
+  const bool state_q = a.mask_mode == 1 && qtok == 0;
 
-  f32x4 o[2][D / 16];
+  f32x16 o[D / 32];
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+  for (int i = 0; i < D / 32; ++i)
 #pragma unroll
-    for (int i = 0; i < D / 16; ++i) o[c][i] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float m_run[2] = {-1e30f, -1e30f}, l_run[2] = {0.f, 0.f};
+    for (int v = 0; v < 16; ++v) o[i][v] = 0.f;
+  float m_run = -1e30f, l_run = 0.f;
   const float sl2 = a.scale * 1.4426950408889634f;
 
   for (int kt0 = kbeg; kt0 < kend; kt0 += 2 * kKT) {
@@ -286,7 +290,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         PHYAI_WAIT_VMCNT(0);
       }
       lds_barrier();
-      if (wave_active) attn_tile<D>(smA, qf, o, m_run, l_run, kt0, kend, plen, state0, state1, sl2, lc, lg);
+      if (wave_active) attn_tile<D>(smA, qf, o, m_run, l_run, kt0, kend, plen, state_q, sl2, lr, hl);
       lds_barrier();
       if (!more) break;
     }
@@ -301,32 +305,28 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         PHYAI_WAIT_VMCNT(0);
       }
       lds_barrier();
-      if (wave_active) attn_tile<D>(smB, qf, o, m_run, l_run, kt1, kend, plen, state0, state1, sl2, lc, lg);
+      if (wave_active) attn_tile<D>(smB, qf, o, m_run, l_run, kt1, kend, plen, state_q, sl2, lr, hl);
       lds_barrier();
     }
   }
 
-#pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    l_run[c] += __shfl_xor(l_run[c], 16, kWave);
-    l_run[c] += __shfl_xor(l_run[c], 32, kWave);
-  }
+  // lanes l and l^32 hold the same query over different keys
+  l_run = pair_sum(l_run);
 
+  // accumulator v of o[db]: d = 32 db + 8(v/4) + 4h + v%4 -> four consecutive d per (db, v/4)
   if (a.n_split == 1) {
+    if (!qv) return;
+    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+    bf16_t* op = static_cast<bf16_t*>(a.out) + (int64_t)(b * a.M + qtok) * a.ldo + qhead * D + 4 * hl;
 #pragma unroll
-    for (int c = 0; c < 2; ++c) {
-      if (!qv[c]) continue;
-      const float inv = l_run[c] > 0.f ? 1.f / l_run[c] : 0.f;
-      const int qhead = kvh * G + qr[c] % G;
-      bf16_t* op = static_cast<bf16_t*>(a.out) + (int64_t)(b * a.M + qtok[c]) * a.ldo + qhead * D + 4 * lg;
+    for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-      for (int dt = 0; dt < D / 16; ++dt) {
+      for (int u = 0; u < 4; ++u) {
         uint2 w;
-        w.x = pack_bf16x2(o[c][dt][0] * inv, o[c][dt][1] * inv);
-        w.y = pack_bf16x2(o[c][dt][2] * inv, o[c][dt][3] * inv);
-        *reinterpret_cast<uint2*>(op + 16 * dt) = w;
+        w.x = pack_bf16x2(o[db][4 * u + 0] * inv, o[db][4 * u + 1] * inv);
+        w.y = pack_bf16x2(o[db][4 * u + 2] * inv, o[db][4 * u + 3] * inv);
+        *reinterpret_cast<uint2*>(op + 32 * db + 8 * u) = w;
       }
-    }
     return;
   }
 
@@ -335,22 +335,21 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   const int64_t tile_id = (int64_t)grp * ntiles + rt;
   bf16_t* obase = reinterpret_cast<bf16_t*>(a.part) + tile_id * a.n_split * (int64_t)kRows * D;
   float* mlbase = a.part + (a.part_ml_off) + tile_id * a.n_split * (int64_t)kRows * 2;
+  const int lrow = wave * 32 + lr;
+  const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
+  bf16_t* op = obase + ((int64_t)split * kRows + lrow) * D + 4 * hl;
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
-    const int lrow = wave * 32 + c * 16 + lc;
-    const float inv = l_run[c] > 0.f ? 1.f / l_run[c] : 0.f;
-    bf16_t* op = obase + ((int64_t)split * kRows + lrow) * D + 4 * lg;
+  for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-    for (int dt = 0; dt < D / 16; ++dt) {
+    for (int u = 0; u < 4; ++u) {
       uint2 w;
-      w.x = pack_bf16x2(o[c][dt][0] * inv, o[c][dt][1] * inv);
-      w.y = pack_bf16x2(o[c][dt][2] * inv, o[c][dt][3] * inv);
-      *reinterpret_cast<uint2*>(op + 16 * dt) = w;
+      w.x = pack_bf16x2(o[db][4 * u + 0] * inv, o[db][4 * u + 1] * inv);
+      w.y = pack_bf16x2(o[db][4 * u + 2] * inv, o[db][4 * u + 3] * inv);
+      *reinterpret_cast<uint2*>(op + 32 * db + 8 * u) = w;
     }
-    if (lg == 0) {
-      mlbase[((int64_t)split * kRows + lrow) * 2] = m_run[c];
-      mlbase[((int64_t)split * kRows + lrow) * 2 + 1] = l_run[c];
-    }
+  if (hl == 0) {
+    mlbase[((int64_t)split * kRows + lrow) * 2] = m_run;
+    mlbase[((int64_t)split * kRows + lrow) * 2 + 1] = l_run;
   }
 }
 
