@@ -28,6 +28,8 @@
 // second kernel merges in a fixed order.
 #include "kernels.hpp"
 
+#include <type_traits>
+
 namespace phyai {
 
 namespace {
@@ -354,9 +356,11 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
 }
 
 // Merge the key splits of one query row per wave: o = sum_s w_s o_s / sum_s w_s
-// with w_s = l_s 2^(m_s - max m); every split's data is requested at once.
-// Lane i merges elements 4i .. 4i+3 (lanes >= D/4 idle).
-template <int D>
+// with w_s = l_s 2^(m_s - max m).  Lane i merges elements 4i .. 4i+3 (lanes
+// >= D/4 idle).  All NS slots are loaded unconditionally (slots past
+// n_split re-read the last split and get weight 0), so every load is in
+// flight at once instead of one round trip per split.
+template <int D, int NS>
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int G = a.nq / a.nkv;
@@ -370,32 +374,28 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
   const int64_t tile_id = (int64_t)grp * ntiles + rt;
   const bf16_t* obase = reinterpret_cast<const bf16_t*>(a.part) + tile_id * a.n_split * (int64_t)kRows * D;
   const float* mlbase = a.part + a.part_ml_off + tile_id * a.n_split * (int64_t)kRows * 2;
-  constexpr int SMAX = 16;
-  float m[SMAX], l[SMAX];
-  uint2 v[SMAX];
+  const int n = a.n_split;
+  float2 ml[NS];
+  uint2 v[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int se = s < n ? s : n - 1;
+    ml[s] = *reinterpret_cast<const float2*>(mlbase + ((int64_t)se * kRows + lrow) * 2);
+    v[s] = *reinterpret_cast<const uint2*>(obase + ((int64_t)se * kRows + lrow) * D + 4 * lane);
+  }
   float mmax = -1e30f;
 #pragma unroll
-  for (int s = 0; s < SMAX; ++s) {
-    if (s < a.n_split) {
-      const float* ml = mlbase + ((int64_t)s * kRows + lrow) * 2;
-      m[s] = ml[0];
-      l[s] = ml[1];
-      v[s] = *reinterpret_cast<const uint2*>(obase + ((int64_t)s * kRows + lrow) * D + 4 * lane);
-      mmax = fmaxf(mmax, m[s]);
-    }
-  }
+  for (int s = 0; s < NS; ++s) mmax = fmaxf(mmax, s < n ? ml[s].x : -1e30f);
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   float lsum = 0.f;
 #pragma unroll
-  for (int s = 0; s < SMAX; ++s) {
-    if (s < a.n_split) {
-      const float w = l[s] * exp2f(m[s] - mmax);
-      lsum += w;
-      acc[0] += w * __uint_as_float(v[s].x << 16);
-      acc[1] += w * __uint_as_float(v[s].x & 0xffff0000u);
-      acc[2] += w * __uint_as_float(v[s].y << 16);
-      acc[3] += w * __uint_as_float(v[s].y & 0xffff0000u);
-    }
+  for (int s = 0; s < NS; ++s) {
+    const float w = s < n ? ml[s].y * __builtin_amdgcn_exp2f(ml[s].x - mmax) : 0.f;
+    lsum += w;
+    acc[0] = fmaf(w, __uint_as_float(v[s].x << 16), acc[0]);
+    acc[1] = fmaf(w, __uint_as_float(v[s].x & 0xffff0000u), acc[1]);
+    acc[2] = fmaf(w, __uint_as_float(v[s].y << 16), acc[2]);
+    acc[3] = fmaf(w, __uint_as_float(v[s].y & 0xffff0000u), acc[3]);
   }
   const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
   const int tok = r / G, qhead = kvh * G + r % G;
@@ -534,9 +534,15 @@ void attention_bf16(const AttnArgs& a0, hipStream_t s) {
   else if (a.D == 64) hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, s, a);
   if (a.n_split > 1) {
     dim3 g2((rows + 3) / 4, a.B * a.nkv);
-    if (a.D == 256) hipLaunchKernelGGL(attn_combine_kernel<256>, g2, dim3(256), 0, s, a);
-    else if (a.D == 128) hipLaunchKernelGGL(attn_combine_kernel<128>, g2, dim3(256), 0, s, a);
-    else if (a.D == 64) hipLaunchKernelGGL(attn_combine_kernel<64>, g2, dim3(256), 0, s, a);
+    auto comb = [&](auto dtag) {
+      constexpr int DD = decltype(dtag)::value;
+      if (a.n_split <= 4) hipLaunchKernelGGL((attn_combine_kernel<DD, 4>), g2, dim3(256), 0, s, a);
+      else if (a.n_split <= 8) hipLaunchKernelGGL((attn_combine_kernel<DD, 8>), g2, dim3(256), 0, s, a);
+      else hipLaunchKernelGGL((attn_combine_kernel<DD, 16>), g2, dim3(256), 0, s, a);
+    };
+    if (a.D == 256) comb(std::integral_constant<int, 256>{});
+    else if (a.D == 128) comb(std::integral_constant<int, 128>{});
+    else if (a.D == 64) comb(std::integral_constant<int, 64>{});
   }
 }
 

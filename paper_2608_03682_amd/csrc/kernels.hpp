@@ -277,7 +277,7 @@ struct ReadoutArgs {
   PendingResid pend;        // residual still pending from the last block
   float eps; int mode;
   const float* mul; const float* shift;   // final norm: * (1 + mul) + shift
-  const float* out_w;       // [d][A] fp32
+  const float* out_w;       // [A][d] fp32 (transposed W_out)
   const float* out_b;       // [A]
   const float* dt;          // t_{k+1} - t_k (device scalar)
   float* x;                 // [B][H][A], updated in place

@@ -12,32 +12,47 @@ constexpr int kMaxPer = 8;   // d <= 2048 with 256 threads
 // n = normalise(h) * (1 + mul) + shift.  RMS: h / sqrt(mean(h^2) + eps);
 // LN: (h - mean) / sqrt(var + eps).  Statistics in fp32.
 // h row += gate * (sum of pending slices + bias), written back; returns the row in v.
+// Every load is requested before any is used (slots past pd.n re-read the
+// last slice and are dropped; element groups past d are skipped on a
+// wave-uniform test), so the row costs one memory round trip, not one per
+// slice.
 __device__ __forceinline__ void load_row_with_pending(float* hr, int64_t row, int d, const PendingResid& pd,
                                                       float (&v)[kMaxPer]) {
+  constexpr int kMaxSplit = 8;
+  const int n = pd.n;
+  float hv[kMaxPer], sl[kMaxPer][kMaxSplit], bs[kMaxPer], gt[kMaxPer];
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    if (256 * i >= d) break;
+    const int c = threadIdx.x + 256 * i;
+    const int cc = c < d ? c : d - 1;
+    hv[i] = hr[cc];
+    if (n > 0) {
+#pragma unroll
+      for (int s = 0; s < kMaxSplit; ++s) {
+        const int ss = s < n ? s : n - 1;
+        sl[i][s] = pd.part[ss * pd.stride + row * d + cc];
+      }
+      bs[i] = pd.bias ? pd.bias[cc] : 0.f;
+      gt[i] = pd.gate ? pd.gate[cc] : 1.f;
+    }
+  }
 #pragma unroll
   for (int i = 0; i < kMaxPer; ++i) {
     const int c = threadIdx.x + 256 * i;
-    v[i] = c < d ? hr[c] : 0.f;
-  }
-  if (pd.n > 0) {
-    // all slices of a column are requested before they are summed (in order)
-    constexpr int kMaxSplit = 8;
-#pragma unroll
-    for (int i = 0; i < kMaxPer; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      if (c < d) {
-        float sl[kMaxSplit];
-#pragma unroll
-        for (int s = 0; s < kMaxSplit; ++s) sl[s] = s < pd.n ? pd.part[s * pd.stride + row * d + c] : 0.f;
-        float t = 0.f;
-#pragma unroll
-        for (int s = 0; s < kMaxSplit; ++s) t += sl[s];
-        if (pd.bias) t += pd.bias[c];
-        if (pd.gate) t *= pd.gate[c];
-        v[i] += t;
-        hr[c] = v[i];
-      }
+    if (256 * i >= d) {
+      v[i] = 0.f;
+      continue;
     }
+    float x = hv[i];
+    if (n > 0) {
+      float t = 0.f;
+#pragma unroll
+      for (int s = 0; s < kMaxSplit; ++s) t += s < n ? sl[i][s] : 0.f;
+      x += (t + bs[i]) * gt[i];
+      if (c < d) hr[c] = x;
+    }
+    v[i] = c < d ? x : 0.f;
   }
 }
 
@@ -121,7 +136,7 @@ __global__ __launch_bounds__(256) void state_embed_kernel(const CallDesc* desc, 
 // One block per action row: final norm -> v = n W_out + b_out -> x += dt v.
 __global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs r) {
   __shared__ float nrm[2048];
-  __shared__ float red[4][64];
+  __shared__ float red[1][64];
   __shared__ float scratch[4];
   const int ar = blockIdx.x;                 // b*H + j
   const int b = ar / r.H, j = ar % r.H;
@@ -152,26 +167,47 @@ __global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs r) {
     }
   }
   __syncthreads();
-  // v = n W_out: thread (group gq of 4, column a) sums rows c = gq (mod 4);
-  // eight independent partial sums keep the W_out loads in flight
-  const int a = threadIdx.x % 64, gq = threadIdx.x / 64;
-  float part = 0.f;
-  if (a < r.A) {
-    float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    int c = gq;
-    for (; c + 28 < r.d; c += 32) {
+  // v = n W_out with W_out^T rows contiguous along d: wave w computes outputs
+  // a = w, w+4, ...; lane l takes 4 consecutive elements per 256 of each row
+  // (8 groups cover d <= 2048).  Outputs go in chunks of 4 per wave: all
+  // W_out loads of a chunk are requested before its first product, and a
+  // wave sum finishes each output.
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  constexpr int QA = 4;                      // outputs per chunk
+  constexpr int QC = kMaxPer;                // float4 groups per lane per row
+  for (int a0 = wave; a0 < r.A; a0 += 4 * QA) {
+    float4 w4[QA][QC];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) acc8[u] = fmaf(nrm[c + 4 * u], r.out_w[(int64_t)(c + 4 * u) * r.A + a], acc8[u]);
+    for (int q = 0; q < QA; ++q) {
+      const int a = a0 + 4 * q;
+      if (a >= r.A) break;
+      const float* wr = r.out_w + (int64_t)a * r.d + 4 * lane;
+#pragma unroll
+      for (int i = 0; i < QC; ++i)
+        if (256 * i < r.d) w4[q][i] = *reinterpret_cast<const float4*>(wr + 256 * i);
     }
-    for (; c < r.d; c += 4) acc8[0] = fmaf(nrm[c], r.out_w[(int64_t)c * r.A + a], acc8[0]);
 #pragma unroll
-    for (int u = 0; u < 8; ++u) part += acc8[u];
+    for (int q = 0; q < QA; ++q) {
+      const int a = a0 + 4 * q;
+      if (a >= r.A) break;
+      float acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < QC; ++i) {
+        if (256 * i >= r.d) break;
+        const int c = 4 * lane + 256 * i;
+        acc = fmaf(nrm[c], w4[q][i].x, acc);
+        acc = fmaf(nrm[c + 1], w4[q][i].y, acc);
+        acc = fmaf(nrm[c + 2], w4[q][i].z, acc);
+        acc = fmaf(nrm[c + 3], w4[q][i].w, acc);
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) red[0][a] = acc;
+    }
   }
-  red[gq][a] = part;
   __syncthreads();
   if (threadIdx.x < r.A) {
-    const float vel = red[0][a] + red[1][a] + red[2][a] + red[3][a] + r.out_b[a];
-    r.x[(int64_t)ar * r.A + a] += r.dt[0] * vel;
+    const float vel = red[0][threadIdx.x] + r.out_b[threadIdx.x];
+    r.x[(int64_t)ar * r.A + threadIdx.x] += r.dt[0] * vel;
   }
 }
 

@@ -317,7 +317,7 @@ template <typename T> EpiStore<T> store_epi(T* out, int ldo, const float* bias, 
 int attn_splits(int B, int rows, int nkv, int keys) {
   const int base = ((rows + 127) / 128) * B * nkv;     // blocks without a split
   int s = (256 + base - 1) / base;
-  const int cap = (keys + 127) / 128;                   // keep >= two 64-key tiles per split
+  const int cap = (keys + 63) / 64;                     // at least one 64-key tile per split
   if (s > cap) s = cap;
   if (s > 16) s = 16;                                   // the merge kernel takes up to 16
   return s < 1 ? 1 : s;
@@ -652,7 +652,16 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
 
   e->in_w = upload_f32(*e, P.get("in_w", A, d), s);
   e->in_b = vec("in_b", d);
-  e->out_w = upload_f32(*e, P.get("out_w", d, A), s);
+  {
+    // W_out is kept transposed, [A][d], so the readout streams rows along d
+    const phyai_tensor* t = P.get("out_w", d, A);
+    std::vector<float> wt((size_t)A * d);
+    for (int k = 0; k < d; ++k)
+      for (int a = 0; a < A; ++a) wt[(size_t)a * d + k] = elem_f32(t, (int64_t)k * A + a);
+    e->out_w = e->mem.alloc_n<float>(wt.size());
+    HIPC(hipMemcpyAsync(e->out_w, wt.data(), wt.size() * 4, hipMemcpyHostToDevice, s));
+    HIPC(hipStreamSynchronize(s));
+  }
   e->out_b = vec("out_b", A);
   if (c.state_token) {
     e->state_w = upload_f32(*e, P.get("state_w", A, d), s);
