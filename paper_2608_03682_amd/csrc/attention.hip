@@ -214,17 +214,8 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   const int grp = gi / a.n_split, split = gi % a.n_split;
   const int b = grp / a.nkv, kvh = grp % a.nkv;
 
-  const int plen = a.desc->prefix_len[b];
-  const int n_keys = (a.keys_from_prefix ? plen : 0) + a.n_suffix;
-  int chunk = (n_keys + a.n_split - 1) / a.n_split;
-  chunk = (chunk + kKT - 1) / kKT * kKT;
-  const int kbeg = split * chunk;
-  const int kend = min(n_keys, kbeg + chunk);
-
-  const bf16_t* Kb = static_cast<const bf16_t*>(a.K) + (int64_t)grp * a.ldk * D;
-  const bf16_t* Vb = static_cast<const bf16_t*>(a.Vt) + (int64_t)grp * a.ldk * D;
-
-  // this lane's query row: B operand of S^T, Q[row][16s + 8h .. +7]
+  // this lane's query row: B operand of S^T, Q[row][16s + 8h .. +7]; requested
+  // before the prefix length, whose load the key range and the tile loads wait on
   const int qr = rt * kRows + wave * 32 + lr;
   const bool qv = qr < rows;
   const int qtok = qv ? qr / G : 0;
@@ -239,6 +230,16 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
       qf[s] = as_bf16x8(v);
     }
   }
+  const int plen = a.desc->prefix_len[b];
+  const int n_keys = (a.keys_from_prefix ? plen : 0) + a.n_suffix;
+  int chunk = (n_keys + a.n_split - 1) / a.n_split;
+  chunk = (chunk + kKT - 1) / kKT * kKT;
+  const int kbeg = split * chunk;
+  const int kend = min(n_keys, kbeg + chunk);
+
+  const bf16_t* Kb = static_cast<const bf16_t*>(a.K) + (int64_t)grp * a.ldk * D;
+  const bf16_t* Vb = static_cast<const bf16_t*>(a.Vt) + (int64_t)grp * a.ldk * D;
+
   // Direct global->LDS loads of one tile (the key range always holds whole,
   // finite 64-key tiles).  Wave w's i-th load fills 1 KiB block 4i + w; the
   // per-thread source offsets (elements) do not depend on the tile.
@@ -337,6 +338,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   const int64_t tile_id = (int64_t)grp * ntiles + rt;
   bf16_t* obase = reinterpret_cast<bf16_t*>(a.part) + tile_id * a.n_split * (int64_t)kRows * D;
   float* mlbase = a.part + (a.part_ml_off) + tile_id * a.n_split * (int64_t)kRows * 2;
+  if (!qv) return;                           // rows past the tile's queries are never merged
   const int lrow = wave * 32 + lr;
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
   bf16_t* op = obase + ((int64_t)split * kRows + lrow) * D + 4 * hl;

@@ -205,6 +205,70 @@ __device__ __forceinline__ void bare_barrier() {
 }
 __device__ __forceinline__ int aswz(int row) { return (row >> 1) & 7; }
 
+// Epilogue of a wave's 64 x 64 tile (4 x 4 MFMA tiles, two pair tiles):
+// every load the epilogue needs (residual rows, biases, RoPE factors) is
+// requested for all 32 elements of the lane before the first store, so the
+// tile costs one memory round trip instead of one per element.
+// Epilogue of a 64x32 wave tile held as acc[mt][n16][v] (rows r0 + 16mt + 4lg
+// + v, pair tiles p0 and p0 + 1).  The element loads of MG row groups are
+// requested together before any of their stores; MG trades registers (and so
+// occupancy) against memory round trips.  MG = 0 finishes each element before
+// loading the next.
+template <int MG, class Epi>
+__device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const Epi& epi, const f32x4 (&acc)[4][4], int r0,
+                                              int p0, int lc, int lg) {
+  static_assert(MG == 0 || 4 % MG == 0, "row groups come in 4s");
+  if constexpr (MG == 0) {
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) {
+      const int p = p0 + pp;
+      const float s0c = g.scale ? g.scale[32 * p + lc] : 1.f;
+      const float s1c = g.scale ? g.scale[32 * p + 16 + lc] : 1.f;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = r0 + 16 * mt + 4 * lg + v;
+          if (row < g.R) epi(row, p, lc, acc[mt][2 * pp][v] * s0c, acc[mt][2 * pp + 1][v] * s1c);
+        }
+    }
+    return;
+  }
+  typename Epi::ColPre cpre[2];
+  float sc[2][2];
+#pragma unroll
+  for (int pp = 0; pp < 2; ++pp) {
+    cpre[pp] = epi.colpre(p0 + pp, lc);
+    sc[pp][0] = g.scale ? g.scale[32 * (p0 + pp) + lc] : 1.f;
+    sc[pp][1] = g.scale ? g.scale[32 * (p0 + pp) + 16 + lc] : 1.f;
+  }
+  constexpr int MS = MG > 0 ? MG : 4;
+#pragma unroll
+  for (int m0 = 0; m0 < 4; m0 += MS) {
+    typename Epi::Pre pre[2][MS][4];
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+      for (int mi = 0; mi < MS; ++mi)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = r0 + 16 * (m0 + mi) + 4 * lg + v;
+          if (row < g.R) pre[pp][mi][v] = epi.pre(row, p0 + pp, lc);
+        }
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+      for (int mi = 0; mi < MS; ++mi)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = r0 + 16 * (m0 + mi) + 4 * lg + v;
+          if (row < g.R)
+            epi.apply(row, p0 + pp, lc, cpre[pp], pre[pp][mi][v], acc[m0 + mi][2 * pp][v] * sc[pp][0],
+                      acc[m0 + mi][2 * pp + 1][v] * sc[pp][1]);
+        }
+  }
+}
+
 template <bool FP8>
 struct TiledSmem {
   bf16_t A[128 * 64];
@@ -307,22 +371,7 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
     }
 
     // epilogue: wave (wm, wn) holds rows mt0+64wm.., pair tiles pt0+2wn, +1
-#pragma unroll
-    for (int pp = 0; pp < 2; ++pp) {
-      const int p = pt0 + 2 * wn + pp;
-      float s0c = 1.f, s1c = 1.f;
-      if (g.scale) {
-        s0c = g.scale[32 * p + lc];
-        s1c = g.scale[32 * p + 16 + lc];
-      }
-#pragma unroll
-      for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) {
-          const int row = mt0 + 64 * wm + 16 * mt + 4 * lg + v;
-          if (row < g.R) epi(row, p, lc, acc[mt][2 * pp][v] * s0c, acc[mt][2 * pp + 1][v] * s1c);
-        }
-    }
+    tile_epilogue<4>(g, epi, acc, mt0 + 64 * wm, pt0 + 2 * wn, lc, lg);
   }
 }
 
@@ -432,22 +481,7 @@ __global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g, Epi epi) 
     compute(kb & 1);
   }
 
-#pragma unroll
-  for (int pp = 0; pp < 2; ++pp) {
-    const int p = pt0 + 2 * wn + pp;
-    float s0c = 1.f, s1c = 1.f;
-    if (g.scale) {
-      s0c = g.scale[32 * p + lc];
-      s1c = g.scale[32 * p + 16 + lc];
-    }
-#pragma unroll
-    for (int mt = 0; mt < 4; ++mt)
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = m0 + 64 * wm + 16 * mt + 4 * lg + v;
-        if (row < g.R) epi(row, p, lc, acc[mt][2 * pp][v] * s0c, acc[mt][2 * pp + 1][v] * s1c);
-      }
-  }
+  tile_epilogue<0>(g, epi, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
 }
 
 }  // namespace

@@ -67,6 +67,11 @@ struct PendingResid {
   const float* bias;
 };
 
+// Epilogues take a pair-tile element (row r, pair tile p, column c, the two
+// halves a0, a1).  Each has two phases so that a tile kernel can request the
+// loads of all its elements before any store: colpre() loads what depends on
+// the column only (once per pair tile), pre() what depends on the element,
+// apply() computes and stores; operator() is all three in turn.
 template <typename OutT>
 struct EpiStore {
   OutT* out; int ldo;
@@ -74,7 +79,20 @@ struct EpiStore {
   const float* rowvec;      // [N] added to every row, or null
   int act;                  // Act
   int grp, grp_stride, grp_off;   // row remap: (r/grp)*grp_stride + grp_off + r%grp (grp=0: identity)
-  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+  struct ColPre { float b[2], rv[2]; };
+  struct Pre {};
+  __device__ __forceinline__ ColPre colpre(int p, int c) const {
+    ColPre q;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int col = 32 * p + 16 * hf + c;
+      q.b[hf] = bias ? bias[col] : 0.f;
+      q.rv[hf] = rowvec ? rowvec[col] : 0.f;
+    }
+    return q;
+  }
+  __device__ __forceinline__ Pre pre(int, int, int) const { return Pre{}; }
+  __device__ __forceinline__ void apply(int r, int p, int c, const ColPre& q, const Pre&, float a0, float a1) const {
     int orow = r;
     if (grp > 0) orow = (r / grp) * grp_stride + grp_off + (r % grp);
     float v[2] = {a0, a1};
@@ -82,10 +100,13 @@ struct EpiStore {
     for (int hf = 0; hf < 2; ++hf) {
       const int col = 32 * p + 16 * hf + c;
       float t = v[hf];
-      if (bias) t += bias[col];
-      if (rowvec) t += rowvec[col];
+      if (bias) t += q.b[hf];
+      if (rowvec) t += q.rv[hf];
       ActIO<OutT>::store(out + (int64_t)orow * ldo + col, apply_act(act, t));
     }
+  }
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    apply(r, p, c, colpre(p, c), pre(r, p, c), a0, a1);
   }
 };
 
@@ -94,16 +115,37 @@ struct EpiResid {
   float* h; int ldh;
   const float* bias;
   const float* gate;
-  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+  struct ColPre { float b[2], g[2]; };
+  struct Pre { float h[2]; };
+  __device__ __forceinline__ ColPre colpre(int p, int c) const {
+    ColPre q;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int col = 32 * p + 16 * hf + c;
+      q.b[hf] = bias ? bias[col] : 0.f;
+      q.g[hf] = gate ? gate[col] : 1.f;
+    }
+    return q;
+  }
+  __device__ __forceinline__ Pre pre(int r, int p, int c) const {
+    Pre q;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) q.h[hf] = h[(int64_t)r * ldh + 32 * p + 16 * hf + c];
+    return q;
+  }
+  __device__ __forceinline__ void apply(int r, int p, int c, const ColPre& cq, const Pre& q, float a0, float a1) const {
     float v[2] = {a0, a1};
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       const int col = 32 * p + 16 * hf + c;
       float t = v[hf];
-      if (bias) t += bias[col];
-      if (gate) t *= gate[col];
-      h[(int64_t)r * ldh + col] += t;
+      if (bias) t += cq.b[hf];
+      if (gate) t *= cq.g[hf];
+      h[(int64_t)r * ldh + col] = q.h[hf] + t;
     }
+  }
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    apply(r, p, c, colpre(p, c), pre(r, p, c), a0, a1);
   }
 };
 
@@ -114,11 +156,18 @@ template <typename OutT>
 struct EpiGeglu {
   OutT* out; int ldo;
   OutT* lo;
-  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+  struct ColPre {};
+  struct Pre {};
+  __device__ __forceinline__ ColPre colpre(int, int) const { return ColPre{}; }
+  __device__ __forceinline__ Pre pre(int, int, int) const { return Pre{}; }
+  __device__ __forceinline__ void apply(int r, int p, int c, const ColPre&, const Pre&, float a0, float a1) const {
     const float v = gelu_tanh_f(a0) * a1;
     const int64_t i = (int64_t)r * ldo + 16 * p + c;
     ActIO<OutT>::store(out + i, v);
     if (lo) ActIO<OutT>::store(lo + i, v - ActIO<OutT>::round(v));
+  }
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    apply(r, p, c, ColPre{}, Pre{}, a0, a1);
   }
 };
 
@@ -138,25 +187,35 @@ struct EpiQkv {
   int keys_after_prefix;
   const float2* rope_cs;    // [rows][D/2]: (cos, sin) of position * base^(-2i/D)
   const CallDesc* desc;     // positions start at prefix_len[b]
-  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+  struct ColPre {};
+  struct Pre { float2 cs; int plen; };
+  __device__ __forceinline__ ColPre colpre(int, int) const { return ColPre{}; }
+  __device__ __forceinline__ Pre pre(int r, int p, int c) const {
+    const int tiles = D / 32;
+    const int head = p / tiles;
+    const int i = 16 * (p % tiles) + c;
+    Pre q;
+    q.cs = (rope && head < nq + nkv) ? rope_cs[(int64_t)r * (D / 2) + i] : make_float2(1.f, 0.f);
+    q.plen = head >= nq ? desc->prefix_len[r / M] : 0;
+    return q;
+  }
+  __device__ __forceinline__ void apply(int r, int p, int c, const ColPre&, const Pre& q, float a0, float a1) const {
     const int tiles = D / 32;
     const int head = p / tiles;
     const int i = 16 * (p % tiles) + c;
     const int b = r / M, tok = r % M;
-    const int plen = desc->prefix_len[b];
     if (rope && head < nq + nkv) {
-      const float2 cs = rope_cs[(int64_t)r * (D / 2) + i];
       const float x1 = a0, x2 = a1;
-      a0 = x1 * cs.x - x2 * cs.y;
-      a1 = x2 * cs.x + x1 * cs.y;
+      a0 = x1 * q.cs.x - x2 * q.cs.y;
+      a1 = x2 * q.cs.x + x1 * q.cs.y;
     }
     if (head < nq) {
-      OutT* dst = q + (int64_t)r * nq * D + head * D + i;
+      OutT* dst = this->q + (int64_t)r * nq * D + head * D + i;
       ActIO<OutT>::store(dst, a0);
       ActIO<OutT>::store(dst + D / 2, a1);
       return;
     }
-    const int key = (keys_after_prefix ? plen : 0) + tok;
+    const int key = (keys_after_prefix ? q.plen : 0) + tok;
     if (head < nq + nkv) {
       OutT* dst = kall + (((int64_t)b * nkv + (head - nq)) * ldk + key) * D + i;
       ActIO<OutT>::store(dst, a0);
@@ -167,6 +226,9 @@ struct EpiQkv {
       ActIO<OutT>::store(dst + (int64_t)(D / 2) * ldk, a1);
     }
   }
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    apply(r, p, c, ColPre{}, pre(r, p, c), a0, a1);
+  }
 };
 
 // K|V projection of feature rows r = b*P + key (identity packing): columns
@@ -175,7 +237,11 @@ template <typename OutT>
 struct EpiKV {
   OutT* kall; OutT* vt;
   int D, nkv, P, ldk;
-  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+  struct ColPre {};
+  struct Pre {};
+  __device__ __forceinline__ ColPre colpre(int, int) const { return ColPre{}; }
+  __device__ __forceinline__ Pre pre(int, int, int) const { return Pre{}; }
+  __device__ __forceinline__ void apply(int r, int p, int c, const ColPre&, const Pre&, float a0, float a1) const {
     const int b = r / P, key = r % P;
     float v[2] = {a0, a1};
 #pragma unroll
@@ -186,6 +252,9 @@ struct EpiKV {
       if (kv == 0) ActIO<OutT>::store(kall + (((int64_t)b * nkv + h) * ldk + key) * D + i, v[hf]);
       else ActIO<OutT>::store(vt + (((int64_t)b * nkv + h) * D + i) * ldk + key, v[hf]);
     }
+  }
+  __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
+    apply(r, p, c, ColPre{}, Pre{}, a0, a1);
   }
 };
 
