@@ -264,13 +264,13 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
       lds_dma16(vbase + voff[i], (lds_void*)(T.Vt + (4 * i + wv) * 512));
   };
 
-  // first tile in flight while the Q fragments land (loads retire in order)
-  if (kbeg < kend) {
-    issue(smA, kbeg);
-    PHYAI_WAIT_VMCNT(2 * NLD);
-  } else {
-    PHYAI_WAIT_VMCNT(0);
-  }
+  // first tile in flight while the Q fragments land.  The first tile's
+  // compute needs both, and a full wait here is also what tells the compiler
+  // that the Q fragments are complete: it cannot count the asm tile loads,
+  // so after a partial wait it would put a full wait in front of the first
+  // MFMA of every tile, stalling each tile on the prefetch of the next.
+  if (kbeg < kend) issue(smA, kbeg);
+  PHYAI_WAIT_VMCNT(0);
   const bool wave_active = rt * kRows + wave * 32 < rows;
   const bool state_q = a.mask_mode == 1 && qtok == 0;
 
@@ -316,32 +316,16 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   // lanes l and l^32 hold the same query over different keys
   l_run = pair_sum(l_run);
 
-  // accumulator v of o[db]: d = 32 db + 8(v/4) + 4h + v%4 -> four consecutive d per (db, v/4)
-  if (a.n_split == 1) {
-    if (!qv) return;
-    const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-    bf16_t* op = static_cast<bf16_t*>(a.out) + (int64_t)(b * a.M + qtok) * a.ldo + qhead * D + 4 * hl;
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        uint2 w;
-        w.x = pack_bf16x2(o[db][4 * u + 0] * inv, o[db][4 * u + 1] * inv);
-        w.y = pack_bf16x2(o[db][4 * u + 2] * inv, o[db][4 * u + 3] * inv);
-        *reinterpret_cast<uint2*>(op + 32 * db + 8 * u) = w;
-      }
-    return;
-  }
-
-  // ---- split: write this block's partial (O normalised by its own l, as
-  // bf16, plus m and l); attn_combine_kernel merges the splits
-  const int64_t tile_id = (int64_t)grp * ntiles + rt;
-  bf16_t* obase = reinterpret_cast<bf16_t*>(a.part) + tile_id * a.n_split * (int64_t)kRows * D;
-  float* mlbase = a.part + (a.part_ml_off) + tile_id * a.n_split * (int64_t)kRows * 2;
-  if (!qv) return;                           // rows past the tile's queries are never merged
-  const int lrow = wave * 32 + lr;
+  // Output rows (final, or this split's partial normalised by its own l),
+  // bf16.  Accumulator v of o[db] holds d = 32 db + 8(v/4) + 4h + v%4, so a
+  // store straight from registers would write 16 bytes into each of 32 rows.
+  // Each wave instead stages its 32 x D rows in LDS (the tiles are free once
+  // the last barrier of the loop has passed; 16-byte chunk c of row r sits at
+  // c ^ (r mod CPR)) and writes whole rows: every store instruction then
+  // covers 64 / CPR complete rows.
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-  bf16_t* op = obase + ((int64_t)split * kRows + lrow) * D + 4 * hl;
+  bf16_t* stage = reinterpret_cast<bf16_t*>(&smA) + wave * 32 * D;
+  static_assert(sizeof(AttnTile<D>) >= 4 * 32 * D * sizeof(bf16_t), "staging needs 4 waves x 32 rows");
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -349,11 +333,35 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
       uint2 w;
       w.x = pack_bf16x2(o[db][4 * u + 0] * inv, o[db][4 * u + 1] * inv);
       w.y = pack_bf16x2(o[db][4 * u + 2] * inv, o[db][4 * u + 3] * inv);
-      *reinterpret_cast<uint2*>(op + 32 * db + 8 * u) = w;
+      const int c = 4 * db + u;
+      *reinterpret_cast<uint2*>(stage + lr * D + 8 * (c ^ (lr & (CPR - 1))) + 4 * hl) = w;
     }
-  if (hl == 0) {
-    mlbase[((int64_t)split * kRows + lrow) * 2] = m_run;
-    mlbase[((int64_t)split * kRows + lrow) * 2 + 1] = l_run;
+  // the rows are read back by other lanes of the same wave; LDS operations of
+  // one wave complete in order
+  __builtin_amdgcn_s_waitcnt(0xC07F);
+  constexpr int RPI = kWave / CPR;            // rows per store instruction
+  const int sr = lane / CPR, sc = lane % CPR;
+  const int64_t tile_id = (int64_t)grp * ntiles + rt;
+  bf16_t* obase = reinterpret_cast<bf16_t*>(a.part) + (tile_id * a.n_split + split) * (int64_t)kRows * D;
+#pragma unroll
+  for (int i = 0; i < 32 / RPI; ++i) {
+    const int r = RPI * i + sr;               // row within the wave
+    const uint4 w = *reinterpret_cast<const uint4*>(stage + r * D + 8 * (sc ^ (r & (CPR - 1))));
+    const int qrow = rt * kRows + wave * 32 + r;
+    if (a.n_split == 1) {
+      if (qrow < rows) {
+        const int tok = qrow / G, head = kvh * G + qrow % G;
+        *reinterpret_cast<uint4*>(static_cast<bf16_t*>(a.out) + (int64_t)(b * a.M + tok) * a.ldo + head * D +
+                                  8 * sc) = w;
+      }
+    } else {
+      // rows past the tile's queries are written too (never merged)
+      *reinterpret_cast<uint4*>(obase + (int64_t)(wave * 32 + r) * D + 8 * sc) = w;
+    }
+  }
+  if (a.n_split > 1 && hl == 0 && qv) {
+    float* mlbase = a.part + a.part_ml_off + tile_id * a.n_split * (int64_t)kRows * 2;
+    *reinterpret_cast<float2*>(mlbase + ((int64_t)split * kRows + wave * 32 + lr) * 2) = make_float2(m_run, l_run);
   }
 }
 
