@@ -81,10 +81,15 @@ __device__ __forceinline__ int perm_row(int i) {
 // consecutive keys (K) or 16 consecutive d (V^T) at one chunk):
 //   K  [64 keys][D]:   chunk c of key row r sits at position c ^ kswz(r)
 //   Vt [D][64 keys]:   chunk c of row d sits at position c ^ ((d >> 1) & 7)
+//
+// The two tile buffers are laid out [K0 | K1 | Vt0 | Vt1]: a fragment read of
+// buffer 1 is then the same per-lane address as buffer 0's plus a constant
+// that fits the LDS instruction's 16-bit offset, so one set of per-lane
+// addresses serves both buffers (at D = 256 each array is 32 KiB).
 template <int D>
-struct AttnTile {
-  bf16_t K[kKT * D];
-  bf16_t Vt[D * kKT];
+struct AttnLds {
+  bf16_t K[2][kKT * D];
+  bf16_t Vt[2][D * kKT];
 };
 
 // D >= 128: a chunk's bank group is its position mod 16; D == 64: two rows
@@ -104,10 +109,32 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
+#ifndef PHYAI_ATTN_PD
+#define PHYAI_ATTN_PD 4
+#endif
+
+// Instruction order of one MFMA loop of n products whose operands come from
+// LDS: the first pd fragment reads, then each MFMA followed by the next read,
+// so every read is issued pd MFMAs (32 cycles each) before its use.  With one
+// wave per SIMD nothing else hides LDS latency, and left to itself the
+// compiler keeps only two reads in flight.
+template <int N, int PD>
+__device__ __forceinline__ void lds_mfma_pipeline() {
+#pragma unroll
+  for (int i = 0; i < PD; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // DS read
+#pragma unroll
+  for (int i = 0; i < N - PD; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                                // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+  }
+#pragma unroll
+  for (int i = 0; i < PD; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+}
+
 // One 64-key tile of the online-softmax attention for the wave's 32 query
-// rows, reading K and V^T from the LDS tile T.
+// rows, reading K and V^T from the LDS tile (TK, TVt).
 template <int D>
-__device__ __forceinline__ void attn_tile(const AttnTile<D>& T, const bf16x8 (&qf)[D / 16], f32x16 (&o)[D / 32],
+__device__ __forceinline__ void attn_tile(const bf16_t* TK, const bf16_t* TVt, const bf16x8 (&qf)[D / 16], f32x16 (&o)[D / 32],
                                           float& m_run, float& l_run, int kt0, int kend, int plen, bool state_q,
                                           float sl2, int lr, int hl) {
   // S^T of the two 32-key blocks as two interleaved accumulator chains
@@ -115,13 +142,18 @@ __device__ __forceinline__ void attn_tile(const AttnTile<D>& T, const bf16x8 (&q
 #pragma unroll
   for (int v = 0; v < 16; ++v) { st[0][v] = 0.f; st[1][v] = 0.f; }
   const int r0 = perm_row(lr), r1 = 32 + r0;
+  bf16x8 kf[2][D / 16];
 #pragma unroll
   for (int s = 0; s < D / 16; ++s) {
-    const bf16x8 k0 = *reinterpret_cast<const bf16x8*>(T.K + r0 * D + 8 * ((2 * s + hl) ^ kswz<D>(r0)));
-    const bf16x8 k1 = *reinterpret_cast<const bf16x8*>(T.K + r1 * D + 8 * ((2 * s + hl) ^ kswz<D>(r1)));
-    st[0] = mfma32x32x16(k0, qf[s], st[0]);
-    st[1] = mfma32x32x16(k1, qf[s], st[1]);
+    kf[0][s] = *reinterpret_cast<const bf16x8*>(TK + r0 * D + 8 * ((2 * s + hl) ^ kswz<D>(r0)));
+    kf[1][s] = *reinterpret_cast<const bf16x8*>(TK + r1 * D + 8 * ((2 * s + hl) ^ kswz<D>(r1)));
   }
+#pragma unroll
+  for (int s = 0; s < D / 16; ++s) {
+    st[0] = mfma32x32x16(kf[0][s], qf[s], st[0]);
+    st[1] = mfma32x32x16(kf[1][s], qf[s], st[1]);
+  }
+  lds_mfma_pipeline<D / 8, PHYAI_ATTN_PD>();
   // Scores are masked only where a mask can bite: the tile holding the end
   // of the key range, and state-token queries (wave-uniform test).  The
   // scale (> 0) is applied after the max, inside the exponent.
@@ -177,25 +209,24 @@ __device__ __forceinline__ void attn_tile(const AttnTile<D>& T, const bf16x8 (&q
   // O^T += V^T P^T: V^T fragment (d-block db, key step t) = row d = 32 db + lr,
   // keys 16t + 8h .. +7, one 16-byte read; consecutive MFMAs go to different
   // d-blocks
+  bf16x8 vf[4][D / 32];
 #pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    bf16x8 vf[D / 32];
+  for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       const int d = 32 * db + lr;
-      vf[db] = *reinterpret_cast<const bf16x8*>(T.Vt + d * kKT + 8 * ((2 * t + hl) ^ vswz(d)));
+      vf[t][db] = *reinterpret_cast<const bf16x8*>(TVt + d * kKT + 8 * ((2 * t + hl) ^ vswz(d)));
     }
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) o[db] = mfma32x32x16(vf[db], pf[t], o[db]);
-  }
+  for (int t = 0; t < 4; ++t)
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) o[db] = mfma32x32x16(vf[t][db], pf[t], o[db]);
+  lds_mfma_pipeline<D / 8, PHYAI_ATTN_PD>();
 }
 
 template <int D>
 __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
-  // two separate LDS objects so that loads into one and reads of the other
-  // are visibly independent
-  __shared__ __attribute__((aligned(1024))) AttnTile<D> smA;
-  __shared__ __attribute__((aligned(1024))) AttnTile<D> smB;
+  __shared__ __attribute__((aligned(1024))) AttnLds<D> sm;
   constexpr int CPR = D / 8;                  // 16-byte chunks per K row
   constexpr int NLD = kKT * D / 8 / 256;      // loads per thread per operand per tile
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -253,15 +284,15 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     const int d = pos / 8, vc = pos % 8;
     voff[i] = d * a.ldk + 8 * (vc ^ vswz(d));
   }
-  auto issue = [&](AttnTile<D>& T, int kt0) {
+  auto issue = [&](int buf, int kt0) {
     const bf16_t* kbase = Kb + (int64_t)kt0 * D;
     const bf16_t* vbase = Vb + kt0;
 #pragma unroll
     for (int i = 0; i < NLD; ++i)
-      lds_dma16(kbase + koff[i], (lds_void*)(T.K + (4 * i + wv) * 512));
+      lds_dma16(kbase + koff[i], (lds_void*)(sm.K[buf] + (4 * i + wv) * 512));
 #pragma unroll
     for (int i = 0; i < NLD; ++i)
-      lds_dma16(vbase + voff[i], (lds_void*)(T.Vt + (4 * i + wv) * 512));
+      lds_dma16(vbase + voff[i], (lds_void*)(sm.Vt[buf] + (4 * i + wv) * 512));
   };
 
   // first tile in flight while the Q fragments land.  The first tile's
@@ -269,7 +300,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   // that the Q fragments are complete: it cannot count the asm tile loads,
   // so after a partial wait it would put a full wait in front of the first
   // MFMA of every tile, stalling each tile on the prefetch of the next.
-  if (kbeg < kend) issue(smA, kbeg);
+  if (kbeg < kend) issue(0, kbeg);
   PHYAI_WAIT_VMCNT(0);
   const bool wave_active = rt * kRows + wave * 32 < rows;
   const bool state_q = a.mask_mode == 1 && qtok == 0;
@@ -287,13 +318,13 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     {
       const bool more = kt0 + kKT < kend;
       if (more) {
-        issue(smB, kt0 + kKT);
+        issue(1, kt0 + kKT);
         PHYAI_WAIT_VMCNT(2 * NLD);
       } else {
         PHYAI_WAIT_VMCNT(0);
       }
       lds_barrier();
-      if (wave_active) attn_tile<D>(smA, qf, o, m_run, l_run, kt0, kend, plen, state_q, sl2, lr, hl);
+      if (wave_active) attn_tile<D>(sm.K[0], sm.Vt[0], qf, o, m_run, l_run, kt0, kend, plen, state_q, sl2, lr, hl);
       lds_barrier();
       if (!more) break;
     }
@@ -302,13 +333,13 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
       const int kt1 = kt0 + kKT;
       const bool more = kt1 + kKT < kend;
       if (more) {
-        issue(smA, kt1 + kKT);
+        issue(0, kt1 + kKT);
         PHYAI_WAIT_VMCNT(2 * NLD);
       } else {
         PHYAI_WAIT_VMCNT(0);
       }
       lds_barrier();
-      if (wave_active) attn_tile<D>(smB, qf, o, m_run, l_run, kt1, kend, plen, state_q, sl2, lr, hl);
+      if (wave_active) attn_tile<D>(sm.K[1], sm.Vt[1], qf, o, m_run, l_run, kt1, kend, plen, state_q, sl2, lr, hl);
       lds_barrier();
     }
   }
@@ -324,8 +355,8 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   // c ^ (r mod CPR)) and writes whole rows: every store instruction then
   // covers 64 / CPR complete rows.
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
-  bf16_t* stage = reinterpret_cast<bf16_t*>(&smA) + wave * 32 * D;
-  static_assert(sizeof(AttnTile<D>) >= 4 * 32 * D * sizeof(bf16_t), "staging needs 4 waves x 32 rows");
+  bf16_t* stage = reinterpret_cast<bf16_t*>(&sm) + wave * 32 * D;
+  static_assert(sizeof(AttnLds<D>) >= 4 * 32 * D * sizeof(bf16_t), "staging needs 4 waves x 32 rows");
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll

@@ -11,12 +11,68 @@
 
 #include <cstdlib>
 #include <cstring>
+#include <type_traits>
 
 namespace phyai {
 
 namespace {
 
 constexpr int kMT = 4;           // 16-row MFMA tiles per block (64 rows)
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef const __attribute__((address_space(1))) u32x4_t gu32x4_t;
+
+// 16-byte load through a global (not generic) pointer, which the compiler
+// counts with vmcnt alone
+__device__ __forceinline__ u32x4_t gload16(const void* p) { return *(gu32x4_t*)(p); }
+
+// One trip of the small-row GEMM: U k-blocks starting at kb, every operand
+// load issued (as global loads, so that the compiler can count them) before
+// the first MFMA.  Columns past N re-read the last pair tile.
+template <int U, bool FP8, bool SPLIT, int NT>
+__device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int lane, int kb,
+                                        const bf16_t* const (&arp)[kMT], const bf16_t* const (&alp)[kMT],
+                                        f32x4 (&acc)[kMT][NT]) {
+  bf16x8 b[U][NT][2];
+  bf16x8 a[U][kMT][2], al[U][kMT][2];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const int kk = kb + u;
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      const int p = min(pt0 + t / 2, g.NPT - 1), hf = t % 2;
+      const int64_t frag = ((int64_t)(p * nkb + kk) * 2 + hf) * kWave + lane;
+      if (FP8) {
+        const u32x4_t v = gload16(static_cast<const uint4*>(g.W) + frag);
+        b[u][t][0] = fp8x8_to_bf16x8(v.x, v.y);
+        b[u][t][1] = fp8x8_to_bf16x8(v.z, v.w);
+      } else {
+        const uint4* src = static_cast<const uint4*>(g.W) + frag * 2;
+        b[u][t][0] = __builtin_bit_cast(bf16x8, gload16(src));
+        b[u][t][1] = __builtin_bit_cast(bf16x8, gload16(src + 1));
+      }
+    }
+#pragma unroll
+    for (int mt = 0; mt < kMT; ++mt)
+#pragma unroll
+      for (int s = 0; s < 2; ++s) {
+        a[u][mt][s] = __builtin_bit_cast(bf16x8, gload16(arp[mt] + kk * 64 + s * 32));
+        if (SPLIT) al[u][mt][s] = __builtin_bit_cast(bf16x8, gload16(alp[mt] + kk * 64 + s * 32));
+      }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int u = 0; u < U; ++u)
+#pragma unroll
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int mt = 0; mt < kMT; ++mt)
+#pragma unroll
+        for (int t = 0; t < NT; ++t) {
+          acc[mt][t] = mfma16x16x32(a[u][mt][s], b[u][t][s], acc[mt][t]);
+          if (SPLIT) acc[mt][t] = mfma16x16x32(al[u][mt][s], b[u][t][s], acc[mt][t]);
+        }
+}
 
 // Small-row GEMM (batch-1 style): one block = 4 waves computing 64 rows x
 // 32*NP columns; the block's K range is split between the 4 waves, whose
@@ -39,21 +95,19 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   const int kb0 = zb0 + wave * (zb1 - zb0) / 4, kb1 = zb0 + (wave + 1) * (zb1 - zb0) / 4;
   const int arow = lane % 16, akg = lane / 16;
 
-  // rows this lane loads A for, with validity
+  // rows this lane loads A for.  Every load below is unconditional: rows past
+  // R read row 0, and columns past N re-read the last pair tile.  Row i of an
+  // MFMA result depends on row i of A only, so such rows (and rows past a
+  // request's prefix length, see the epilogue) are simply never used, which
+  // keeps the loads free of branches the compiler could not count through.
   const bf16_t* arp[kMT];
   const bf16_t* alp[kMT];
-  bool aval[kMT];
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt) {
     const int row = m0 + 16 * mt + arow;
-    bool ok = row < g.R;
-    if (ok && g.rows_per_req > 0) {
-      const int b = row / g.rows_per_req;
-      ok = (row % g.rows_per_req) < g.desc->prefix_len[b];
-    }
-    aval[mt] = ok;
-    arp[mt] = A + (int64_t)(ok ? row : 0) * g.lda + akg * 8;
-    alp[mt] = SPLIT ? static_cast<const bf16_t*>(g.A_lo) + (int64_t)(ok ? row : 0) * g.lda + akg * 8 : nullptr;
+    const int lr = row < g.R ? row : 0;
+    arp[mt] = A + (int64_t)lr * g.lda + akg * 8;
+    alp[mt] = SPLIT ? static_cast<const bf16_t*>(g.A_lo) + (int64_t)lr * g.lda + akg * 8 : nullptr;
   }
 
   f32x4 acc[kMT][NT];
@@ -62,59 +116,14 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // up to KU k-blocks per trip, every load of the trip issued before its
-  // MFMAs (blocks past the wave's range re-read a valid block with a zero A)
-  constexpr int KU = 4;
-  for (int kb = kb0; kb < kb1; kb += KU) {
-    bf16x8 b[KU][NT][2];
-    bf16x8 a[KU][kMT][2], al[KU][kMT][2];
-#pragma unroll
-    for (int u = 0; u < KU; ++u) {
-      const bool live = kb + u < kb1;
-      const int kk = live ? kb + u : kb;
-#pragma unroll
-      for (int t = 0; t < NT; ++t) {
-        const int p = pt0 + t / 2, hf = t % 2;
-        const int64_t frag = ((int64_t)(p * nkb + kk) * 2 + hf) * kWave + lane;
-        if (p >= g.NPT) {
-          b[u][t][0] = as_bf16x8(make_uint4(0, 0, 0, 0));
-          b[u][t][1] = b[u][t][0];
-        } else if (FP8) {
-          const uint4 v = static_cast<const uint4*>(g.W)[frag];
-          b[u][t][0] = fp8x8_to_bf16x8(v.x, v.y);
-          b[u][t][1] = fp8x8_to_bf16x8(v.z, v.w);
-        } else {
-          const uint4* src = static_cast<const uint4*>(g.W) + frag * 2;
-          b[u][t][0] = as_bf16x8(src[0]);
-          b[u][t][1] = as_bf16x8(src[1]);
-        }
-      }
-#pragma unroll
-      for (int mt = 0; mt < kMT; ++mt) {
-#pragma unroll
-        for (int s = 0; s < 2; ++s) {
-          uint4 v = make_uint4(0, 0, 0, 0), w = make_uint4(0, 0, 0, 0);
-          if (aval[mt] && live) {
-            v = *reinterpret_cast<const uint4*>(arp[mt] + kk * 64 + s * 32);
-            if (SPLIT) w = *reinterpret_cast<const uint4*>(alp[mt] + kk * 64 + s * 32);
-          }
-          a[u][mt][s] = as_bf16x8(v);
-          al[u][mt][s] = as_bf16x8(w);
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < KU; ++u)
-#pragma unroll
-      for (int s = 0; s < 2; ++s)
-#pragma unroll
-        for (int mt = 0; mt < kMT; ++mt)
-#pragma unroll
-          for (int t = 0; t < NT; ++t) {
-            acc[mt][t] = mfma16x16x32(a[u][mt][s], b[u][t][s], acc[mt][t]);
-            if (SPLIT) acc[mt][t] = mfma16x16x32(al[u][mt][s], b[u][t][s], acc[mt][t]);
-          }
+  // trips of 4, then 2, then 1 k-blocks, so no k-block is loaded twice
+  int kb = kb0;
+  for (; kb + 4 <= kb1; kb += 4) b1_trip<4, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc);
+  if (kb + 2 <= kb1) {
+    b1_trip<2, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc);
+    kb += 2;
   }
+  if (kb < kb1) b1_trip<1, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc);
 
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt)
@@ -129,6 +138,14 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   const int c = lane % 16;
   const int N = 32 * g.NPT;
   float* sp = g.split_out ? g.split_out + (int64_t)z * g.split_stride : nullptr;
+  // rows of a request past its prefix length (rows_per_req > 0) count as zero
+  bool rowok[4];
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int row = m0 + 16 * mt + 4 * akg + v;
+    rowok[v] = true;
+    if (g.rows_per_req > 0 && row < g.R) rowok[v] = (row % g.rows_per_req) < g.desc->prefix_len[row / g.rows_per_req];
+  }
 #pragma unroll
   for (int pp = 0; pp < NP; ++pp) {
     const int p = pt0 + pp;
@@ -142,6 +159,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
         s0 += red[w][(mt * NT + 2 * pp) * 4 + v][lane];
         s1 += red[w][(mt * NT + 2 * pp + 1) * 4 + v][lane];
       }
+      if (!rowok[v]) s0 = s1 = 0.f;       // what a zero A row gives
       if (g.scale) {
         s0 *= g.scale[32 * p + c];
         s1 *= g.scale[32 * p + 16 + c];
