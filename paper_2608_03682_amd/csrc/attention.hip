@@ -98,11 +98,22 @@ template <int D>
 __device__ __forceinline__ int kswz(int r) { return D >= 128 ? (r & 15) : ((r >> 1) & 7); }
 __device__ __forceinline__ int vswz(int d) { return (d >> 1) & 7; }
 
+// max(a, b, c) as one v_max3_f32.  fmaxf makes the compiler quiet each input
+// first (one extra instruction per operand); the scores reduced here are
+// never NaN (masked keys are -inf, padding keys are zero), so that step is
+// not needed.
+__device__ __forceinline__ float max3_f32(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
+}
+
 // The value of lane l ^ 32 combined with this lane's (gfx950 permlane32
 // swap: the two results are this lane's and its partner's value).
 __device__ __forceinline__ float pair_max(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+  const float a = __uint_as_float(r[0]), b = __uint_as_float(r[1]);
+  return max3_f32(a, b, b);
 }
 __device__ __forceinline__ float pair_sum(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
@@ -155,9 +166,11 @@ __device__ __forceinline__ void attn_tile(const bf16_t* TK, const bf16_t* TVt, c
   }
   lds_mfma_pipeline<D / 8, PHYAI_ATTN_PD>();
   // Scores are masked only where a mask can bite: the tile holding the end
-  // of the key range, and state-token queries (wave-uniform test).  The
-  // scale (> 0) is applied after the max, inside the exponent.
-  const bool need_mask = !(kt0 + kKT <= kend) || state_q;
+  // of the key range, and for state-token queries the tiles that reach past
+  // the prefix (wave-uniform test; a state-token row shares its wave with
+  // action rows, and the whole block waits for its slowest wave at every
+  // tile).  The scale (> 0) is applied after the max, inside the exponent.
+  const bool need_mask = !(kt0 + kKT <= kend) || (state_q && kt0 + kKT - 1 > plen);
   if (__ballot(need_mask)) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
@@ -168,15 +181,18 @@ __device__ __forceinline__ void attn_tile(const bf16_t* TK, const bf16_t* TVt, c
         st[kb][v] = ok ? st[kb][v] : -INFINITY;
       }
   }
-  float mx[8];
+  // tile max: four independent v_max3 chains over the 32 scores, then merged
+  float mx[4];
 #pragma unroll
-  for (int i = 0; i < 8; ++i)
-    mx[i] = fmaxf(fmaxf(st[0][2 * i], st[0][2 * i + 1]), fmaxf(st[1][2 * i], st[1][2 * i + 1]));
-#pragma unroll
-  for (int w = 4; w > 0; w >>= 1)
-#pragma unroll
-    for (int i = 0; i < w; ++i) mx[i] = fmaxf(mx[i], mx[i + w]);
-  const float tmax = pair_max(mx[0]) * sl2;
+  for (int c = 0; c < 4; ++c) {
+    const f32x16& a = st[c >> 1];
+    const int o = 8 * (c & 1);
+    float m = max3_f32(a[o], a[o + 1], a[o + 2]);
+    m = max3_f32(m, a[o + 3], a[o + 4]);
+    m = max3_f32(m, a[o + 5], a[o + 6]);
+    mx[c] = max3_f32(m, a[o + 7], a[o + 7]);
+  }
+  const float tmax = pair_max(max3_f32(mx[0], mx[1], max3_f32(mx[2], mx[3], mx[3]))) * sl2;
   // Lazy rescaling: the running reference m only moves when the tile max
   // exceeds it by more than 8 (log2 units), so exp2(s - m) <= 256 and the
   // accumulators are rescaled only a few times per key range.
