@@ -389,7 +389,8 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
     }
 
     // epilogue: wave (wm, wn) holds rows mt0+64wm.., pair tiles pt0+2wn, +1
-    tile_epilogue<4>(g, epi, acc, mt0 + 64 * wm, pt0 + 2 * wn, lc, lg);
+    if constexpr (Epi::kWaveTile) epi.wave_tile(g, acc, mt0 + 64 * wm, pt0 + 2 * wn, lc, lg);
+    else tile_epilogue<4>(g, epi, acc, mt0 + 64 * wm, pt0 + 2 * wn, lc, lg);
   }
 }
 
@@ -413,7 +414,7 @@ struct RingCfg {
 };
 
 template <class Epi, bool FP8>
-__global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g, Epi epi) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FP8 ? 3 : 2))) void gemm_ring_kernel(GemmArgs g, Epi epi) {
   typedef RingCfg<FP8> C;
   __shared__ __attribute__((aligned(1024))) uint8_t ring[2 * C::STAGE];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
@@ -499,7 +500,8 @@ __global__ __launch_bounds__(256, 1) void gemm_ring_kernel(GemmArgs g, Epi epi) 
     compute(kb & 1);
   }
 
-  tile_epilogue<0>(g, epi, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
+  if constexpr (Epi::kWaveTile) epi.wave_tile(g, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
+  else tile_epilogue<0>(g, epi, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
 }
 
 }  // namespace

@@ -4,6 +4,8 @@
 
 #include "common.hpp"
 
+#include <type_traits>
+
 namespace phyai {
 
 constexpr int kMaxBatch = 512;
@@ -74,6 +76,7 @@ struct PendingResid {
 // apply() computes and stores; operator() is all three in turn.
 template <typename OutT>
 struct EpiStore {
+  static constexpr bool kWaveTile = false;
   OutT* out; int ldo;
   const float* bias;        // [N] or null
   const float* rowvec;      // [N] added to every row, or null
@@ -112,6 +115,7 @@ struct EpiStore {
 
 // h[r][col] += gate[col] * (acc + bias[col])
 struct EpiResid {
+  static constexpr bool kWaveTile = false;
   float* h; int ldh;
   const float* bias;
   const float* gate;
@@ -154,6 +158,7 @@ struct EpiResid {
 // out + lo carries about 16 significant bits into the next GEMM.
 template <typename OutT>
 struct EpiGeglu {
+  static constexpr bool kWaveTile = false;
   OutT* out; int ldo;
   OutT* lo;
   struct ColPre {};
@@ -179,6 +184,7 @@ struct EpiGeglu {
 // [b][kvh][D][key]) at key = (prefix_len[b] if keys_after_prefix) + token.
 template <typename OutT>
 struct EpiQkv {
+  static constexpr bool kWaveTile = true;   // see wave_tile
   OutT* q; OutT* kall; OutT* vt;
   int D, nq, nkv;
   int rope;
@@ -229,12 +235,92 @@ struct EpiQkv {
   __device__ __forceinline__ void operator()(int r, int p, int c, float a0, float a1) const {
     apply(r, p, c, ColPre{}, pre(r, p, c), a0, a1);
   }
+
+  // Epilogue of a wave's 64 x 64 tile of a many-row GEMM: rows r0 + 16mt +
+  // 4lg + v, pair tiles p0 (even) and p0 + 1, which always belong to one
+  // head, so whether the tile is Q, K or V (and whether it is rotated) is
+  // known once per tile.  Per group of four rows every RoPE factor and
+  // prefix length is requested before the group's stores; the per-element
+  // form above would wait for each element's loads in turn.  Tiles that
+  // reach past R take the per-element form.
+  __device__ __forceinline__ void wave_tile(const GemmArgs& g, const f32x4 (&acc)[4][4], int r0, int p0, int lc,
+                                            int lg) const {
+    const int tiles = D / 32;
+    const int head = p0 / tiles;
+    float sc[2][2];
+#pragma unroll
+    for (int pp = 0; pp < 2; ++pp) {
+      sc[pp][0] = g.scale ? g.scale[32 * (p0 + pp) + lc] : 1.f;
+      sc[pp][1] = g.scale ? g.scale[32 * (p0 + pp) + 16 + lc] : 1.f;
+    }
+    if (r0 + 64 > g.R) {
+#pragma unroll
+      for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int row = r0 + 16 * mt + 4 * lg + v;
+            if (row < g.R)
+              (*this)(row, p0 + pp, lc, acc[mt][2 * pp][v] * sc[pp][0], acc[mt][2 * pp + 1][v] * sc[pp][1]);
+          }
+      return;
+    }
+    auto emit = [&](auto kind) {
+      constexpr int KIND = decltype(kind)::value;     // 0: q, 1: k, 2: v
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt) {
+        float2 cs[2][4];
+        int key[4];
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+          const int row = r0 + 16 * mt + 4 * lg + v;
+#pragma unroll
+          for (int pp = 0; pp < 2; ++pp) {
+            const int i = 16 * ((p0 + pp) % tiles) + lc;
+            cs[pp][v] = (KIND < 2 && rope) ? rope_cs[(int64_t)row * (D / 2) + i] : make_float2(1.f, 0.f);
+          }
+          key[v] = KIND > 0 ? (keys_after_prefix ? desc->prefix_len[row / M] : 0) + row % M : 0;
+        }
+#pragma unroll
+        for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int row = r0 + 16 * mt + 4 * lg + v;
+            const int i = 16 * ((p0 + pp) % tiles) + lc;
+            const float x1 = acc[mt][2 * pp][v] * sc[pp][0], x2 = acc[mt][2 * pp + 1][v] * sc[pp][1];
+            float a0 = x1, a1 = x2;
+            if (KIND < 2 && rope) {
+              a0 = x1 * cs[pp][v].x - x2 * cs[pp][v].y;
+              a1 = x2 * cs[pp][v].x + x1 * cs[pp][v].y;
+            }
+            if (KIND == 0) {
+              OutT* dst = q + (int64_t)row * nq * D + head * D + i;
+              ActIO<OutT>::store(dst, a0);
+              ActIO<OutT>::store(dst + D / 2, a1);
+            } else if (KIND == 1) {
+              OutT* dst = kall + (((int64_t)(row / M) * nkv + (head - nq)) * ldk + key[v]) * D + i;
+              ActIO<OutT>::store(dst, a0);
+              ActIO<OutT>::store(dst + D / 2, a1);
+            } else {
+              OutT* dst = vt + (((int64_t)(row / M) * nkv + (head - nq - nkv)) * D + i) * ldk + key[v];
+              ActIO<OutT>::store(dst, a0);
+              ActIO<OutT>::store(dst + (int64_t)(D / 2) * ldk, a1);
+            }
+          }
+      }
+    };
+    if (head < nq) emit(std::integral_constant<int, 0>{});
+    else if (head < nq + nkv) emit(std::integral_constant<int, 1>{});
+    else emit(std::integral_constant<int, 2>{});
+  }
 };
 
 // K|V projection of feature rows r = b*P + key (identity packing): columns
 // [0, nkv*D) are K heads, [nkv*D, 2*nkv*D) V heads, stored like EpiQkv's k/v.
 template <typename OutT>
 struct EpiKV {
+  static constexpr bool kWaveTile = false;
   OutT* kall; OutT* vt;
   int D, nkv, P, ldk;
   struct ColPre {};
