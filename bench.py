@@ -108,8 +108,12 @@ def chunk_bytes(cfg, B, plen_sum):
 
 def time_calls(fn, steps, warmup):
     import torch
-    for _ in range(warmup):
+    short = steps + warmup <= 8            # counter passes: one progress line per call
+    for i in range(warmup):
         fn()
+        if short:
+            torch.cuda.synchronize()
+            _log(f"warm-up call {i + 1} done")
     torch.cuda.synchronize()
     evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     torch.cuda.synchronize()
@@ -118,6 +122,9 @@ def time_calls(fn, steps, warmup):
     for i in range(steps):
         fn()
         evs[i + 1].record()
+        if short:
+            torch.cuda.synchronize()
+            _log(f"timed call {i + 1} done")
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     per = np.array([evs[i].elapsed_time(evs[i + 1]) for i in range(steps)])
@@ -207,6 +214,60 @@ def measured_roofs():
     return out
 
 
+def leg_batch1(args, px, wl, K, W):
+    import torch
+    cfg = wl.CONFIGS["pi0_bf16_b1"]
+    _log(f"generating {cfg.name}")
+    case = wl.make_case(cfg, seed=args.seed)
+    ex = px.Expert(cfg, case.weights)
+    prefix, noise, state = _upload(case)
+    out = torch.empty_like(noise)
+    ex.prepare(1, cfg.n_steps)
+    fn = lambda: ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=out)
+    _log(f"timing {cfg.name}: {W} warmup + {K} timed")
+    wall, per = time_calls(fn, K, W)
+    ms = wall * 1e3 / K
+    assert np.isfinite(out.cpu().numpy()).all()
+    plen_sum = int(case.prefix_len.sum())
+    cb = chunk_bytes(cfg, 1, plen_sum)
+    roof, stages = None, {}
+    if not args.no_stages:
+        stages = time_stages(ex)
+        sb = stage_bytes_flops(cfg, 1, plen_sum)
+        dom = max(("qkv", "attn", "oproj", "mlp_up", "mlp_down"), key=lambda s: stages[s])
+        dom_bytes = sb[dom][0]
+        ach = dom_bytes / (stages[dom] * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(cfg.name, dom),
+                "kernel": dom, "bytes_per_launch": int(dom_bytes), "avg_us": round(stages[dom], 2)}
+    rec = {
+        "metric": "pi0-shape action-chunk latency ms @B=1 + chunks/s @B=64; % HBM / MFMA peak",
+        "value": round(ms, 4), "unit": "ms/chunk", "n_gpus": 1, "steps": K, "warmup": W,
+        "ms_per_step": round(ms, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+        "dtype": "bf16", "data": "synthetic (seeded N(0,0.02) weights, N(0,1) prefix K/V and noise)",
+        "config": {"workload": "pi0_bf16_b1: 18 layers, width 1024, 8 q heads + 1 kv head, head_dim 256, "
+                               "GeGLU 4096, RoPE, prefix 816, H=50 + state token, A=32, K=10 Euler steps, B=1",
+                   "batch": 1, "prefix_len": int(case.prefix_len[0]), "euler_steps": cfg.n_steps},
+        "latency_ms": {"mean": round(float(per.mean()), 4), "p50": round(float(np.median(per)), 4),
+                       "p99": round(float(np.percentile(per, 99)), 4)},
+        "stage_us_per_launch": {k: round(v, 2) for k, v in stages.items()},
+        "roofline": roof,
+        "chunk_roofline": {"bytes_per_chunk": int(cb), "achieved_GBs": round(cb / (ms * 1e-3) / 1e9, 1),
+                           "frac_of_hbm_peak": round(cb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
+    }
+    if not args.no_roofs:
+        _log("measuring the copy and GEMM roofs")
+        rec["measured_roofs"] = measured_roofs()
+    if not args.no_cpu_baseline:
+        _log("timing the CPU oracle baseline")
+        rec["cpu_baseline"] = cpu_baseline(cfg, case)
+    ex.close()
+    del prefix, noise, state, out, case
+    torch.cuda.empty_cache()
+
+    return rec
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -214,6 +275,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-batch64", action="store_true")
+    ap.add_argument("--no-batch1", action="store_true",
+                    help="only the batch-64 leg (for counter passes; the line then has no batch-1 value)")
+    ap.add_argument("--no-stages", action="store_true",
+                    help="skip the per-stage graph timings and the rooflines built on them (counter passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-roofs", action="store_true")
     args = ap.parse_args()
@@ -230,51 +295,12 @@ def main():
     K, W = args.steps, args.warmup
 
     # ---------------- batch 1, pi0-shaped, bf16 ----------------
-    cfg = wl.CONFIGS["pi0_bf16_b1"]
-    _log(f"generating {cfg.name}")
-    case = wl.make_case(cfg, seed=args.seed)
-    ex = px.Expert(cfg, case.weights)
-    prefix, noise, state = _upload(case)
-    out = torch.empty_like(noise)
-    ex.prepare(1, cfg.n_steps)
-    fn = lambda: ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=out)
-    _log(f"timing {cfg.name}: {W} warmup + {K} timed")
-    wall, per = time_calls(fn, K, W)
-    ms = wall * 1e3 / K
-    assert np.isfinite(out.cpu().numpy()).all()
-    stages = time_stages(ex)
-    plen_sum = int(case.prefix_len.sum())
-    sb = stage_bytes_flops(cfg, 1, plen_sum)
-    dom = max(("qkv", "attn", "oproj", "mlp_up", "mlp_down"), key=lambda s: stages[s])
-    dom_bytes = sb[dom][0]
-    ach = dom_bytes / (stages[dom] * 1e-6) / 1e9
-    cb = chunk_bytes(cfg, 1, plen_sum)
-    rec = {
-        "metric": "pi0-shape action-chunk latency ms @B=1 + chunks/s @B=64; % HBM / MFMA peak",
-        "value": round(ms, 4), "unit": "ms/chunk", "n_gpus": 1, "steps": K, "warmup": W,
-        "ms_per_step": round(ms, 4), "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
-        "dtype": "bf16", "data": "synthetic (seeded N(0,0.02) weights, N(0,1) prefix K/V and noise)",
-        "config": {"workload": "pi0_bf16_b1: 18 layers, width 1024, 8 q heads + 1 kv head, head_dim 256, "
-                               "GeGLU 4096, RoPE, prefix 816, H=50 + state token, A=32, K=10 Euler steps, B=1",
-                   "batch": 1, "prefix_len": int(case.prefix_len[0]), "euler_steps": cfg.n_steps},
-        "latency_ms": {"mean": round(float(per.mean()), 4), "p50": round(float(np.median(per)), 4),
-                       "p99": round(float(np.percentile(per, 99)), 4)},
-        "stage_us_per_launch": {k: round(v, 2) for k, v in stages.items()},
-        "roofline": {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(cfg.name, dom),
-                     "kernel": dom, "bytes_per_launch": int(dom_bytes), "avg_us": round(stages[dom], 2)},
-        "chunk_roofline": {"bytes_per_chunk": int(cb), "achieved_GBs": round(cb / (ms * 1e-3) / 1e9, 1),
-                           "frac_of_hbm_peak": round(cb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
-    }
-    if not args.no_roofs:
+    rec = {}
+    if not args.no_batch1:
+        rec = leg_batch1(args, px, wl, K, W)
+    elif not args.no_roofs:
         _log("measuring the copy and GEMM roofs")
-        rec["measured_roofs"] = measured_roofs()
-    if not args.no_cpu_baseline:
-        _log("timing the CPU oracle baseline")
-        rec["cpu_baseline"] = cpu_baseline(cfg, case)
-    ex.close()
-    del prefix, noise, state, out, case
-    torch.cuda.empty_cache()
+        rec["measured_roofs"] = measured_roofs()      # counter passes calibrate on its copy
 
     # ---------------- batch 64, ragged prefixes, fp8 weights ----------------
     if not args.no_batch64:
@@ -286,27 +312,31 @@ def main():
         out = torch.empty_like(noise)
         ex.prepare(cfg.batch, cfg.n_steps)
         fn = lambda: ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=out)
-        K64, W64 = max(5, K // 5), max(2, W // 5)
+        K64 = K if K < 5 else max(5, K // 5)
+        W64 = W if W < 2 else max(2, W // 5)
         _log(f"timing {cfg.name}: {W64} warmup + {K64} timed")
         wall, per = time_calls(fn, K64, W64)
         ms64 = wall * 1e3 / K64
         assert np.isfinite(out.cpu().numpy()).all()
-        stages = time_stages(ex, reps=2)
         plen_sum = int(case.prefix_len.sum())
         sb = stage_bytes_flops(cfg, cfg.batch, plen_sum)
-        dom = max(("qkv", "attn", "oproj", "mlp_up", "mlp_down"), key=lambda s: stages[s])
-        fl = sb[dom][1]
-        ach = fl / (stages[dom] * 1e-6) / 1e12
         chunk_flops = sum(v[1] for v in sb.values()) * cfg.n_layers * cfg.n_steps
+        roof, stages = None, {}
+        if not args.no_stages:
+            stages = time_stages(ex, reps=2)
+            dom = max(("qkv", "attn", "oproj", "mlp_up", "mlp_down"), key=lambda s: stages[s])
+            fl = sb[dom][1]
+            ach = fl / (stages[dom] * 1e-6) / 1e12
+            roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                    "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(cfg.name, dom),
+                    "kernel": dom, "flops_per_launch": int(fl), "avg_us": round(stages[dom], 2)}
         rec["batch64"] = {
             "workload": "pi0_fp8_b64: pi0 shape, B=64, ragged prefixes U[600,1000], fp8 e4m3 trunk weights "
                         "(per-output-channel scales), bf16 prefix K/V, K=10",
             "steps": K64, "warmup": W64, "ms_per_batch": round(ms64, 3),
             "chunks_per_s": round(cfg.batch / (ms64 * 1e-3), 1),
             "stage_us_per_launch": {k: round(v, 2) for k, v in stages.items()},
-            "roofline": {"bound": "mfma", "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                         "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
-                         "flops_per_launch": int(fl), "avg_us": round(stages[dom], 2)},
+            "roofline": roof,
             "batch_TFLOPs": round(chunk_flops / (ms64 * 1e-3) / 1e12, 1),
         }
         ex.close()

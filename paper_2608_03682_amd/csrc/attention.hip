@@ -147,7 +147,7 @@ __device__ __forceinline__ void lds_mfma_pipeline() {
 template <int D>
 __device__ __forceinline__ void attn_tile(const bf16_t* TK, const bf16_t* TVt, const bf16x8 (&qf)[D / 16], f32x16 (&o)[D / 32],
                                           float& m_run, float& l_run, int kt0, int kend, int plen, bool state_q,
-                                          float sl2, int lr, int hl) {
+                                          float sl2, int lr, int hl, bool first) {
   // S^T of the two 32-key blocks as two interleaved accumulator chains
   f32x16 st[2];
 #pragma unroll
@@ -196,13 +196,17 @@ __device__ __forceinline__ void attn_tile(const bf16_t* TK, const bf16_t* TVt, c
   // Lazy rescaling: the running reference m only moves when the tile max
   // exceeds it by more than 8 (log2 units), so exp2(s - m) <= 256 and the
   // accumulators are rescaled only a few times per key range.
+  // On the block's first tile nothing has been accumulated yet (o and l are
+  // zero), so only the reference moves.
   if (__ballot(tmax > m_run + 8.f)) {
     const float m_new = fmaxf(m_run, tmax);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
+    if (!first) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
 #pragma unroll
-    for (int i = 0; i < D / 32; ++i) o[i] *= alpha;
+      for (int i = 0; i < D / 32; ++i) o[i] *= alpha;
+    }
+    m_run = m_new;
   }
   // P^T fragment of key step t (0..3): keys 16t + 8h + j = accumulator
   // 8(t%2) + j of key block t/2
@@ -340,7 +344,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         PHYAI_WAIT_VMCNT(0);
       }
       lds_barrier();
-      if (wave_active) attn_tile<D>(sm.K[0], sm.Vt[0], qf, o, m_run, l_run, kt0, kend, plen, state_q, sl2, lr, hl);
+      if (wave_active) attn_tile<D>(sm.K[0], sm.Vt[0], qf, o, m_run, l_run, kt0, kend, plen, state_q, sl2, lr, hl, kt0 == kbeg);
       lds_barrier();
       if (!more) break;
     }
@@ -355,7 +359,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
         PHYAI_WAIT_VMCNT(0);
       }
       lds_barrier();
-      if (wave_active) attn_tile<D>(sm.K[1], sm.Vt[1], qf, o, m_run, l_run, kt1, kend, plen, state_q, sl2, lr, hl);
+      if (wave_active) attn_tile<D>(sm.K[1], sm.Vt[1], qf, o, m_run, l_run, kt1, kend, plen, state_q, sl2, lr, hl, false);
       lds_barrier();
     }
   }
