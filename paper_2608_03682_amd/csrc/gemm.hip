@@ -413,6 +413,38 @@ struct RingCfg {
   static constexpr int A_LD = A_KB / 4, B_LD = B_KB / 4;
 };
 
+// Tile of a ring-kernel block, XCD-aware.  Blocks are dealt to the 8 XCDs
+// round-robin and each XCD has its own L2.  The 128 x 128 tiles are ordered in
+// bands of kRingBand column tiles, row by row within a band, and XCD x takes
+// the x-th eighth of that order.  An XCD then streams the weights of about one
+// band and the activation rows its resident blocks share, instead of every
+// XCD fetching all of both.  Grid: 8 * ceil(tiles / 8) blocks; spare blocks
+// return false.  BANDED = false keeps the plain order (row tile fastest),
+// which spreads every column band over all XCDs: the QKV epilogue's cost
+// differs a lot between bands (transposed V stores), so it is better spread.
+constexpr int kRingBand = 8;
+__host__ __device__ inline int ring_tiles(const GemmArgs& g) { return ((g.R + 127) / 128) * (g.NPT / 4); }
+template <bool BANDED>
+__device__ __forceinline__ bool ring_tile(const GemmArgs& g, int& m0, int& pt0) {
+  const int mtiles = (g.R + 127) / 128, ntiles = g.NPT / 4;
+  if (!BANDED) {
+    if ((int)blockIdx.x >= mtiles * ntiles) return false;
+    m0 = (blockIdx.x % mtiles) * 128;
+    pt0 = (blockIdx.x / mtiles) * 4;
+    return true;
+  }
+  const int T = mtiles * ntiles, per = (T + 7) / 8;
+  const int j = blockIdx.x / 8;
+  const int t = (blockIdx.x % 8) * per + j;
+  if (j >= per || t >= T) return false;
+  const int band = t / (mtiles * kRingBand);
+  const int rem = t - band * mtiles * kRingBand;
+  const int bw = min(kRingBand, ntiles - band * kRingBand);
+  m0 = (rem / bw) * 128;
+  pt0 = (band * kRingBand + rem % bw) * 4;
+  return true;
+}
+
 template <class Epi, bool FP8>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FP8 ? 3 : 2))) void gemm_ring_kernel(GemmArgs g, Epi epi) {
   typedef RingCfg<FP8> C;
@@ -422,9 +454,8 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FP8 ? 3 : 2
   const int wm = wave >> 1, wn = wave & 1;
   const int lc = lane % 16, lg = lane / 16;
   const int nkb = g.K / 64;
-  const int mtiles = (g.R + 127) / 128;
-  const int m0 = (blockIdx.x % mtiles) * 128;
-  const int pt0 = (blockIdx.x / mtiles) * 4;
+  int m0, pt0;
+  if (!ring_tile<!Epi::kWaveTile>(g, m0, pt0)) return;
   const bf16_t* A = static_cast<const bf16_t*>(g.A);
   const uint8_t* W = static_cast<const uint8_t*>(g.W);
 
@@ -524,12 +555,13 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
     dim3 grid(g.NPT, (g.R + 15) / 16);
     hipLaunchKernelGGL(gemm_f32_kernel<Epi>, grid, dim3(256), 0, s, g, epi);
   } else if (g.R >= 256 && g.A_lo == nullptr && g.A_ind == nullptr && g.rows_per_req == 0 && g.NPT % 4 == 0) {
-    const int tiles = ((g.R + 127) / 128) * (g.NPT / 4);
+    const int tiles = ring_tiles(g);
     const char* force = getenv("PHYAI_GEMM_TILE");   // tests: "ring" / "strided" (read at enqueue time)
     const bool ring = force ? strcmp(force, "ring") == 0 : g.K <= 1024;
     if (ring) {
-      if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true>), dim3(tiles), dim3(256), 0, s, g, epi);
-      else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false>), dim3(tiles), dim3(256), 0, s, g, epi);
+      const dim3 rgrid(8 * ((tiles + 7) / 8));
+      if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true>), rgrid, dim3(256), 0, s, g, epi);
+      else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false>), rgrid, dim3(256), 0, s, g, epi);
     } else {
       dim3 grid(tiles < 512 ? tiles : 512);
       if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_tiled_kernel<Epi, true>), grid, dim3(256), 0, s, g, epi);
