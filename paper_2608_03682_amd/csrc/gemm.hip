@@ -223,6 +223,56 @@ __device__ __forceinline__ void bare_barrier() {
 }
 __device__ __forceinline__ int aswz(int row) { return (row >> 1) & 7; }
 
+// XCD-aware tile order of the many-row GEMMs.  Blocks are dealt to the 8 XCDs
+// round-robin and each XCD has its own L2, so with a plain order every XCD
+// streams all of A and all of W.  When W is the larger operand the 128 x 128
+// tiles are put in bands of kBand column tiles, row by row within a band,
+// and XCD x takes the x-th eighth of that order (block b runs position
+// (b % 8) * per + b / 8, plus multiples of the grid's share per XCD): an XCD
+// then streams about one band of W.  Otherwise (and for the QKV epilogue,
+// whose cost differs a lot between bands because of the transposed V
+// stores) the plain order is kept: row tile fastest over the block index.
+// (A row-major split by XCD for A-heavy shapes measured no better.)
+constexpr int kOrderPlain = 0, kOrderBands = 2;
+constexpr int kBand = 8;
+__host__ __device__ inline int gemm_tiles(const GemmArgs& g) { return ((g.R + 127) / 128) * (g.NPT / 4); }
+__host__ __device__ inline int tile_order(const GemmArgs& g, bool plain) {
+  if (plain) return kOrderPlain;
+  const int wb = g.kind == W_FP8 ? 1 : 2;
+  return (int64_t)32 * g.NPT * wb >= (int64_t)2 * g.R ? kOrderBands : kOrderPlain;
+}
+// Position t of the order -> (row tile, column tile).
+__device__ __forceinline__ void tile_at(int t, int mtiles, int ntiles, int order, int& mi, int& ni) {
+  if (order == kOrderPlain) {
+    mi = t % mtiles;
+    ni = t / mtiles;
+  } else {
+    const int band = t / (mtiles * kBand);
+    const int rem = t - band * mtiles * kBand;
+    const int bw = min(kBand, ntiles - band * kBand);
+    mi = rem / bw;
+    ni = band * kBand + rem % bw;
+  }
+}
+// The j-th tile of block b (j = 0, 1, ...) under the XCD split, -1 past the end;
+// the grid is a multiple of 8.
+__device__ __forceinline__ int xcd_tile(int b, int j, int grid, int T, int order) {
+  if (order == kOrderPlain) {
+    const int t = b + j * grid;
+    return t < T ? t : -1;
+  }
+  const int per = (T + 7) / 8;
+  const int k = b / 8 + j * (grid / 8);
+  const int t = (b % 8) * per + k;
+  return (k < per && t < T) ? t : -1;
+}
+// Grid for T tiles with at most `cap` blocks: a multiple of 8.
+inline int xcd_grid(int T, int cap) {
+  const int g = 8 * ((T + 7) / 8);
+  return g < cap ? g : cap;
+}
+
+
 // Epilogue of a wave's 64 x 64 tile (4 x 4 MFMA tiles, two pair tiles):
 // every load the epilogue needs (residual rows, biases, RoPE factors) is
 // requested for all 32 elements of the lane before the first store, so the
@@ -318,9 +368,14 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
     acol[i] = 8 * ((pos % 8) ^ aswz(pos / 8));
   }
 
-  for (int tile = blockIdx.x; tile < mtiles * ntiles; tile += gridDim.x) {
-    const int mt0 = (tile % mtiles) * 128;
-    const int pt0 = (tile / mtiles) * 4;
+  const int order = tile_order(g, Epi::kWaveTile);
+  for (int j = 0;; ++j) {
+    const int tile = xcd_tile(blockIdx.x, j, gridDim.x, mtiles * ntiles, order);
+    if (tile < 0) break;
+    int mi, ni;
+    tile_at(tile, mtiles, ntiles, order, mi, ni);
+    const int mt0 = mi * 128;
+    const int pt0 = ni * 4;
     int aoff[4];       // element offsets of this thread's A chunks (rows clamped into range)
 #pragma unroll
     for (int i = 0; i < 4; ++i) aoff[i] = min(mt0 + arow[i], g.R - 1) * g.lda + acol[i];
@@ -413,38 +468,6 @@ struct RingCfg {
   static constexpr int A_LD = A_KB / 4, B_LD = B_KB / 4;
 };
 
-// Tile of a ring-kernel block, XCD-aware.  Blocks are dealt to the 8 XCDs
-// round-robin and each XCD has its own L2.  The 128 x 128 tiles are ordered in
-// bands of kRingBand column tiles, row by row within a band, and XCD x takes
-// the x-th eighth of that order.  An XCD then streams the weights of about one
-// band and the activation rows its resident blocks share, instead of every
-// XCD fetching all of both.  Grid: 8 * ceil(tiles / 8) blocks; spare blocks
-// return false.  BANDED = false keeps the plain order (row tile fastest),
-// which spreads every column band over all XCDs: the QKV epilogue's cost
-// differs a lot between bands (transposed V stores), so it is better spread.
-constexpr int kRingBand = 8;
-__host__ __device__ inline int ring_tiles(const GemmArgs& g) { return ((g.R + 127) / 128) * (g.NPT / 4); }
-template <bool BANDED>
-__device__ __forceinline__ bool ring_tile(const GemmArgs& g, int& m0, int& pt0) {
-  const int mtiles = (g.R + 127) / 128, ntiles = g.NPT / 4;
-  if (!BANDED) {
-    if ((int)blockIdx.x >= mtiles * ntiles) return false;
-    m0 = (blockIdx.x % mtiles) * 128;
-    pt0 = (blockIdx.x / mtiles) * 4;
-    return true;
-  }
-  const int T = mtiles * ntiles, per = (T + 7) / 8;
-  const int j = blockIdx.x / 8;
-  const int t = (blockIdx.x % 8) * per + j;
-  if (j >= per || t >= T) return false;
-  const int band = t / (mtiles * kRingBand);
-  const int rem = t - band * mtiles * kRingBand;
-  const int bw = min(kRingBand, ntiles - band * kRingBand);
-  m0 = (rem / bw) * 128;
-  pt0 = (band * kRingBand + rem % bw) * 4;
-  return true;
-}
-
 template <class Epi, bool FP8>
 __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FP8 ? 3 : 2))) void gemm_ring_kernel(GemmArgs g, Epi epi) {
   typedef RingCfg<FP8> C;
@@ -454,8 +477,13 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FP8 ? 3 : 2
   const int wm = wave >> 1, wn = wave & 1;
   const int lc = lane % 16, lg = lane / 16;
   const int nkb = g.K / 64;
-  int m0, pt0;
-  if (!ring_tile<!Epi::kWaveTile>(g, m0, pt0)) return;
+  const int mtiles = (g.R + 127) / 128, ntiles = g.NPT / 4;
+  const int order = tile_order(g, Epi::kWaveTile);
+  const int t = xcd_tile(blockIdx.x, 0, gridDim.x, mtiles * ntiles, order);
+  if (t < 0) return;
+  int mi, ni;
+  tile_at(t, mtiles, ntiles, order, mi, ni);
+  const int m0 = mi * 128, pt0 = ni * 4;
   const bf16_t* A = static_cast<const bf16_t*>(g.A);
   const uint8_t* W = static_cast<const uint8_t*>(g.W);
 
@@ -555,15 +583,15 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
     dim3 grid(g.NPT, (g.R + 15) / 16);
     hipLaunchKernelGGL(gemm_f32_kernel<Epi>, grid, dim3(256), 0, s, g, epi);
   } else if (g.R >= 256 && g.A_lo == nullptr && g.A_ind == nullptr && g.rows_per_req == 0 && g.NPT % 4 == 0) {
-    const int tiles = ring_tiles(g);
+    const int tiles = gemm_tiles(g);
     const char* force = getenv("PHYAI_GEMM_TILE");   // tests: "ring" / "strided" (read at enqueue time)
     const bool ring = force ? strcmp(force, "ring") == 0 : g.K <= 1024;
     if (ring) {
-      const dim3 rgrid(8 * ((tiles + 7) / 8));
+      const dim3 rgrid(xcd_grid(tiles, 1 << 30));
       if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true>), rgrid, dim3(256), 0, s, g, epi);
       else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false>), rgrid, dim3(256), 0, s, g, epi);
     } else {
-      dim3 grid(tiles < 512 ? tiles : 512);
+      dim3 grid(xcd_grid(tiles, 512));
       if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_tiled_kernel<Epi, true>), grid, dim3(256), 0, s, g, epi);
       else hipLaunchKernelGGL((gemm_tiled_kernel<Epi, false>), grid, dim3(256), 0, s, g, epi);
     }
