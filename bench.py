@@ -33,15 +33,19 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # MI355X dense bf16 MFMA
 
 # HBM bytes moved by one launch of a block stage, from two rocprofv3 --pmc
-# passes (FETCH_SIZE, WRITE_SIZE) over `bench.py --no-batch64`, each scaled by
-# what the counter reads for the bench's 4 GiB device copy (profiles/
-# traffic_pi0_b1_fetch_write.md).  Reported only while the sources the counters
-# were taken on are unchanged (sha256 prefix over the listed files).
+# passes (FETCH_SIZE, WRITE_SIZE) over the leg (`--no-batch64 --no-stages` for
+# batch 1, `--no-batch1 --no-stages` for batch 64), each scaled by what the
+# counter reads for the 4 GiB device copy in the same run (profiles/
+# traffic_pi0_b1_fetch_write.md, profiles/traffic_pi0_fp8_b64_fetch_write.md).
+# Reported only while the sources the counters were taken on are unchanged
+# (sha256 prefix over the listed files).
+_ATTN_SRC = ("paper_2608_03682_amd/csrc/attention.hip", "paper_2608_03682_amd/csrc/kernels.hpp",
+             "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
+_GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/kernels.hpp",
+             "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
 MEASURED_TRAFFIC = {
-    ("pi0_bf16_b1", "attn"): {"bytes": 10013151,
-                              "sources": ("paper_2608_03682_amd/csrc/attention.hip",
-                                          "paper_2608_03682_amd/csrc/runtime.hip"),
-                              "sha256": "819c8ea7138a1224"},
+    ("pi0_bf16_b1", "attn"): {"bytes": 10044700, "sources": _ATTN_SRC, "sha256": "c0fa3ca0f333887d"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 96262498, "sources": _GEMM_SRC, "sha256": "cfcb92679afc7b95"},
 }
 
 
