@@ -520,9 +520,14 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(AttnArgs a) {
 // Copy the caller's prefix K (row-major) and transpose its V into the
 // library's key ranges, for every layer, request and kv head: keys
 // 0 .. prefix_len[b]-1.  Block: 64 keys x D of one (layer, request, head).
+// Moves are 16 bytes wide (the caller's buffer permitting): K rows are copied
+// directly; V rows go through an LDS tile (rows padded by 16 bytes, which
+// keeps them aligned and spreads a column over the banks) and leave as runs
+// of consecutive keys of one V^T row.
 template <typename T, int D>
 __global__ __launch_bounds__(256) void prefix_relayout_kernel(RelayoutArgs r) {
-  __shared__ T tile[64][D + 1];
+  constexpr int VE = 16 / sizeof(T);           // elements per 16-byte move
+  __shared__ __attribute__((aligned(16))) T tile[64][D + VE];
   const int key0 = blockIdx.x * 64;
   const int grp = blockIdx.y;                  // b * nkv + kvh
   const int l = blockIdx.z;
@@ -547,17 +552,39 @@ __global__ __launch_bounds__(256) void prefix_relayout_kernel(RelayoutArgs r) {
   }
   const int nk = min(64, plen - key0);
   if (nk <= 0) return;
-  for (int i = threadIdx.x; i < 64 * D; i += 256) {
-    const int kr = i / D, c = i % D;
+  // the library's ranges are allocated aligned; the caller's rows are 16-byte
+  // multiples apart, so its base decides
+  const bool vec = (reinterpret_cast<uintptr_t>(src) & 15) == 0;
+  constexpr int CPR = D / VE;                  // 16-byte chunks per key row
+  for (int i = threadIdx.x; i < 64 * CPR; i += 256) {
+    const int kr = i / CPR, c = (i % CPR) * VE;
+    const int64_t so = (int64_t)(key0 + kr) * W + c;
     if (kr < nk) {
-      kd[(int64_t)(key0 + kr) * D + c] = ks[(int64_t)(key0 + kr) * W + c];
-      tile[kr][c] = vs[(int64_t)(key0 + kr) * W + c];
+      if (vec) {
+        *reinterpret_cast<uint4*>(kd + (int64_t)(key0 + kr) * D + c) = *reinterpret_cast<const uint4*>(ks + so);
+        *reinterpret_cast<uint4*>(&tile[kr][c]) = *reinterpret_cast<const uint4*>(vs + so);
+      } else {
+#pragma unroll
+        for (int e = 0; e < VE; ++e) {
+          kd[(int64_t)(key0 + kr) * D + c + e] = ks[so + e];
+          tile[kr][c + e] = vs[so + e];
+        }
+      }
     }
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < 64 * D; i += 256) {
-    const int c = i / 64, kr = i % 64;
-    if (kr < nk) vd[(int64_t)c * r.ldk + key0 + kr] = tile[kr][c];
+  constexpr int KC = 64 / VE;                  // 16-byte runs per V^T row of the tile
+  for (int i = threadIdx.x; i < D * KC; i += 256) {
+    const int d = i / KC, k = (i % KC) * VE;
+    T* dst = vd + (int64_t)d * r.ldk + key0 + k;
+    if (k + VE <= nk) {
+      __attribute__((aligned(16))) T run[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) run[e] = tile[k + e][d];
+      *reinterpret_cast<uint4*>(dst) = *reinterpret_cast<const uint4*>(run);
+    } else {
+      for (int e = 0; k + e < nk; ++e) dst[e] = tile[k + e][d];
+    }
   }
 }
 
