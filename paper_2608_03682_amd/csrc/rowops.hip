@@ -92,6 +92,100 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(float* __restrict__ h, O
   }
 }
 
+// The same normalisation with one wave per row, for d a multiple of 256 and
+// at most 1024: lane l holds the float4 groups l, l + 64, ... of the row
+// (every load of the row, pending slices included, requested before any is
+// used; groups past d re-read the last one and are dropped), the statistics
+// are wave sums (no LDS, no barrier), and a block holds blockDim.x / 64 rows.
+// The pending slices are added in the same order as above.
+template <typename OutT>
+__global__ __launch_bounds__(256) void norm_rows_wave_kernel(float* __restrict__ h, OutT* __restrict__ n,
+                                                             OutT* __restrict__ n_lo, int R, int d, float eps,
+                                                             int mode, const float* __restrict__ mul,
+                                                             const float* __restrict__ shift, PendingResid pend) {
+  constexpr int kMaxG = 4;                      // float4 groups per lane (d <= 1024)
+  constexpr int kMaxSplit = 8;
+  const int lane = threadIdx.x % kWave;
+  const int row = blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+  if (row >= R) return;
+  const int ng = d / (4 * kWave);
+  const int np = pend.n;
+  float* hr = h + (int64_t)row * d;
+  float4 hv[kMaxG], sl[kMaxG][kMaxSplit], bs[kMaxG], gt[kMaxG];
+#pragma unroll
+  for (int j = 0; j < kMaxG; ++j) {
+    const int c = 4 * (lane + kWave * (j < ng ? j : ng - 1));
+    hv[j] = *reinterpret_cast<const float4*>(hr + c);
+    if (np > 0) {
+#pragma unroll
+      for (int sp = 0; sp < kMaxSplit; ++sp) {
+        const int ss = sp < np ? sp : np - 1;
+        sl[j][sp] = *reinterpret_cast<const float4*>(pend.part + ss * pend.stride + (int64_t)row * d + c);
+      }
+      bs[j] = pend.bias ? *reinterpret_cast<const float4*>(pend.bias + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      gt[j] = pend.gate ? *reinterpret_cast<const float4*>(pend.gate + c) : make_float4(1.f, 1.f, 1.f, 1.f);
+    }
+  }
+  float x[kMaxG][4];
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxG; ++j) {
+    float v[4] = {hv[j].x, hv[j].y, hv[j].z, hv[j].w};
+    if (np > 0) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        float t = 0.f;
+#pragma unroll
+        for (int sp = 0; sp < kMaxSplit; ++sp) {
+          const float4& q = sl[j][sp];
+          const float qe = e == 0 ? q.x : e == 1 ? q.y : e == 2 ? q.z : q.w;
+          t += sp < np ? qe : 0.f;
+        }
+        const float be = e == 0 ? bs[j].x : e == 1 ? bs[j].y : e == 2 ? bs[j].z : bs[j].w;
+        const float ge = e == 0 ? gt[j].x : e == 1 ? gt[j].y : e == 2 ? gt[j].z : gt[j].w;
+        v[e] += (t + be) * ge;
+      }
+      if (j < ng) *reinterpret_cast<float4*>(hr + 4 * (lane + kWave * j)) = make_float4(v[0], v[1], v[2], v[3]);
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      x[j][e] = j < ng ? v[e] : 0.f;
+      s += x[j][e];
+    }
+  }
+  float mu = 0.f;
+  if (mode == NORM_LN) mu = wave_sum(s) / d;
+  float ss = 0.f;
+#pragma unroll
+  for (int j = 0; j < kMaxG; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float t = j < ng ? x[j][e] - mu : 0.f;
+      ss += t * t;
+    }
+  const float r = rsqrtf(wave_sum(ss) / d + eps);
+  OutT* nr = n + (int64_t)row * d;
+#pragma unroll
+  for (int j = 0; j < kMaxG; ++j) {
+    if (j >= ng) break;
+    const int c = 4 * (lane + kWave * j);
+    const float4 mv = *reinterpret_cast<const float4*>(mul + c);
+    const float4 sv = shift ? *reinterpret_cast<const float4*>(shift + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+    const float m4[4] = {mv.x, mv.y, mv.z, mv.w}, s4[4] = {sv.x, sv.y, sv.z, sv.w};
+    float t[4];
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      t[e] = (x[j][e] - mu) * r * (1.f + m4[e]);
+      if (shift) t[e] += s4[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      ActIO<OutT>::store(nr + c + e, t[e]);
+      if (n_lo) ActIO<OutT>::store(n_lo + (int64_t)row * d + c + e, t[e] - ActIO<OutT>::round(t[e]));
+    }
+  }
+}
+
 // One block per suffix token row (b, t).
 __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs e) {
   __shared__ float xs[64];
@@ -255,6 +349,14 @@ __global__ void fp8_decode_kernel(const uint8_t* codes, bf16_t* out, int64_t n) 
 
 void norm_rows_bf16(float* h, bf16_t* n, bf16_t* n_lo, int R, int d, float eps, int mode, const float* mul,
                     const float* shift, const PendingResid& pend, hipStream_t s) {
+  // many rows: four rows per block, one per wave (fewer, fuller blocks); a
+  // few rows (batch 1) keep 256 threads per row, which spreads a row's loads
+  // over four waves and measured faster there
+  if (R >= 256 && d % 256 == 0 && d <= 1024 && pend.n <= 8) {
+    hipLaunchKernelGGL(norm_rows_wave_kernel<bf16_t>, dim3((R + 3) / 4), dim3(4 * kWave), 0, s, h, n, n_lo, R, d,
+                       eps, mode, mul, shift, pend);
+    return;
+  }
   hipLaunchKernelGGL(norm_rows_kernel<bf16_t>, dim3(R), dim3(256), 0, s, h, n, n_lo, d, eps, mode, mul, shift, pend);
 }
 void norm_rows_f32(float* h, float* n, int R, int d, float eps, int mode, const float* mul,
