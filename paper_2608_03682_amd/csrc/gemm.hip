@@ -468,10 +468,17 @@ struct RingCfg {
   static constexpr int A_LD = A_KB / 4, B_LD = B_KB / 4;
 };
 
-template <class Epi, bool FP8>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FP8 ? 3 : 2))) void gemm_ring_kernel(GemmArgs g, Epi epi) {
+// NS = 2: two stages (48 KiB fp8 / 64 KiB bf16), so three (two) blocks share
+// a CU and cover each other's load latency.  NS = 4: for GEMMs with at most
+// one tile per CU, where no other block is there to do that: four stages
+// (96 / 128 KiB), two k-blocks in flight while one is computed, and the
+// register room of a lone block for the batched epilogue.
+template <class Epi, bool FP8, int NS = 2>
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NS > 2 ? 1 : (FP8 ? 3 : 2)))) void gemm_ring_kernel(
+    GemmArgs g, Epi epi) {
   typedef RingCfg<FP8> C;
-  __shared__ __attribute__((aligned(1024))) uint8_t ring[2 * C::STAGE];
+  static_assert(NS == 2 || NS == 4, "two or four stages");
+  __shared__ __attribute__((aligned(1024))) uint8_t ring[NS * C::STAGE];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int wv = __builtin_amdgcn_readfirstlane(wave);
   const int wm = wave >> 1, wn = wave & 1;
@@ -551,16 +558,31 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(FP8 ? 3 : 2
     }
   };
 
-  issue(0, 0);
-  for (int kb = 0; kb < nkb; ++kb) {
-    GEMM_WAIT_VMCNT(0);                      // this wave's loads of k-block kb have landed
-    bare_barrier();                          // ... everyone's, and k-block kb-1 is consumed
-    if (kb + 1 < nkb) issue((kb + 1) & 1, kb + 1);
-    compute(kb & 1);
+  if constexpr (NS == 2) {
+    issue(0, 0);
+    for (int kb = 0; kb < nkb; ++kb) {
+      GEMM_WAIT_VMCNT(0);                    // this wave's loads of k-block kb have landed
+      bare_barrier();                        // ... everyone's, and k-block kb-1 is consumed
+      if (kb + 1 < nkb) issue((kb + 1) & 1, kb + 1);
+      compute(kb & 1);
+    }
+  } else {
+    constexpr int LPK = C::A_LD + C::B_LD;   // loads per wave per k-block
+    for (int q = 0; q < NS - 1 && q < nkb; ++q) issue(q, q);
+    for (int kb = 0; kb < nkb; ++kb) {
+      // k-block kb landed; the (up to NS - 2) later ones issued may still fly
+      const int later = min(NS - 2, nkb - 1 - kb);
+      if (later >= 2) GEMM_WAIT_VMCNT(2 * LPK);
+      else if (later == 1) GEMM_WAIT_VMCNT(LPK);
+      else GEMM_WAIT_VMCNT(0);
+      bare_barrier();                        // everyone's landed, and k-block kb-1's slot is free
+      if (kb + NS - 1 < nkb) issue((kb + NS - 1) % NS, kb + NS - 1);
+      compute(kb % NS);
+    }
   }
 
   if constexpr (Epi::kWaveTile) epi.wave_tile(g, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
-  else tile_epilogue<0>(g, epi, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
+  else tile_epilogue<NS == 2 ? 0 : 4>(g, epi, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
 }
 
 }  // namespace
@@ -584,9 +606,19 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
     hipLaunchKernelGGL(gemm_f32_kernel<Epi>, grid, dim3(256), 0, s, g, epi);
   } else if (g.R >= 256 && g.A_lo == nullptr && g.A_ind == nullptr && g.rows_per_req == 0 && g.NPT % 4 == 0) {
     const int tiles = gemm_tiles(g);
-    const char* force = getenv("PHYAI_GEMM_TILE");   // tests: "ring" / "strided" (read at enqueue time)
-    const bool ring = force ? strcmp(force, "ring") == 0 : g.K <= 1024;
-    if (ring) {
+    const char* force = getenv("PHYAI_GEMM_TILE");   // tests: "ring" / "deep" / "strided" (read at enqueue time)
+    // at most one tile per CU: no second block covers the load latency, so
+    // the four-stage ring; otherwise the two-stage ring for short K and the
+    // strided kernel for long K
+    const bool deep = !Epi::kWaveTile && (force ? strcmp(force, "deep") == 0 : tiles <= 256);
+    const bool ring = force ? strcmp(force, "strided") != 0 : g.K <= 1024;
+    if (deep) {
+      const dim3 rgrid(xcd_grid(tiles, 1 << 30));
+      if constexpr (!Epi::kWaveTile) {
+        if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true, 4>), rgrid, dim3(256), 0, s, g, epi);
+        else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false, 4>), rgrid, dim3(256), 0, s, g, epi);
+      }
+    } else if (ring) {
       const dim3 rgrid(xcd_grid(tiles, 1 << 30));
       if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true>), rgrid, dim3(256), 0, s, g, epi);
       else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false>), rgrid, dim3(256), 0, s, g, epi);

@@ -94,11 +94,12 @@ def test_full_size_batch64_fp8_sampled():
 
 
 @pytest.mark.parametrize("wdt", ["bf16", "fp8"])
-@pytest.mark.parametrize("tile", ["ring", "strided"])
+@pytest.mark.parametrize("tile", ["ring", "deep", "strided"])
 def test_many_row_gemm_tiles(tile, wdt):
-    """Both many-row GEMM kernels, forced in turn for every projection: 357
+    """Each many-row GEMM kernel, forced in turn for every projection: 357
     rows (a ragged last row tile), QKV 512 columns, GeGLU 2 x 512, output and
-    down projections 256 columns."""
+    down projections 256 columns.  "deep" (the four-stage ring) leaves the
+    QKV projection on the two-stage ring."""
     cfg = small_cfg("pi0", n_q_heads=6, batch=7, weight_dtype=wdt)
     print(f"[case] gemm tile {tile} {wdt}", flush=True)
     case = wl.make_case(cfg, seed=4)
