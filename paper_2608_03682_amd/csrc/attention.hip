@@ -605,11 +605,6 @@ int64_t attention_partial_floats(int B, int M, int nq, int nkv, int D, int n_spl
   return attention_partial_ml_off(B, M, nq, nkv, D, n_split) + tiles * n_split * kRows * 2;
 }
 
-int64_t attention_counters(int B, int M, int nq, int nkv) {
-  const int rows = M * (nq / nkv);
-  return (int64_t)B * nkv * ((rows + kRows - 1) / kRows);
-}
-
 void attention_bf16(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
   const int rows = a.M * (a.nq / a.nkv);

@@ -150,27 +150,45 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   for (int pp = 0; pp < NP; ++pp) {
     const int p = pt0 + pp;
     if (p >= g.NPT) break;
+    float s0[4], s1[4];
 #pragma unroll
     for (int v = 0; v < 4; ++v) {
-      const int row = m0 + 16 * mt + 4 * akg + v;
-      float s0 = 0.f, s1 = 0.f;
+      s0[v] = s1[v] = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        s0 += red[w][(mt * NT + 2 * pp) * 4 + v][lane];
-        s1 += red[w][(mt * NT + 2 * pp + 1) * 4 + v][lane];
+        s0[v] += red[w][(mt * NT + 2 * pp) * 4 + v][lane];
+        s1[v] += red[w][(mt * NT + 2 * pp + 1) * 4 + v][lane];
       }
-      if (!rowok[v]) s0 = s1 = 0.f;       // what a zero A row gives
-      if (g.scale) {
-        s0 *= g.scale[32 * p + c];
-        s1 *= g.scale[32 * p + 16 + c];
-      }
-      if (row < g.R) {
-        if (sp) {
-          sp[(int64_t)row * N + 32 * p + c] = s0;
-          sp[(int64_t)row * N + 32 * p + 16 + c] = s1;
-        } else {
-          epi(row, p, c, s0, s1);
+      if (!rowok[v]) s0[v] = s1[v] = 0.f;   // what a zero A row gives
+    }
+    const float sc0 = g.scale ? g.scale[32 * p + c] : 1.f, sc1 = g.scale ? g.scale[32 * p + 16 + c] : 1.f;
+    if (sp) {
+      __builtin_amdgcn_s_waitcnt(0xF70);      // the scales landed (see below)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = m0 + 16 * mt + 4 * akg + v;
+        if (row < g.R) {
+          sp[(int64_t)row * N + 32 * p + c] = s0[v] * sc0;
+          sp[(int64_t)row * N + 32 * p + 16 + c] = s1[v] * sc1;
         }
+      }
+    } else {
+      // every load the epilogue needs for the four rows first (rows past R
+      // read row 0 and are not stored), then the stores: one round trip
+      const typename Epi::ColPre cq = epi.colpre(p, c);
+      typename Epi::Pre pre[4];
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = m0 + 16 * mt + 4 * akg + v;
+        pre[v] = epi.pre(row < g.R ? row : 0, p, c);
+      }
+      // all of them landed: without this the compiler waits again, stores
+      // included, in front of each row's guarded stores
+      __builtin_amdgcn_s_waitcnt(0xF70);      // vmcnt(0), other counters open
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = m0 + 16 * mt + 4 * akg + v;
+        if (row < g.R) epi.apply(row, p, c, cq, pre[v], s0[v] * sc0, s1[v] * sc1);
       }
     }
   }

@@ -372,7 +372,6 @@ struct AttnArgs {
   void* out; int ldo;
   float* part;              // split partials (n_split > 1)
   int64_t part_ml_off;      // set by the launcher
-  int* counters;            // one per (group, row tile), zero between launches
   int n_split;
   const CallDesc* desc;
   int B, M, nq, nkv, D;
@@ -382,7 +381,6 @@ struct AttnArgs {
 void attention_bf16(const AttnArgs&, hipStream_t);
 void attention_f32(const AttnArgs&, hipStream_t);
 int64_t attention_partial_floats(int B, int M, int nq, int nkv, int D, int n_split);
-int64_t attention_counters(int B, int M, int nq, int nkv);
 
 // Copy the caller's prefix K and transpose its V ([L][2][B][P][nkv*D]) into
 // the per-layer key ranges (layer l at K/Vt + l * layer_stride).

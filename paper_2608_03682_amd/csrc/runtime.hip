@@ -109,7 +109,6 @@ struct phyai_expert {
   float* pend = nullptr;    // split-K partial sums of the residual GEMMs (small batches)
   int ldk = 0;
   int64_t kv_layer = 0;     // elements per layer
-  int* counters = nullptr;
   // two-term activations (hi + lo bf16) for the GEMMs fed by a norm or by GeGLU
   bool split_act = false;
   void *n_lo = nullptr, *g_lo = nullptr;
@@ -386,7 +385,7 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   at.q = q; at.ldq = e.qd;
   at.K = kl; at.Vt = vl; at.ldk = e.ldk;
   at.out = o; at.ldo = e.qd;
-  at.part = e.part; at.counters = e.counters;
+  at.part = e.part;
   at.desc = e.desc;
   at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
   at.scale = inv_sqrt_d;
@@ -795,12 +794,7 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
       }
     e->pend = e->mem.alloc_n<float>(pend);
   }
-  {
-    const int64_t nc = attention_counters(e->Bmax, e->M, e->nq, e->nkv);
-    e->counters = e->mem.alloc_n<int>(nc);
-    HIPC(hipMemsetAsync(e->counters, 0, nc * sizeof(int), s));
-    HIPC(hipStreamSynchronize(s));
-  }
+  HIPC(hipStreamSynchronize(s));
   e->desc = static_cast<CallDesc*>(e->mem.alloc(sizeof(CallDesc)));
   // tables
   const int64_t Km = e->Kmax;
