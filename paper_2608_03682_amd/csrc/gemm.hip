@@ -28,11 +28,12 @@ __device__ __forceinline__ u32x4_t gload16(const void* p) { return *(gu32x4_t*)(
 
 // One trip of the small-row GEMM: U k-blocks starting at kb, every operand
 // load issued (as global loads, so that the compiler can count them) before
-// the first MFMA.  Columns past N re-read the last pair tile.
-template <int U, bool FP8, bool SPLIT, int NT>
+// the first MFMA; `hook` runs between the loads and the MFMAs.  Columns past
+// N re-read the last pair tile.
+template <int U, bool FP8, bool SPLIT, int NT, class Hook>
 __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int lane, int kb,
                                         const bf16_t* const (&arp)[kMT], const bf16_t* const (&alp)[kMT],
-                                        f32x4 (&acc)[kMT][NT]) {
+                                        f32x4 (&acc)[kMT][NT], const Hook& hook) {
   bf16x8 b[U][NT][2];
   bf16x8 a[U][kMT][2], al[U][kMT][2];
 #pragma unroll
@@ -60,6 +61,7 @@ __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int
         if (SPLIT) al[u][mt][s] = __builtin_bit_cast(bf16x8, gload16(alp[mt] + kk * 64 + s * 32));
       }
   }
+  hook();
   __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
   for (int u = 0; u < U; ++u)
@@ -110,20 +112,55 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
     alp[mt] = SPLIT ? static_cast<const bf16_t*>(g.A_lo) + (int64_t)lr * g.lda + akg * 8 : nullptr;
   }
 
+  // Epilogue inputs of the rows this wave finishes (wave w finishes row
+  // tile w): they do not depend on the products, so the first trip requests
+  // them right behind its operands and they land together.  Rows past R read
+  // row 0 and columns past N the last pair tile; neither is stored.
+  const int c = lane % 16;
+  typename Epi::ColPre cq[NP];
+  typename Epi::Pre pre[NP][4];
+  float sc[NP][2];
+  auto epi_loads = [&]() {
+#pragma unroll
+    for (int pp = 0; pp < NP; ++pp) {
+      const int p = min(pt0 + pp, g.NPT - 1);
+      cq[pp] = epi.colpre(p, c);
+      sc[pp][0] = g.scale ? g.scale[32 * p + c] : 1.f;
+      sc[pp][1] = g.scale ? g.scale[32 * p + 16 + c] : 1.f;
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = m0 + 16 * wave + 4 * akg + v;
+        pre[pp][v] = epi.pre(row < g.R ? row : 0, p, c);
+      }
+    }
+  };
+  auto no_loads = []() {};
+
   f32x4 acc[kMT][NT];
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // trips of 4, then 2, then 1 k-blocks, so no k-block is loaded twice
+  // trips of 4, then 2, then 1 k-blocks, so no k-block is loaded twice; the
+  // first trip carries the epilogue loads
   int kb = kb0;
-  for (; kb + 4 <= kb1; kb += 4) b1_trip<4, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc);
-  if (kb + 2 <= kb1) {
-    b1_trip<2, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc);
-    kb += 2;
+  if (kb + 4 <= kb1) {
+    b1_trip<4, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+    for (kb += 4; kb + 4 <= kb1; kb += 4) b1_trip<4, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+    if (kb + 2 <= kb1) {
+      b1_trip<2, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+      kb += 2;
+    }
+    if (kb < kb1) b1_trip<1, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+  } else if (kb + 2 <= kb1) {
+    b1_trip<2, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+    if (kb + 3 == kb1) b1_trip<1, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb + 2, arp, alp, acc, no_loads);
+  } else if (kb < kb1) {
+    b1_trip<1, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+  } else {
+    epi_loads();
   }
-  if (kb < kb1) b1_trip<1, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc);
 
 #pragma unroll
   for (int mt = 0; mt < kMT; ++mt)
@@ -135,7 +172,6 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
 
   // wave w finishes row tile w
   const int mt = wave;
-  const int c = lane % 16;
   const int N = 32 * g.NPT;
   float* sp = g.split_out ? g.split_out + (int64_t)z * g.split_stride : nullptr;
   // rows of a request past its prefix length (rows_per_req > 0) count as zero
@@ -161,34 +197,20 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
       }
       if (!rowok[v]) s0[v] = s1[v] = 0.f;   // what a zero A row gives
     }
-    const float sc0 = g.scale ? g.scale[32 * p + c] : 1.f, sc1 = g.scale ? g.scale[32 * p + 16 + c] : 1.f;
-    if (sp) {
-      __builtin_amdgcn_s_waitcnt(0xF70);      // the scales landed (see below)
+    // the epilogue loads landed with the operands; saying so here keeps the
+    // compiler from waiting again, stores included, in front of each row's
+    // guarded stores
+    __builtin_amdgcn_s_waitcnt(0xF70);        // vmcnt(0), other counters open
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = m0 + 16 * mt + 4 * akg + v;
-        if (row < g.R) {
-          sp[(int64_t)row * N + 32 * p + c] = s0[v] * sc0;
-          sp[(int64_t)row * N + 32 * p + 16 + c] = s1[v] * sc1;
+    for (int v = 0; v < 4; ++v) {
+      const int row = m0 + 16 * mt + 4 * akg + v;
+      if (row < g.R) {
+        if (sp) {
+          sp[(int64_t)row * N + 32 * p + c] = s0[v] * sc[pp][0];
+          sp[(int64_t)row * N + 32 * p + 16 + c] = s1[v] * sc[pp][1];
+        } else {
+          epi.apply(row, p, c, cq[pp], pre[pp][v], s0[v] * sc[pp][0], s1[v] * sc[pp][1]);
         }
-      }
-    } else {
-      // every load the epilogue needs for the four rows first (rows past R
-      // read row 0 and are not stored), then the stores: one round trip
-      const typename Epi::ColPre cq = epi.colpre(p, c);
-      typename Epi::Pre pre[4];
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = m0 + 16 * mt + 4 * akg + v;
-        pre[v] = epi.pre(row < g.R ? row : 0, p, c);
-      }
-      // all of them landed: without this the compiler waits again, stores
-      // included, in front of each row's guarded stores
-      __builtin_amdgcn_s_waitcnt(0xF70);      // vmcnt(0), other counters open
-#pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = m0 + 16 * mt + 4 * akg + v;
-        if (row < g.R) epi.apply(row, p, c, cq, pre[v], s0[v] * sc0, s1[v] * sc1);
       }
     }
   }
