@@ -64,6 +64,17 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(float* __restrict__ h, O
   __shared__ float scratch[4];
   const int row = blockIdx.x;
   float* hr = h + (int64_t)row * d;
+  // the norm's own factors first: they do not wait on the row, and landing
+  // with it saves a round trip after the statistics
+  float mv[kMaxPer], sv[kMaxPer];
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) {
+    if (256 * i >= d) break;
+    const int c = threadIdx.x + 256 * i;
+    const int cc = c < d ? c : d - 1;
+    mv[i] = mul[cc];
+    sv[i] = shift ? shift[cc] : 0.f;
+  }
   float v[kMaxPer];
   load_row_with_pending(hr, row, d, pend, v);
   float s = 0.f;
@@ -84,8 +95,8 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(float* __restrict__ h, O
   for (int i = 0; i < kMaxPer; ++i) {
     const int c = threadIdx.x + 256 * i;
     if (c < d) {
-      float t = (v[i] - mu) * r * (1.f + mul[c]);
-      if (shift) t += shift[c];
+      float t = (v[i] - mu) * r * (1.f + mv[i]);
+      if (shift) t += sv[i];
       ActIO<OutT>::store(nr + c, t);
       if (n_lo) ActIO<OutT>::store(n_lo + (int64_t)row * d + c, t - ActIO<OutT>::round(t));
     }
@@ -94,8 +105,9 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(float* __restrict__ h, O
 
 // The same normalisation with one wave per row, for d a multiple of 256 and
 // at most 1024: lane l holds the float4 groups l, l + 64, ... of the row
-// (every load of the row, pending slices included, requested before any is
-// used; groups past d re-read the last one and are dropped), the statistics
+// (every load of the row and of the norm's factors, pending slices included,
+// requested before any is used; groups past d re-read the last one and are
+// dropped), the statistics
 // are wave sums (no LDS, no barrier), and a block holds blockDim.x / 64 rows.
 // The pending slices are added in the same order as above.
 template <typename OutT>
@@ -111,10 +123,12 @@ __global__ __launch_bounds__(256) void norm_rows_wave_kernel(float* __restrict__
   const int ng = d / (4 * kWave);
   const int np = pend.n;
   float* hr = h + (int64_t)row * d;
-  float4 hv[kMaxG], sl[kMaxG][kMaxSplit], bs[kMaxG], gt[kMaxG];
+  float4 hv[kMaxG], sl[kMaxG][kMaxSplit], bs[kMaxG], gt[kMaxG], mv[kMaxG], sv[kMaxG];
 #pragma unroll
   for (int j = 0; j < kMaxG; ++j) {
     const int c = 4 * (lane + kWave * (j < ng ? j : ng - 1));
+    mv[j] = *reinterpret_cast<const float4*>(mul + c);
+    sv[j] = shift ? *reinterpret_cast<const float4*>(shift + c) : make_float4(0.f, 0.f, 0.f, 0.f);
     hv[j] = *reinterpret_cast<const float4*>(hr + c);
     if (np > 0) {
 #pragma unroll
@@ -169,9 +183,7 @@ __global__ __launch_bounds__(256) void norm_rows_wave_kernel(float* __restrict__
   for (int j = 0; j < kMaxG; ++j) {
     if (j >= ng) break;
     const int c = 4 * (lane + kWave * j);
-    const float4 mv = *reinterpret_cast<const float4*>(mul + c);
-    const float4 sv = shift ? *reinterpret_cast<const float4*>(shift + c) : make_float4(0.f, 0.f, 0.f, 0.f);
-    const float m4[4] = {mv.x, mv.y, mv.z, mv.w}, s4[4] = {sv.x, sv.y, sv.z, sv.w};
+    const float m4[4] = {mv[j].x, mv[j].y, mv[j].z, mv[j].w}, s4[4] = {sv[j].x, sv[j].y, sv[j].z, sv[j].w};
     float t[4];
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
@@ -305,6 +317,159 @@ __global__ __launch_bounds__(256) void readout_kernel(ReadoutArgs r) {
   }
 }
 
+// Sums over the block of K values at once; scratch holds K floats per wave.
+template <int K>
+__device__ __forceinline__ void block_sums(float (&v)[K], float (*scratch)[K]) {
+  const int w = threadIdx.x / kWave, l = threadIdx.x % kWave;
+#pragma unroll
+  for (int k = 0; k < K; ++k) v[k] = wave_sum(v[k]);
+  __syncthreads();
+  if (l == 0)
+#pragma unroll
+    for (int k = 0; k < K; ++k) scratch[w][k] = v[k];
+  __syncthreads();
+#pragma unroll
+  for (int k = 0; k < K; ++k) {
+    float t = 0.f;
+#pragma unroll
+    for (int i = 0; i < 256 / kWave; ++i) t += scratch[i][k];
+    v[k] = t;
+  }
+}
+
+// The readout for d a multiple of 256 up to 1024 and A <= 32, RB action rows
+// per block.  Every load the block needs is requested before any is used --
+// its waves' W_out rows (wave w takes outputs w, w + 4, ...), the final
+// norm's factors, b_out, dt and the x entries it updates, then the rows --
+// so the block makes one memory round trip.  RB = 1 adds the pending split
+// partials of the last block; RB > 1 (rows without them) shares each W_out
+// load among RB rows.  Per output the products are summed in the order of
+// readout_kernel.
+template <int RB>
+__global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
+  constexpr int QA = 8;                      // outputs per wave
+  constexpr int QC = 4;                      // float4 groups per lane per row (d <= 1024)
+  __shared__ float4 nrm4[RB][QC * kWave];
+  __shared__ float red[RB][32];
+  __shared__ float scratch[256 / kWave][RB];
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int nrows = r.B * r.H;
+  const int ar0 = blockIdx.x * RB;
+  const int ng = r.d / 256;
+
+  float4 w4[QA][QC];
+#pragma unroll
+  for (int q = 0; q < QA; ++q) {
+    const int a = min(wave + 4 * q, r.A - 1);
+#pragma unroll
+    for (int i = 0; i < QC; ++i)
+      if (i < ng) w4[q][i] = *reinterpret_cast<const float4*>(r.out_w + (int64_t)a * r.d + 4 * lane + 256 * i);
+  }
+  float mv[QC], sv[QC];
+#pragma unroll
+  for (int i = 0; i < QC; ++i) {
+    if (i >= ng) break;
+    mv[i] = r.mul[threadIdx.x + 256 * i];
+    sv[i] = r.shift ? r.shift[threadIdx.x + 256 * i] : 0.f;
+  }
+  const int ur = threadIdx.x / r.A, ua = threadIdx.x % r.A;
+  const bool upd = threadIdx.x < RB * r.A && ar0 + ur < nrows;
+  const int64_t xi = upd ? (int64_t)(ar0 + ur) * r.A + ua : 0;
+  const float xv = r.x[xi], bv = r.out_b[upd ? ua : 0], dtv = r.dt[0];
+
+  float v[RB][QC];
+  if constexpr (RB == 1) {
+    const int b = ar0 / r.H, j = ar0 % r.H;
+    const int64_t hrow = (int64_t)b * r.M + r.off + j;
+    float vv[kMaxPer];
+    load_row_with_pending(r.h + hrow * r.d, hrow, r.d, r.pend, vv);
+#pragma unroll
+    for (int i = 0; i < QC; ++i) v[0][i] = vv[i];
+  } else {
+#pragma unroll
+    for (int rr = 0; rr < RB; ++rr) {
+      const int ar = min(ar0 + rr, nrows - 1);
+      const int b = ar / r.H, j = ar % r.H;
+      const float* hr = r.h + ((int64_t)b * r.M + r.off + j) * r.d;
+#pragma unroll
+      for (int i = 0; i < QC; ++i)
+        if (i < ng) v[rr][i] = hr[threadIdx.x + 256 * i];
+    }
+  }
+#pragma unroll
+  for (int rr = 0; rr < RB; ++rr)
+#pragma unroll
+    for (int i = 0; i < QC; ++i)
+      if (i >= ng) v[rr][i] = 0.f;
+
+  float mu[RB], st[RB];
+#pragma unroll
+  for (int rr = 0; rr < RB; ++rr) {
+    mu[rr] = 0.f;
+#pragma unroll
+    for (int i = 0; i < QC; ++i) mu[rr] += v[rr][i];
+  }
+  if (r.mode == NORM_LN) {
+    block_sums<RB>(mu, scratch);
+#pragma unroll
+    for (int rr = 0; rr < RB; ++rr) mu[rr] /= r.d;
+  } else {
+#pragma unroll
+    for (int rr = 0; rr < RB; ++rr) mu[rr] = 0.f;
+  }
+#pragma unroll
+  for (int rr = 0; rr < RB; ++rr) {
+    st[rr] = 0.f;
+#pragma unroll
+    for (int i = 0; i < QC; ++i) {
+      const float t = i < ng ? v[rr][i] - mu[rr] : 0.f;
+      st[rr] += t * t;
+    }
+  }
+  block_sums<RB>(st, scratch);
+  float* nrm = reinterpret_cast<float*>(nrm4);
+#pragma unroll
+  for (int rr = 0; rr < RB; ++rr) {
+    const float rs = rsqrtf(st[rr] / r.d + r.eps);
+#pragma unroll
+    for (int i = 0; i < QC; ++i) {
+      if (i >= ng) break;
+      float t = (v[rr][i] - mu[rr]) * rs * (1.f + mv[i]);
+      if (r.shift) t += sv[i];
+      nrm[rr * QC * 256 + threadIdx.x + 256 * i] = t;
+    }
+  }
+  __syncthreads();
+
+  // v = n W_out: lane l takes elements 4l .. 4l+3 of each 256, a wave sum
+  // finishes each (row, output)
+#pragma unroll
+  for (int rr = 0; rr < RB; ++rr) {
+    float4 n4[QC];
+#pragma unroll
+    for (int i = 0; i < QC; ++i)
+      if (i < ng) n4[i] = nrm4[rr][lane + kWave * i];
+#pragma unroll
+    for (int q = 0; q < QA; ++q) {
+      const int a = wave + 4 * q;
+      if (a >= r.A) break;
+      float acc = 0.f;
+#pragma unroll
+      for (int i = 0; i < QC; ++i) {
+        if (i >= ng) break;
+        acc = fmaf(n4[i].x, w4[q][i].x, acc);
+        acc = fmaf(n4[i].y, w4[q][i].y, acc);
+        acc = fmaf(n4[i].z, w4[q][i].z, acc);
+        acc = fmaf(n4[i].w, w4[q][i].w, acc);
+      }
+      acc = wave_sum(acc);
+      if (lane == 0) red[rr][a] = acc;
+    }
+  }
+  __syncthreads();
+  if (upd) r.x[xi] = xv + dtv * (red[ur][ua] + bv);
+}
+
 __global__ __launch_bounds__(128) void rope_table_kernel(const CallDesc* desc, const float* inv_freq, float2* tab,
                                                         int M, int half) {
   const int row = blockIdx.x;                    // b*M + t
@@ -372,7 +537,13 @@ void embed_state(const CallDesc* desc, const float* w, const float* b, float* e,
   hipLaunchKernelGGL(state_embed_kernel, dim3(B), dim3(256), 0, s, desc, w, b, e, A, d);
 }
 void readout_euler(const ReadoutArgs& r, hipStream_t s) {
-  hipLaunchKernelGGL(readout_kernel, dim3(r.B * r.H), dim3(256), 0, s, r);
+  const int rows = r.B * r.H;
+  if (r.d % 256 == 0 && r.d <= 1024 && r.A <= 32) {
+    if (r.pend.n == 0 && rows >= 1024) hipLaunchKernelGGL(readout_rows_kernel<4>, dim3((rows + 3) / 4), dim3(256), 0, s, r);
+    else hipLaunchKernelGGL(readout_rows_kernel<1>, dim3(rows), dim3(256), 0, s, r);
+  } else {
+    hipLaunchKernelGGL(readout_kernel, dim3(rows), dim3(256), 0, s, r);
+  }
 }
 void copy_noise_to_state(const CallDesc* desc, float* x, int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(copy_in_kernel, dim3((n + 255) / 256), dim3(256), 0, s, desc, x, n);
