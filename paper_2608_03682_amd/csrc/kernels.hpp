@@ -412,6 +412,8 @@ struct EmbedArgs {
   const float* x;           // solver state [B][H][A]
   const float* in_w;        // [A][d] fp32
   const float* in_b;        // [d]
+  const float* rowvec;      // [d] also added to every action row, or null
+  int act;                  // Act applied to action rows
   const float* pos;         // [H][d] or null
   const float* e_state;     // [B][d] or null (state rows of h)
   float* h;                 // [B*M][d]: destination of state rows, and of action rows if act_out == null

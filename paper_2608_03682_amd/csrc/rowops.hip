@@ -214,13 +214,105 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs e) {
     float y = e.in_b[c];
 #pragma unroll 16
     for (int a = 0; a < e.A; ++a) y = fmaf(xs[a], e.in_w[(int64_t)a * e.d + c], y);
+    if (e.rowvec) y += e.rowvec[c];
     if (e.pos) y += e.pos[(int64_t)j * e.d + c];
+    y = apply_act(e.act, y);
     if (e.act_out) {
       const int64_t o = ((int64_t)b * e.H + j) * e.d + c;
       if (e.act_is_bf16) static_cast<bf16_t*>(e.act_out)[o] = f32_to_bf16(y);
       else static_cast<float*>(e.act_out)[o] = y;
     } else {
       e.h[(int64_t)row * e.d + c] = y;
+    }
+  }
+}
+
+// The same embedding for A <= 32 and d a multiple of 4, RB suffix rows per
+// block.  Thread t owns columns 4t .. 4t+3 of each 1024; every load of a
+// group of 1024 columns (the weight columns for all A inputs, bias, rowvec,
+// pos and state rows, and for the first group the rows' x entries) is
+// requested before the first store, and the weight loads are shared by the
+// block's RB rows.  Action rows: y = bias + sum_a x_a W[a] (+ rowvec)
+// (+ pos), then act.
+template <int RB>
+__global__ __launch_bounds__(256) void embed_rows_kernel(EmbedArgs e) {
+  static_assert(RB * 32 <= 256, "one x entry per thread");
+  __shared__ float xs[RB][32];
+  const int R = e.B * e.M;
+  const int r0 = blockIdx.x * RB;
+  float xv = 0.f;
+  {
+    const int rr = threadIdx.x / 32, a = threadIdx.x % 32;
+    if (rr < RB && a < e.A) {
+      const int r = min(r0 + rr, R - 1);
+      const int b = r / e.M, j = max(r % e.M - e.off, 0);
+      xv = e.x[((int64_t)b * e.H + j) * e.A + a];
+    }
+  }
+  for (int g0 = 0; g0 < e.d; g0 += 1024) {
+    const int c = g0 + 4 * threadIdx.x;
+    const bool cv = c < e.d;
+    const int cc = cv ? c : 0;
+    float4 w[32];
+#pragma unroll
+    for (int a = 0; a < 32; ++a)
+      if (a < e.A) w[a] = *reinterpret_cast<const float4*>(e.in_w + (int64_t)a * e.d + cc);
+    const float4 bias = *reinterpret_cast<const float4*>(e.in_b + cc);
+    const float4 rv = e.rowvec ? *reinterpret_cast<const float4*>(e.rowvec + cc) : make_float4(0.f, 0.f, 0.f, 0.f);
+    float4 pv[RB], sv[RB];
+#pragma unroll
+    for (int rr = 0; rr < RB; ++rr) {
+      const int r = min(r0 + rr, R - 1);
+      const int b = r / e.M, j = max(r % e.M - e.off, 0);
+      pv[rr] = e.pos ? *reinterpret_cast<const float4*>(e.pos + (int64_t)j * e.d + cc) : make_float4(0.f, 0.f, 0.f, 0.f);
+      sv[rr] = e.off ? *reinterpret_cast<const float4*>(e.e_state + (int64_t)b * e.d + cc) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    if (g0 == 0) {
+      if (threadIdx.x < RB * 32) xs[threadIdx.x / 32][threadIdx.x % 32] = xv;
+      __syncthreads();
+    }
+    if (!cv) continue;
+#pragma unroll
+    for (int rr = 0; rr < RB; ++rr) {
+      const int r = r0 + rr;
+      if (r >= R) break;
+      const int b = r / e.M, t = r % e.M;
+      if (e.off && t == 0) {
+        *reinterpret_cast<float4*>(e.h + (int64_t)r * e.d + c) = sv[rr];
+        continue;
+      }
+      float y[4] = {bias.x, bias.y, bias.z, bias.w};
+#pragma unroll
+      for (int a = 0; a < 32; ++a) {
+        if (a < e.A) {
+          const float xa = xs[rr][a];
+          y[0] = fmaf(xa, w[a].x, y[0]);
+          y[1] = fmaf(xa, w[a].y, y[1]);
+          y[2] = fmaf(xa, w[a].z, y[2]);
+          y[3] = fmaf(xa, w[a].w, y[3]);
+        }
+      }
+      const float r4[4] = {rv.x, rv.y, rv.z, rv.w}, p4[4] = {pv[rr].x, pv[rr].y, pv[rr].z, pv[rr].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (e.rowvec) y[q] += r4[q];
+        if (e.pos) y[q] += p4[q];
+        y[q] = apply_act(e.act, y[q]);
+      }
+      const int j = t - e.off;
+      if (e.act_out) {
+        const int64_t o = ((int64_t)b * e.H + j) * e.d + c;
+        if (e.act_is_bf16) {
+          uint2 u;
+          u.x = pack_bf16x2(y[0], y[1]);
+          u.y = pack_bf16x2(y[2], y[3]);
+          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(e.act_out) + o) = u;
+        } else {
+          *reinterpret_cast<float4*>(static_cast<float*>(e.act_out) + o) = make_float4(y[0], y[1], y[2], y[3]);
+        }
+      } else {
+        *reinterpret_cast<float4*>(e.h + (int64_t)r * e.d + c) = make_float4(y[0], y[1], y[2], y[3]);
+      }
     }
   }
 }
@@ -530,7 +622,13 @@ void norm_rows_f32(float* h, float* n, int R, int d, float eps, int mode, const 
                      pend);
 }
 void embed_actions(const EmbedArgs& e, hipStream_t s) {
-  hipLaunchKernelGGL(embed_kernel, dim3(e.B * e.M), dim3(256), 0, s, e);
+  const int R = e.B * e.M;
+  if (e.A <= 32 && e.d % 4 == 0) {
+    if (R >= 1024) hipLaunchKernelGGL(embed_rows_kernel<8>, dim3((R + 7) / 8), dim3(256), 0, s, e);
+    else hipLaunchKernelGGL(embed_rows_kernel<1>, dim3(R), dim3(256), 0, s, e);
+  } else {
+    hipLaunchKernelGGL(embed_kernel, dim3(R), dim3(256), 0, s, e);
+  }
 }
 void embed_state(const CallDesc* desc, const float* w, const float* b, float* e, int B, int A, int d,
                  hipStream_t s) {

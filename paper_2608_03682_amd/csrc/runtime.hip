@@ -94,15 +94,18 @@ struct phyai_expert {
   DevMem mem;
   // parameters
   float *in_w = nullptr, *in_b = nullptr, *state_w = nullptr, *state_b = nullptr, *pos = nullptr;
+  // pi0: the action embedding folded into the time MLP's first layer
+  // (x -> W_in x + b_in -> W1a (.) is one affine map of x): [A][d] and [d]
+  float *tin_w = nullptr, *tin_b = nullptr;
   float *out_w = nullptr, *out_b = nullptr, *final_norm = nullptr;
   float *time_b1 = nullptr, *time_b2 = nullptr, *cond_b1 = nullptr, *cond_b2 = nullptr, *final_b = nullptr;
-  Lin time_w1a, time_w1t, time_w2, cond_w1, cond_w2, final_mod;
+  Lin time_w1t, time_w2, cond_w1, cond_w2, final_mod;
   std::vector<LayerW> layers;
   float* inv_freq = nullptr;
   float2* rope_cs = nullptr;   // per-call RoPE table [max_batch * M][D/2]
   // working buffers
   float *x = nullptr, *h = nullptr, *e_state = nullptr, *part = nullptr;
-  void *n = nullptr, *abuf = nullptr, *zbuf = nullptr, *q = nullptr;
+  void *n = nullptr, *zbuf = nullptr, *q = nullptr;
   void *o = nullptr, *g = nullptr;
   // per-layer key ranges: K [L][Bmax][nkv][ldk][D], V transposed [L][Bmax][nkv][D][ldk]
   void *kall = nullptr, *vt = nullptr;
@@ -499,14 +502,20 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
     em.pos = e.pos;
     em.e_state = e.e_state;
     em.h = e.h;
-    em.act_out = variant == PHYAI_VARIANT_PI0 ? e.abuf : nullptr;
     em.act_is_bf16 = e.f32 ? 0 : 1;
     em.B = B; em.H = H; em.M = M; em.A = e.A; em.d = d; em.off = e.off;
+    if (variant == PHYAI_VARIANT_PI0) {
+      // z = swish(W1a (W_in x + b_in) + (W1t tau(t_k) + b1)), the embedding
+      // folded into W1a (tin_w, tin_b); the state rows of h are reset too
+      em.in_w = e.tin_w;
+      em.in_b = e.tin_b;
+      em.rowvec = e.T + (int64_t)k * d;
+      em.act = ACT_SWISH;
+      em.act_out = e.zbuf;
+    }
     embed_actions(em, s);
     if (variant == PHYAI_VARIANT_PI0) {
-      // u = W2 swish(W1a a + (W1t tau(t_k) + b1)) + b2, written into the action rows of h
-      gemm_store(gargs(e.time_w1a, e.abuf, d, B * H),
-                 store_epi<T>(static_cast<T*>(e.zbuf), d, nullptr, e.T + (int64_t)k * d, ACT_SWISH), s);
+      // u = W2 z + b2, written into the action rows of h
       EpiStore<float> ep = store_epi<float>(e.h, d, e.time_b2, nullptr, ACT_NONE);
       ep.grp = H; ep.grp_stride = M; ep.grp_off = e.off;
       gemm_store(gargs(e.time_w2, e.zbuf, d, B * H), ep, s);
@@ -674,7 +683,28 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     ta.rows = d;
     tt.rows = c.time_dim;
     tt.data = static_cast<const char*>(w1->data) + (size_t)d * d * esz;
-    e->time_w1a = pack_identity(*e, {&ta}, wk_small, s);
+    {
+      // tin_w = W_in W1a and tin_b = b_in W1a, in fp64 from the weights as
+      // given, kept in fp32: the time MLP's first layer then reads x directly
+      const phyai_tensor* wi = P.get("in_w", A, d);
+      const phyai_tensor* bi = P.get("in_b", 1, d);
+      std::vector<double> w1a((size_t)d * d), acc((size_t)(A + 1) * d, 0.0);
+      for (int64_t i = 0; i < (int64_t)d * d; ++i) w1a[i] = elem_f32(&ta, i);
+      for (int a = 0; a <= A; ++a) {
+        double* row = &acc[(size_t)a * d];
+        for (int k = 0; k < d; ++k) {
+          const double xk = a < A ? elem_f32(wi, (int64_t)a * d + k) : elem_f32(bi, k);
+          const double* wr = &w1a[(size_t)k * d];
+          for (int c2 = 0; c2 < d; ++c2) row[c2] += xk * wr[c2];
+        }
+      }
+      std::vector<float> f(acc.begin(), acc.end());
+      e->tin_w = e->mem.alloc_n<float>((int64_t)A * d);
+      e->tin_b = e->mem.alloc_n<float>(d);
+      HIPC(hipMemcpyAsync(e->tin_w, f.data(), (size_t)A * d * 4, hipMemcpyHostToDevice, s));
+      HIPC(hipMemcpyAsync(e->tin_b, f.data() + (size_t)A * d, (size_t)d * 4, hipMemcpyHostToDevice, s));
+      HIPC(hipStreamSynchronize(s));
+    }
     e->time_w1t = pack_identity(*e, {&tt}, wk_small, s);
     e->time_b1 = vec("time_b1", d);
     e->time_w2 = pack_identity(*e, {P.get("time_w2", d, d)}, wk_small, s);
@@ -745,7 +775,6 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
   e->h = e->mem.alloc_n<float>(Bm * M * d);
   e->e_state = e->mem.alloc_n<float>(Bm * d);
   e->n = e->mem.alloc(Bm * M * d * ab);
-  e->abuf = e->mem.alloc(Bm * e->H * d * ab);
   e->zbuf = e->mem.alloc(Bm * e->H * d * ab);
   e->q = e->mem.alloc(Bm * M * e->qd * ab);
   e->o = e->mem.alloc(Bm * M * e->qd * ab);
