@@ -233,11 +233,12 @@ __global__ __launch_bounds__(256) void embed_kernel(EmbedArgs e) {
 // pos and state rows, and for the first group the rows' x entries) is
 // requested before the first store, and the weight loads are shared by the
 // block's RB rows.  Action rows: y = bias + sum_a x_a W[a] (+ rowvec)
-// (+ pos), then act.
+// (+ pos), then act.  The loops run over 32 inputs without tests: inputs
+// past A re-read weight row A-1 and meet x = 0.
 template <int RB>
 __global__ __launch_bounds__(256) void embed_rows_kernel(EmbedArgs e) {
   static_assert(RB * 32 <= 256, "one x entry per thread");
-  __shared__ float xs[RB][32];
+  __shared__ __attribute__((aligned(16))) float xs[RB][32];
   const int R = e.B * e.M;
   const int r0 = blockIdx.x * RB;
   float xv = 0.f;
@@ -255,8 +256,7 @@ __global__ __launch_bounds__(256) void embed_rows_kernel(EmbedArgs e) {
     const int cc = cv ? c : 0;
     float4 w[32];
 #pragma unroll
-    for (int a = 0; a < 32; ++a)
-      if (a < e.A) w[a] = *reinterpret_cast<const float4*>(e.in_w + (int64_t)a * e.d + cc);
+    for (int a = 0; a < 32; ++a) w[a] = *reinterpret_cast<const float4*>(e.in_w + (int64_t)min(a, e.A - 1) * e.d + cc);
     const float4 bias = *reinterpret_cast<const float4*>(e.in_b + cc);
     const float4 rv = e.rowvec ? *reinterpret_cast<const float4*>(e.rowvec + cc) : make_float4(0.f, 0.f, 0.f, 0.f);
     float4 pv[RB], sv[RB];
@@ -282,15 +282,18 @@ __global__ __launch_bounds__(256) void embed_rows_kernel(EmbedArgs e) {
         continue;
       }
       float y[4] = {bias.x, bias.y, bias.z, bias.w};
+      float xr[32];
+#pragma unroll
+      for (int a4 = 0; a4 < 8; ++a4) {
+        const float4 x4 = reinterpret_cast<const float4*>(xs[rr])[a4];
+        xr[4 * a4] = x4.x; xr[4 * a4 + 1] = x4.y; xr[4 * a4 + 2] = x4.z; xr[4 * a4 + 3] = x4.w;
+      }
 #pragma unroll
       for (int a = 0; a < 32; ++a) {
-        if (a < e.A) {
-          const float xa = xs[rr][a];
-          y[0] = fmaf(xa, w[a].x, y[0]);
-          y[1] = fmaf(xa, w[a].y, y[1]);
-          y[2] = fmaf(xa, w[a].z, y[2]);
-          y[3] = fmaf(xa, w[a].w, y[3]);
-        }
+        y[0] = fmaf(xr[a], w[a].x, y[0]);
+        y[1] = fmaf(xr[a], w[a].y, y[1]);
+        y[2] = fmaf(xr[a], w[a].z, y[2]);
+        y[3] = fmaf(xr[a], w[a].w, y[3]);
       }
       const float r4[4] = {rv.x, rv.y, rv.z, rv.w}, p4[4] = {pv[rr].x, pv[rr].y, pv[rr].z, pv[rr].w};
 #pragma unroll
@@ -429,38 +432,36 @@ __device__ __forceinline__ void block_sums(float (&v)[K], float (*scratch)[K]) {
   }
 }
 
-// The readout for d a multiple of 256 up to 1024 and A <= 32, RB action rows
-// per block.  Every load the block needs is requested before any is used --
-// its waves' W_out rows (wave w takes outputs w, w + 4, ...), the final
-// norm's factors, b_out, dt and the x entries it updates, then the rows --
-// so the block makes one memory round trip.  RB = 1 adds the pending split
-// partials of the last block; RB > 1 (rows without them) shares each W_out
-// load among RB rows.  Per output the products are summed in the order of
-// readout_kernel.
-template <int RB>
+// The readout for d = 256 NG (NG <= 4) and A <= 32, RB action rows per
+// block.  Every load the block needs is requested before any is used -- its
+// waves' W_out rows (wave w takes outputs w, w + 4, ..., rows past A re-read
+// row A-1 and are not stored), the final norm's factors, b_out, dt and the x
+// entries it updates, then the rows -- so the block makes one memory round
+// trip.  RB = 1 adds the pending split partials of the last block; RB > 1
+// (rows without them) shares each W_out load among RB rows.  Per output the
+// products are summed in the order of readout_kernel.
+template <int RB, int NG>
 __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
   constexpr int QA = 8;                      // outputs per wave
-  constexpr int QC = 4;                      // float4 groups per lane per row (d <= 1024)
-  __shared__ float4 nrm4[RB][QC * kWave];
+  __shared__ float4 nrm4[RB][NG * kWave];
   __shared__ float red[RB][32];
   __shared__ float scratch[256 / kWave][RB];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int nrows = r.B * r.H;
   const int ar0 = blockIdx.x * RB;
-  const int ng = r.d / 256;
+  const int d = 256 * NG;
 
-  float4 w4[QA][QC];
+  float4 w4[QA][NG];
 #pragma unroll
   for (int q = 0; q < QA; ++q) {
     const int a = min(wave + 4 * q, r.A - 1);
 #pragma unroll
-    for (int i = 0; i < QC; ++i)
-      if (i < ng) w4[q][i] = *reinterpret_cast<const float4*>(r.out_w + (int64_t)a * r.d + 4 * lane + 256 * i);
+    for (int i = 0; i < NG; ++i)
+      w4[q][i] = *reinterpret_cast<const float4*>(r.out_w + (int64_t)a * d + 4 * lane + 256 * i);
   }
-  float mv[QC], sv[QC];
+  float mv[NG], sv[NG];
 #pragma unroll
-  for (int i = 0; i < QC; ++i) {
-    if (i >= ng) break;
+  for (int i = 0; i < NG; ++i) {
     mv[i] = r.mul[threadIdx.x + 256 * i];
     sv[i] = r.shift ? r.shift[threadIdx.x + 256 * i] : 0.f;
   }
@@ -469,42 +470,36 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
   const int64_t xi = upd ? (int64_t)(ar0 + ur) * r.A + ua : 0;
   const float xv = r.x[xi], bv = r.out_b[upd ? ua : 0], dtv = r.dt[0];
 
-  float v[RB][QC];
+  float v[RB][NG];
   if constexpr (RB == 1) {
     const int b = ar0 / r.H, j = ar0 % r.H;
     const int64_t hrow = (int64_t)b * r.M + r.off + j;
     float vv[kMaxPer];
-    load_row_with_pending(r.h + hrow * r.d, hrow, r.d, r.pend, vv);
+    load_row_with_pending(r.h + hrow * d, hrow, d, r.pend, vv);
 #pragma unroll
-    for (int i = 0; i < QC; ++i) v[0][i] = vv[i];
+    for (int i = 0; i < NG; ++i) v[0][i] = vv[i];
   } else {
 #pragma unroll
     for (int rr = 0; rr < RB; ++rr) {
       const int ar = min(ar0 + rr, nrows - 1);
       const int b = ar / r.H, j = ar % r.H;
-      const float* hr = r.h + ((int64_t)b * r.M + r.off + j) * r.d;
+      const float* hr = r.h + ((int64_t)b * r.M + r.off + j) * d;
 #pragma unroll
-      for (int i = 0; i < QC; ++i)
-        if (i < ng) v[rr][i] = hr[threadIdx.x + 256 * i];
+      for (int i = 0; i < NG; ++i) v[rr][i] = hr[threadIdx.x + 256 * i];
     }
   }
-#pragma unroll
-  for (int rr = 0; rr < RB; ++rr)
-#pragma unroll
-    for (int i = 0; i < QC; ++i)
-      if (i >= ng) v[rr][i] = 0.f;
 
   float mu[RB], st[RB];
 #pragma unroll
   for (int rr = 0; rr < RB; ++rr) {
     mu[rr] = 0.f;
 #pragma unroll
-    for (int i = 0; i < QC; ++i) mu[rr] += v[rr][i];
+    for (int i = 0; i < NG; ++i) mu[rr] += v[rr][i];
   }
   if (r.mode == NORM_LN) {
     block_sums<RB>(mu, scratch);
 #pragma unroll
-    for (int rr = 0; rr < RB; ++rr) mu[rr] /= r.d;
+    for (int rr = 0; rr < RB; ++rr) mu[rr] /= d;
   } else {
 #pragma unroll
     for (int rr = 0; rr < RB; ++rr) mu[rr] = 0.f;
@@ -513,8 +508,8 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
   for (int rr = 0; rr < RB; ++rr) {
     st[rr] = 0.f;
 #pragma unroll
-    for (int i = 0; i < QC; ++i) {
-      const float t = i < ng ? v[rr][i] - mu[rr] : 0.f;
+    for (int i = 0; i < NG; ++i) {
+      const float t = v[rr][i] - mu[rr];
       st[rr] += t * t;
     }
   }
@@ -522,13 +517,12 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
   float* nrm = reinterpret_cast<float*>(nrm4);
 #pragma unroll
   for (int rr = 0; rr < RB; ++rr) {
-    const float rs = rsqrtf(st[rr] / r.d + r.eps);
+    const float rs = rsqrtf(st[rr] / d + r.eps);
 #pragma unroll
-    for (int i = 0; i < QC; ++i) {
-      if (i >= ng) break;
+    for (int i = 0; i < NG; ++i) {
       float t = (v[rr][i] - mu[rr]) * rs * (1.f + mv[i]);
       if (r.shift) t += sv[i];
-      nrm[rr * QC * 256 + threadIdx.x + 256 * i] = t;
+      nrm[rr * d + threadIdx.x + 256 * i] = t;
     }
   }
   __syncthreads();
@@ -537,25 +531,21 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
   // finishes each (row, output)
 #pragma unroll
   for (int rr = 0; rr < RB; ++rr) {
-    float4 n4[QC];
+    float4 n4[NG];
 #pragma unroll
-    for (int i = 0; i < QC; ++i)
-      if (i < ng) n4[i] = nrm4[rr][lane + kWave * i];
+    for (int i = 0; i < NG; ++i) n4[i] = nrm4[rr][lane + kWave * i];
 #pragma unroll
     for (int q = 0; q < QA; ++q) {
-      const int a = wave + 4 * q;
-      if (a >= r.A) break;
       float acc = 0.f;
 #pragma unroll
-      for (int i = 0; i < QC; ++i) {
-        if (i >= ng) break;
+      for (int i = 0; i < NG; ++i) {
         acc = fmaf(n4[i].x, w4[q][i].x, acc);
         acc = fmaf(n4[i].y, w4[q][i].y, acc);
         acc = fmaf(n4[i].z, w4[q][i].z, acc);
         acc = fmaf(n4[i].w, w4[q][i].w, acc);
       }
       acc = wave_sum(acc);
-      if (lane == 0) red[rr][a] = acc;
+      if (lane == 0 && wave + 4 * q < r.A) red[rr][wave + 4 * q] = acc;
     }
   }
   __syncthreads();
@@ -636,10 +626,16 @@ void embed_state(const CallDesc* desc, const float* w, const float* b, float* e,
 }
 void readout_euler(const ReadoutArgs& r, hipStream_t s) {
   const int rows = r.B * r.H;
-  if (r.d % 256 == 0 && r.d <= 1024 && r.A <= 32) {
-    if (r.pend.n == 0 && rows >= 1024) hipLaunchKernelGGL(readout_rows_kernel<4>, dim3((rows + 3) / 4), dim3(256), 0, s, r);
-    else hipLaunchKernelGGL(readout_rows_kernel<1>, dim3(rows), dim3(256), 0, s, r);
-  } else {
+  auto rows_kernel = [&](auto ng) {
+    constexpr int NG = decltype(ng)::value;
+    if (r.pend.n == 0 && rows >= 1024)
+      hipLaunchKernelGGL((readout_rows_kernel<4, NG>), dim3((rows + 3) / 4), dim3(256), 0, s, r);
+    else
+      hipLaunchKernelGGL((readout_rows_kernel<1, NG>), dim3(rows), dim3(256), 0, s, r);
+  };
+  if (r.A <= 32 && r.d == 1024) rows_kernel(std::integral_constant<int, 4>{});
+  else if (r.A <= 32 && r.d == 256) rows_kernel(std::integral_constant<int, 1>{});
+  else {
     hipLaunchKernelGGL(readout_kernel, dim3(rows), dim3(256), 0, s, r);
   }
 }
