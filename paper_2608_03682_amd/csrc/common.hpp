@@ -101,12 +101,6 @@ __device__ __forceinline__ float wave_sum(float v) {
   return v;
 }
 
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, kWave));
-  return v;
-}
-
 // Sum over the block; `scratch` holds one float per wave.  All threads get it.
 template <int NT>
 __device__ __forceinline__ float block_sum(float v, float* scratch) {

@@ -272,20 +272,27 @@ __device__ __forceinline__ int aswz(int row) { return (row >> 1) & 7; }
 // then streams about one band of W.  Otherwise (and for the QKV epilogue,
 // whose cost differs a lot between bands because of the transposed V
 // stores) the plain order is kept: row tile fastest over the block index.
-// (A row-major split by XCD for A-heavy shapes measured no better.)
-constexpr int kOrderPlain = 0, kOrderBands = 2;
+// With one tile per CU (the four-stage ring) and the activations the larger
+// operand, the tiles go row by row and XCD x takes the x-th eighth, so that
+// each activation row tile is streamed by one XCD.  (For the grid-strided
+// kernel that row split measured no better than the plain order.)
+constexpr int kOrderPlain = 0, kOrderRows = 1, kOrderBands = 2;
 constexpr int kBand = 8;
 __host__ __device__ inline int gemm_tiles(const GemmArgs& g) { return ((g.R + 127) / 128) * (g.NPT / 4); }
-__host__ __device__ inline int tile_order(const GemmArgs& g, bool plain) {
+__host__ __device__ inline int tile_order(const GemmArgs& g, bool plain, bool rows_ok = false) {
   if (plain) return kOrderPlain;
   const int wb = g.kind == W_FP8 ? 1 : 2;
-  return (int64_t)32 * g.NPT * wb >= (int64_t)2 * g.R ? kOrderBands : kOrderPlain;
+  if ((int64_t)32 * g.NPT * wb >= (int64_t)2 * g.R) return kOrderBands;
+  return rows_ok ? kOrderRows : kOrderPlain;
 }
 // Position t of the order -> (row tile, column tile).
 __device__ __forceinline__ void tile_at(int t, int mtiles, int ntiles, int order, int& mi, int& ni) {
   if (order == kOrderPlain) {
     mi = t % mtiles;
     ni = t / mtiles;
+  } else if (order == kOrderRows) {
+    mi = t / ntiles;
+    ni = t % ntiles;
   } else {
     const int band = t / (mtiles * kBand);
     const int rem = t - band * mtiles * kBand;
@@ -322,13 +329,14 @@ inline int xcd_grid(int T, int cap) {
 // requested together before any of their stores; MG trades registers (and so
 // occupancy) against memory round trips.  MG = 0 finishes each element before
 // loading the next.
-template <int MG, class Epi>
-__device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const Epi& epi, const f32x4 (&acc)[4][4], int r0,
+template <int MG, class Epi, int NT>
+__device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const Epi& epi, const f32x4 (&acc)[4][NT], int r0,
                                               int p0, int lc, int lg) {
   static_assert(MG == 0 || 4 % MG == 0, "row groups come in 4s");
+  constexpr int NP = NT / 2;                  // pair tiles of the wave tile
   if constexpr (MG == 0) {
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp) {
+    for (int pp = 0; pp < NP; ++pp) {
       const int p = p0 + pp;
       const float s0c = g.scale ? g.scale[32 * p + lc] : 1.f;
       const float s1c = g.scale ? g.scale[32 * p + 16 + lc] : 1.f;
@@ -342,10 +350,10 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const Epi& epi,
     }
     return;
   }
-  typename Epi::ColPre cpre[2];
-  float sc[2][2];
+  typename Epi::ColPre cpre[NP];
+  float sc[NP][2];
 #pragma unroll
-  for (int pp = 0; pp < 2; ++pp) {
+  for (int pp = 0; pp < NP; ++pp) {
     cpre[pp] = epi.colpre(p0 + pp, lc);
     sc[pp][0] = g.scale ? g.scale[32 * (p0 + pp) + lc] : 1.f;
     sc[pp][1] = g.scale ? g.scale[32 * (p0 + pp) + 16 + lc] : 1.f;
@@ -353,9 +361,9 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const Epi& epi,
   constexpr int MS = MG > 0 ? MG : 4;
 #pragma unroll
   for (int m0 = 0; m0 < 4; m0 += MS) {
-    typename Epi::Pre pre[2][MS][4];
+    typename Epi::Pre pre[NP][MS][4];
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
+    for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
       for (int mi = 0; mi < MS; ++mi)
 #pragma unroll
@@ -364,7 +372,7 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const Epi& epi,
           if (row < g.R) pre[pp][mi][v] = epi.pre(row, p0 + pp, lc);
         }
 #pragma unroll
-    for (int pp = 0; pp < 2; ++pp)
+    for (int pp = 0; pp < NP; ++pp)
 #pragma unroll
       for (int mi = 0; mi < MS; ++mi)
 #pragma unroll
@@ -500,32 +508,38 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
 // shapes (3264 rows, fp8 weights): faster for K = 1024 (QKV 28.5 vs 39 us,
 // GeGLU 65 vs 77 us), slower for K >= 2048, where the other one is used.
 // ---------------------------------------------------------------------------
-template <bool FP8>
+template <bool FP8, int NW = 4>
 struct RingCfg {
   static constexpr int FB = FP8 ? 1024 : 2048;   // bytes per (pair, half) fragment per k-block
   static constexpr int A_KB = 16, B_KB = 8 * FB / 1024;
   static constexpr int STAGE = (A_KB + B_KB) * 1024;
-  static constexpr int A_LD = A_KB / 4, B_LD = B_KB / 4;
+  static constexpr int A_LD = A_KB / NW, B_LD = B_KB / NW;   // 1 KiB DMA blocks per wave
 };
 
 // NS = 2: two stages (48 KiB fp8 / 64 KiB bf16), so three (two) blocks share
 // a CU and cover each other's load latency.  NS = 4: for GEMMs with at most
 // one tile per CU, where no other block is there to do that: four stages
 // (96 / 128 KiB), two k-blocks in flight while one is computed, and the
-// register room of a lone block for the batched epilogue.
-template <class Epi, bool FP8, int NS = 2>
-__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NS > 2 ? 1 : (FP8 ? 3 : 2)))) void gemm_ring_kernel(
-    GemmArgs g, Epi epi) {
-  typedef RingCfg<FP8> C;
+// register room of a lone block for the batched epilogue.  WN = waves along
+// N: 2 (four 64 x 64 wave tiles) or 4 (eight 64 x 32 wave tiles, two waves
+// per SIMD for a lone block, so that one wave's LDS reads and fp8
+// conversions overlap the other's MFMAs).
+template <class Epi, bool FP8, int NS = 2, int WN = 2>
+__global__ __launch_bounds__(128 * WN) __attribute__((amdgpu_waves_per_eu(NS > 2 ? WN / 2 : (WN == 4 ? 4 : (FP8 ? 3 : 2))))) void
+gemm_ring_kernel(GemmArgs g, Epi epi) {
+  constexpr int NW = 2 * WN;                  // waves per block
+  constexpr int NT = 8 / WN;                  // 16-column MFMA tiles per wave (NT / 2 pair tiles)
+  typedef RingCfg<FP8, NW> C;
   static_assert(NS == 2 || NS == 4, "two or four stages");
+  static_assert(WN == 2 || (WN == 4 && !Epi::kWaveTile), "eight waves only with the generic epilogue");
   __shared__ __attribute__((aligned(1024))) uint8_t ring[NS * C::STAGE];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int wv = __builtin_amdgcn_readfirstlane(wave);
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int lc = lane % 16, lg = lane / 16;
   const int nkb = g.K / 64;
   const int mtiles = (g.R + 127) / 128, ntiles = g.NPT / 4;
-  const int order = tile_order(g, Epi::kWaveTile);
+  const int order = tile_order(g, Epi::kWaveTile, NS == 4);
   const int t = xcd_tile(blockIdx.x, 0, gridDim.x, mtiles * ntiles, order);
   if (t < 0) return;
   int mi, ni;
@@ -537,39 +551,39 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NS > 2 ? 1 
   int aoff[C::A_LD];
 #pragma unroll
   for (int i = 0; i < C::A_LD; ++i) {
-    const int row = 8 * (4 * i + wave) + lane / 8;       // 1 KiB block 4i + wave = rows 8 blk ..
+    const int row = 8 * (NW * i + wave) + lane / 8;      // 1 KiB block NW i + wave = rows 8 blk ..
     aoff[i] = min(m0 + row, g.R - 1) * g.lda + 8 * ((lane % 8) ^ aswz(row));
   }
   const uint8_t* bsrc[C::B_LD];
 #pragma unroll
   for (int i = 0; i < C::B_LD; ++i) {
-    const int blk = 4 * i + wave;
+    const int blk = NW * i + wave;
     const int f = blk / (C::FB / 1024), part = blk % (C::FB / 1024);
     bsrc[i] = W + ((int64_t)(pt0 + f / 2) * nkb * 2 + f % 2) * C::FB + part * 1024 + lane * 16;
   }
   auto issue = [&](int slot, int kb) {
     uint8_t* base = ring + slot * C::STAGE;
 #pragma unroll
-    for (int i = 0; i < C::A_LD; ++i) dma16(A + aoff[i] + kb * 64, (lds_void_t*)(base + (4 * i + wv) * 1024));
+    for (int i = 0; i < C::A_LD; ++i) dma16(A + aoff[i] + kb * 64, (lds_void_t*)(base + (NW * i + wv) * 1024));
 #pragma unroll
     for (int i = 0; i < C::B_LD; ++i)
-      dma16(bsrc[i] + (int64_t)kb * 2 * C::FB, (lds_void_t*)(base + (C::A_KB + 4 * i + wv) * 1024));
+      dma16(bsrc[i] + (int64_t)kb * 2 * C::FB, (lds_void_t*)(base + (C::A_KB + NW * i + wv) * 1024));
   };
 
-  f32x4 acc[4][4];
+  f32x4 acc[4][NT];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NT; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   auto compute = [&](int slot) {
     const bf16_t* As = reinterpret_cast<const bf16_t*>(ring + slot * C::STAGE);
     const uint8_t* Bs = ring + slot * C::STAGE + C::A_KB * 1024;
     constexpr int BW = FP8 ? 1 : 2;
-    uint4 braw[4][BW];
+    uint4 braw[NT][BW];
 #pragma unroll
-    for (int nt = 0; nt < 4; ++nt) {
-      const int f = 2 * (2 * wn + nt / 2) + nt % 2;
+    for (int nt = 0; nt < NT; ++nt) {
+      const int f = 2 * ((NT / 2) * wn + nt / 2) + nt % 2;
 #pragma unroll
       for (int w = 0; w < BW; ++w) braw[nt][w] = *reinterpret_cast<const uint4*>(Bs + f * C::FB + lane * 16 * BW + 16 * w);
     }
@@ -584,9 +598,9 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NS > 2 ? 1 
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int st = 0; st < 2; ++st) {
-      bf16x8 bfr[4];
+      bf16x8 bfr[NT];
 #pragma unroll
-      for (int nt = 0; nt < 4; ++nt) {
+      for (int nt = 0; nt < NT; ++nt) {
         if (FP8) bfr[nt] = st == 0 ? fp8x8_to_bf16x8(braw[nt][0].x, braw[nt][0].y)
                                    : fp8x8_to_bf16x8(braw[nt][0].z, braw[nt][0].w);
         else bfr[nt] = as_bf16x8(braw[nt][BW - 1 < st ? 0 : st]);
@@ -594,7 +608,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NS > 2 ? 1 
 #pragma unroll
       for (int mt = 0; mt < 4; ++mt)
 #pragma unroll
-        for (int nt = 0; nt < 4; ++nt) acc[mt][nt] = mfma16x16x32(af[st][mt], bfr[nt], acc[mt][nt]);
+        for (int nt = 0; nt < NT; ++nt) acc[mt][nt] = mfma16x16x32(af[st][mt], bfr[nt], acc[mt][nt]);
     }
   };
 
@@ -622,7 +636,7 @@ __global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(NS > 2 ? 1 
   }
 
   if constexpr (Epi::kWaveTile) epi.wave_tile(g, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
-  else tile_epilogue<NS == 2 ? 0 : 4>(g, epi, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
+  else tile_epilogue<NS == 2 ? 0 : 4>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg);
 }
 
 }  // namespace
@@ -648,20 +662,23 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
     const int tiles = gemm_tiles(g);
     const char* force = getenv("PHYAI_GEMM_TILE");   // tests: "ring" / "deep" / "strided" (read at enqueue time)
     // at most one tile per CU: no second block covers the load latency, so
-    // the four-stage ring; otherwise the two-stage ring for short K and the
-    // strided kernel for long K
+    // the four-stage ring with eight waves (two per SIMD); otherwise the
+    // two-stage ring for short K and the strided kernel for long K
     const bool deep = !Epi::kWaveTile && (force ? strcmp(force, "deep") == 0 : tiles <= 256);
     const bool ring = force ? strcmp(force, "strided") != 0 : g.K <= 1024;
     if (deep) {
       const dim3 rgrid(xcd_grid(tiles, 1 << 30));
       if constexpr (!Epi::kWaveTile) {
-        if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true, 4>), rgrid, dim3(256), 0, s, g, epi);
-        else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false, 4>), rgrid, dim3(256), 0, s, g, epi);
+        if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true, 4, 4>), rgrid, dim3(512), 0, s, g, epi);
+        else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false, 4, 4>), rgrid, dim3(512), 0, s, g, epi);
       }
     } else if (ring) {
+      // eight waves per block too, except for the QKV epilogue, whose wave-tile
+      // form is written for 64 x 64 wave tiles
       const dim3 rgrid(xcd_grid(tiles, 1 << 30));
-      if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true>), rgrid, dim3(256), 0, s, g, epi);
-      else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false>), rgrid, dim3(256), 0, s, g, epi);
+      constexpr int WN = Epi::kWaveTile ? 2 : 4;
+      if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true, 2, WN>), rgrid, dim3(128 * WN), 0, s, g, epi);
+      else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false, 2, WN>), rgrid, dim3(128 * WN), 0, s, g, epi);
     } else {
       dim3 grid(xcd_grid(tiles, 512));
       if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_tiled_kernel<Epi, true>), grid, dim3(256), 0, s, g, epi);
