@@ -285,11 +285,20 @@ __host__ __device__ inline int tile_order(const GemmArgs& g, bool plain, bool ro
   if ((int64_t)32 * g.NPT * wb >= (int64_t)2 * g.R) return kOrderBands;
   return rows_ok ? kOrderRows : kOrderPlain;
 }
-// Position t of the order -> (row tile, column tile).
-__device__ __forceinline__ void tile_at(int t, int mtiles, int ntiles, int order, int& mi, int& ni) {
+// Position t of the order -> (row tile, column tile).  In the plain order a
+// partial last row tile (tail) comes after all the full ones: the positions
+// past two blocks per CU, which share a CU with two others, are then cheap
+// half-empty tiles instead of full ones.
+__device__ __forceinline__ void tile_at(int t, int mtiles, int ntiles, int order, bool tail, int& mi, int& ni) {
   if (order == kOrderPlain) {
-    mi = t % mtiles;
-    ni = t / mtiles;
+    const int full = tail ? mtiles - 1 : mtiles;
+    if (t < full * ntiles) {
+      mi = t % full;
+      ni = t / full;
+    } else {
+      mi = mtiles - 1;
+      ni = t - full * ntiles;
+    }
   } else if (order == kOrderRows) {
     mi = t / ntiles;
     ni = t % ntiles;
@@ -421,7 +430,7 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
     const int tile = xcd_tile(blockIdx.x, j, gridDim.x, mtiles * ntiles, order);
     if (tile < 0) break;
     int mi, ni;
-    tile_at(tile, mtiles, ntiles, order, mi, ni);
+    tile_at(tile, mtiles, ntiles, order, g.R % 128 != 0, mi, ni);
     const int mt0 = mi * 128;
     const int pt0 = ni * 4;
     int aoff[4];       // element offsets of this thread's A chunks (rows clamped into range)
@@ -543,7 +552,7 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
   const int t = xcd_tile(blockIdx.x, 0, gridDim.x, mtiles * ntiles, order);
   if (t < 0) return;
   int mi, ni;
-  tile_at(t, mtiles, ntiles, order, mi, ni);
+  tile_at(t, mtiles, ntiles, order, g.R % 128 != 0, mi, ni);
   const int m0 = mi * 128, pt0 = ni * 4;
   const bf16_t* A = static_cast<const bf16_t*>(g.A);
   const uint8_t* W = static_cast<const uint8_t*>(g.W);
