@@ -44,8 +44,8 @@ _ATTN_SRC = ("paper_2608_03682_amd/csrc/attention.hip", "paper_2608_03682_amd/cs
 _GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/kernels.hpp",
              "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
 MEASURED_TRAFFIC = {
-    ("pi0_bf16_b1", "attn"): {"bytes": 10044826, "sources": _ATTN_SRC, "sha256": "d90be19e0cc1a7c1"},
-    ("pi0_fp8_b64", "mlp_up"): {"bytes": 96023450, "sources": _GEMM_SRC, "sha256": "7ec127a1abd010cb"},
+    ("pi0_bf16_b1", "attn"): {"bytes": 10044803, "sources": _ATTN_SRC, "sha256": "8a35db6808aed333"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90704983, "sources": _GEMM_SRC, "sha256": "0f4eb62b841ed7fb"},
 }
 
 
