@@ -507,15 +507,15 @@ __global__ __launch_bounds__(256, 2) void gemm_tiled_kernel(GemmArgs g, Epi epi)
 }
 
 // ---------------------------------------------------------------------------
-// Ring-pipelined 128 x 128 GEMM for many rows and short K.  4 waves in a
-// 2 x 2 arrangement of 64 x 64; per k-block of 64 the activation tile and
-// the block's 8 packed weight fragments go through a 2-stage LDS ring (48
-// KiB per block for fp8 weights, so three blocks share a compute unit and
-// cover each other's barrier and load stalls); one barrier per k-block;
-// every fragment of a k-block is requested before its first MFMA.
-// Measured against the grid-strided kernel above on the rollout-batch
-// shapes (3264 rows, fp8 weights): faster for K = 1024 (QKV 28.5 vs 39 us,
-// GeGLU 65 vs 77 us), slower for K >= 2048, where the other one is used.
+// Ring-pipelined 128 x 128 GEMM for many rows.  Waves in a 2 x 2 (64 x 64
+// wave tiles) or 2 x 4 (64 x 32) arrangement; per k-block of 64 the
+// activation tile and the block's 8 packed weight fragments go through an
+// LDS ring of 2 or 4 stages (48 / 96 KiB per block for fp8 weights); one
+// barrier per k-block; every fragment of a k-block is requested before its
+// first MFMA.  On the rollout-batch shapes (3264 rows, fp8 weights) the
+// two-stage form beat the grid-strided kernel above for K = 1024 (QKV 28.5
+// vs 39 us, GeGLU 65 vs 77 us), and the four-stage eight-wave form beats
+// both wherever a GEMM has at most one tile per CU (O 23.5, down 38.7 us).
 // ---------------------------------------------------------------------------
 template <bool FP8, int NW = 4>
 struct RingCfg {
