@@ -644,8 +644,15 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
     }
   }
 
-  if constexpr (Epi::kWaveTile) epi.wave_tile(g, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg);
-  else tile_epilogue<NS == 2 ? 0 : 4>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg);
+  if constexpr (Epi::kWaveTile) {
+    // the ring is free once every wave is past its last k-block: each wave
+    // stages its V tile there
+    static_assert(NW * Epi::kVStage * 2 <= NS * C::STAGE, "V staging fits the ring");
+    bare_barrier();
+    epi.wave_tile(g, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg, reinterpret_cast<bf16_t*>(ring) + wave * Epi::kVStage);
+  } else {
+    tile_epilogue<NS == 2 ? 0 : 4>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg);
+  }
 }
 
 }  // namespace

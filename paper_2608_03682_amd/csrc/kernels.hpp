@@ -243,8 +243,14 @@ struct EpiQkv {
   // prefix length is requested before the group's stores; the per-element
   // form above would wait for each element's loads in turn.  Tiles that
   // reach past R take the per-element form.
+  // V tiles through LDS: `st` (kVStage elements per wave, or null) receives the
+  // wave's 64 x 64 tile as [column][row], and each store instruction then
+  // writes 64 consecutive keys of one V^T row (128 contiguous bytes) instead of
+  // 16 rows x 4 keys.
+  static constexpr int kVRow = 66;                    // padded row: 64 tokens, no bank conflicts
+  static constexpr int kVStage = 64 * kVRow;
   __device__ __forceinline__ void wave_tile(const GemmArgs& g, const f32x4 (&acc)[4][4], int r0, int p0, int lc,
-                                            int lg) const {
+                                            int lg, bf16_t* st = nullptr) const {
     const int tiles = D / 32;
     const int head = p0 / tiles;
     float sc[2][2];
@@ -312,7 +318,44 @@ struct EpiQkv {
     };
     if (head < nq) emit(std::integral_constant<int, 0>{});
     else if (head < nq + nkv) emit(std::integral_constant<int, 1>{});
-    else emit(std::integral_constant<int, 2>{});
+    else {
+      if constexpr (std::is_same<OutT, bf16_t>::value) {
+        if (st != nullptr) {
+          store_v_staged(acc, sc, r0, p0, lc, lg, st);
+          return;
+        }
+      }
+      emit(std::integral_constant<int, 2>{});
+    }
+  }
+
+  __device__ __forceinline__ void store_v_staged(const f32x4 (&acc)[4][4], const float (&sc)[2][2], int r0, int p0,
+                                                 int lc, int lg, bf16_t* st) const {
+    const int tiles = D / 32;
+    const int head = p0 / tiles;
+    {
+#pragma unroll
+      for (int pp = 0; pp < 2; ++pp)
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int row = 16 * mt + 4 * lg + v;
+            st[(32 * pp + lc) * kVRow + row] = f32_to_bf16(acc[mt][2 * pp][v] * sc[pp][0]);
+            st[(32 * pp + 16 + lc) * kVRow + row] = f32_to_bf16(acc[mt][2 * pp + 1][v] * sc[pp][1]);
+          }
+      const int lane = 16 * lg + lc;
+      const int row = r0 + lane;
+      const int key = (keys_after_prefix ? desc->prefix_len[row / M] : 0) + row % M;
+      bf16_t* vrow = reinterpret_cast<bf16_t*>(vt) + ((int64_t)(row / M) * nkv + (head - nq - nkv)) * D * ldk + key;
+      __builtin_amdgcn_s_waitcnt(0xC07F);             // the wave's LDS writes are done (lgkmcnt 0)
+#pragma unroll 8
+      for (int col = 0; col < 64; ++col) {
+        const int i = 16 * ((p0 + col / 32) % tiles) + col % 16;
+        const int d = i + ((col / 16) % 2) * (D / 2);
+        vrow[(int64_t)d * ldk] = st[col * kVRow + lane];
+      }
+    }
   }
 };
 
