@@ -43,6 +43,8 @@ def test_fp8_decode_all_codes_bit_exact():
     ("pi0", dict(weight_dtype="fp8", batch=4)),
     ("pi0", dict(batch=7)),                         # 357 rows: the tiled GEMM with a ragged row tile
     ("pi0", dict(weight_dtype="fp8", batch=7)),
+    ("pi0", dict(batch=21)),                        # 1071 rows, 1050 action rows: the row-blocked
+                                                    # embedding and readout, each with a partial last block
     ("pi05", {}),
     ("dit", {}),
     ("pi0", dict(weight_dtype="f32", kv_dtype="f32", state_token=False, rope=False)),
