@@ -44,8 +44,8 @@ _ATTN_SRC = ("paper_2608_03682_amd/csrc/attention.hip", "paper_2608_03682_amd/cs
 _GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/kernels.hpp",
              "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
 MEASURED_TRAFFIC = {
-    ("pi0_bf16_b1", "attn"): {"bytes": 10044803, "sources": _ATTN_SRC, "sha256": "4902d3cc2f319e20"},
-    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90704983, "sources": _GEMM_SRC, "sha256": "b9ded9575f12172f"},
+    ("pi0_bf16_b1", "attn"): {"bytes": 10044804, "sources": _ATTN_SRC, "sha256": "8a82a202841ce4ef"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90507969, "sources": _GEMM_SRC, "sha256": "6bdffcbb20f4acb8"},
 }
 
 
