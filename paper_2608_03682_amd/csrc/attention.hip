@@ -605,6 +605,20 @@ int64_t attention_partial_floats(int B, int M, int nq, int nkv, int D, int n_spl
   return attention_partial_ml_off(B, M, nq, nkv, D, n_split) + tiles * n_split * kRows * 2;
 }
 
+AttnParts attention_parts(const AttnArgs& a) {
+  AttnParts p{};
+  p.o = reinterpret_cast<const bf16_t*>(a.part);
+  p.ml = a.part + attention_partial_ml_off(a.B, a.M, a.nq, a.nkv, a.D, a.n_split);
+  p.n_split = a.n_split;
+  p.rows_per_tile = kRows;
+  p.G = a.nq / a.nkv;
+  p.ntiles = (a.M * p.G + kRows - 1) / kRows;
+  p.M = a.M;
+  p.nkv = a.nkv;
+  p.D = a.D;
+  return p;
+}
+
 void attention_bf16(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
   const int rows = a.M * (a.nq / a.nkv);
@@ -615,7 +629,7 @@ void attention_bf16(const AttnArgs& a0, hipStream_t s) {
   if (a.D == 256) hipLaunchKernelGGL(attn_mfma_kernel<256>, grid, dim3(256), 0, s, a);
   else if (a.D == 128) hipLaunchKernelGGL(attn_mfma_kernel<128>, grid, dim3(256), 0, s, a);
   else if (a.D == 64) hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, s, a);
-  if (a.n_split > 1) {
+  if (a.n_split > 1 && !a.defer_merge) {
     dim3 g2((rows + 3) / 4, a.B * a.nkv);
     auto comb = [&](auto dtag) {
       constexpr int DD = decltype(dtag)::value;

@@ -669,6 +669,149 @@ int gemm_split_k(int R, int NPT, int K) {
 
 namespace {
 
+// Output projection fed by key-split attention partials (small row counts).
+// Block = 16 token rows x 4 pair tiles (128 columns) x one 256-wide slice z of
+// K, i.e. of the concatenated heads; 8 waves.  Each thread first merges 8
+// consecutive elements of one row from all splits, o = sum_s w_s o_s /
+// sum_s w_s with w_s = l_s 2^(m_s - max m) (the split-softmax merge), into a
+// bf16 LDS panel.  Waves w and w + 4 then multiply the two halves of the
+// panel's K by pair tile w and add through LDS.  The split loads, the weights
+// and the epilogue inputs are all requested before the first wait, so the
+// block makes one memory round trip.  Rows past R merge row R-1 and are never
+// stored; splits past n_split re-read the last one and are skipped.  The 1-D
+// grid deals consecutive tiles (slice-major) to one XCD, so each XCD's L2
+// fetches the partials and weights of its own slices only.
+template <class Epi, bool FP8, int NS>
+__global__ __launch_bounds__(512) void merge_gemm_kernel(GemmArgs g, AttnParts ap, Epi epi) {
+  constexpr int KZ = 256;                     // K per slice
+  constexpr int KH = KZ / 128;                // k-blocks of 64 per wave half
+  __shared__ __attribute__((aligned(16))) bf16_t panel[16 * KZ];
+  __shared__ f32x4 red[4][2][kWave];
+  const int nx = (g.NPT + 3) / 4, ny = (g.R + 15) / 16;
+  const int T = nx * ny * (g.K / KZ);
+  const int t = (blockIdx.x % 8) * (int)(gridDim.x / 8) + blockIdx.x / 8;
+  if (t >= T) return;
+  const int z = t / (nx * ny), bx = t % nx, m0 = (t / nx) % ny * 16;
+  const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+  const int wq = wave % 4, kh = wave / 4;     // pair tile within the block, K half
+  const int pw = bx * 4 + wq;
+  const int p = min(pw, g.NPT - 1);
+  const int nkb = g.K / 64;
+  const int c = lane % 16, akg = lane / 16;
+
+  // weights of pair tile p over this wave's half of the slice
+  bf16x8 b[KH][2][2];
+#pragma unroll
+  for (int j = 0; j < KH; ++j)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int64_t frag = ((int64_t)(p * nkb + z * (KZ / 64) + kh * KH + j) * 2 + hf) * kWave + lane;
+      if (FP8) {
+        const u32x4_t v = gload16(static_cast<const uint4*>(g.W) + frag);
+        b[j][hf][0] = fp8x8_to_bf16x8(v.x, v.y);
+        b[j][hf][1] = fp8x8_to_bf16x8(v.z, v.w);
+      } else {
+        const uint4* src = static_cast<const uint4*>(g.W) + frag * 2;
+        b[j][hf][0] = __builtin_bit_cast(bf16x8, gload16(src));
+        b[j][hf][1] = __builtin_bit_cast(bf16x8, gload16(src + 1));
+      }
+    }
+
+  // split partials of row i, elements 8 cc .. 8 cc + 7 of the slice
+  const int i = threadIdx.x / 32, cc = threadIdx.x % 32;
+  const int r = min(m0 + i, g.R - 1);
+  const int rb = r / ap.M, tok = r % ap.M;
+  const int n = ap.n_split;
+  const int k = z * KZ + 8 * cc;
+  const int head = k / ap.D, dd = k % ap.D;
+  const int qr = tok * ap.G + head % ap.G;
+  const int64_t tile = (int64_t)(rb * ap.nkv + head / ap.G) * ap.ntiles + qr / ap.rows_per_tile;
+  const int lrow = qr % ap.rows_per_tile;
+  uint4 ov[NS];
+  f32x2 ml[NS];
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    const int se = s < n ? s : n - 1;
+    const int64_t prow = (tile * n + se) * ap.rows_per_tile + lrow;
+    ov[s] = *reinterpret_cast<const uint4*>(ap.o + prow * ap.D + dd);
+    ml[s] = *reinterpret_cast<const f32x2*>(ap.ml + prow * 2);
+  }
+  // epilogue inputs last: a wait the compiler puts behind their branch then
+  // finds every load already issued
+  float* sp = g.split_out ? g.split_out + (int64_t)z * g.split_stride : nullptr;
+  const float sc0 = g.scale ? g.scale[32 * p + c] : 1.f;
+  const float sc1 = g.scale ? g.scale[32 * p + 16 + c] : 1.f;
+  typename Epi::ColPre cq{};
+  typename Epi::Pre pre[4]{};
+  if (!sp) {
+    cq = epi.colpre(p, c);
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int row = m0 + 4 * akg + v;
+      pre[v] = epi.pre(row < g.R ? row : 0, p, c);
+    }
+  }
+  float mmax = -1e30f;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) mmax = fmaxf(mmax, s < n ? ml[s][0] : -1e30f);
+  float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  float lsum = 0.f;
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    if (s < n) {
+      const float w = ml[s][1] * __builtin_amdgcn_exp2f(ml[s][0] - mmax);
+      lsum += w;
+      const uint32_t q[4] = {ov[s].x, ov[s].y, ov[s].z, ov[s].w};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        acc8[2 * e] = fmaf(w, __uint_as_float(q[e] << 16), acc8[2 * e]);
+        acc8[2 * e + 1] = fmaf(w, __uint_as_float(q[e] & 0xffff0000u), acc8[2 * e + 1]);
+      }
+    }
+  }
+  const float inv = lsum > 0.f ? 1.f / lsum : 0.f;
+  uint4 pk;
+  pk.x = pack_bf16x2(acc8[0] * inv, acc8[1] * inv);
+  pk.y = pack_bf16x2(acc8[2] * inv, acc8[3] * inv);
+  pk.z = pack_bf16x2(acc8[4] * inv, acc8[5] * inv);
+  pk.w = pack_bf16x2(acc8[6] * inv, acc8[7] * inv);
+  // 16-byte chunk cc of row i sits at cc ^ i: the 16 rows one MFMA operand
+  // read covers then hit 16 different bank groups
+  *reinterpret_cast<uint4*>(panel + i * KZ + 8 * (cc ^ i)) = pk;
+  __syncthreads();
+
+  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+#pragma unroll
+  for (int j = 0; j < KH; ++j)
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int ch = 8 * (kh * KH + j) + 4 * s + akg;
+      const bf16x8 a = as_bf16x8(*reinterpret_cast<const uint4*>(panel + c * KZ + 8 * (ch ^ c)));
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) acc[hf] = mfma16x16x32(a, b[j][hf][s], acc[hf]);
+    }
+  if (kh == 1) {
+    red[wq][0][lane] = acc[0];
+    red[wq][1][lane] = acc[1];
+  }
+  __syncthreads();
+  if (kh == 1 || pw >= g.NPT) return;
+  acc[0] += red[wq][0][lane];
+  acc[1] += red[wq][1][lane];
+  const int N = 32 * g.NPT;
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int row = m0 + 4 * akg + v;
+    if (row >= g.R) continue;
+    if (sp) {
+      sp[(int64_t)row * N + 32 * p + c] = acc[0][v] * sc0;
+      sp[(int64_t)row * N + 32 * p + 16 + c] = acc[1][v] * sc1;
+    } else {
+      epi.apply(row, p, c, cq, pre[v], acc[0][v] * sc0, acc[1][v] * sc1);
+    }
+  }
+}
+
 template <class Epi>
 void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
   if (g.kind == W_F32) {
@@ -727,5 +870,19 @@ void gemm_qkv_bf16(const GemmArgs& g, const EpiQkv<bf16_t>& e, hipStream_t s) { 
 void gemm_qkv_f32(const GemmArgs& g, const EpiQkv<float>& e, hipStream_t s) { launch(g, e, s); }
 void gemm_kv_bf16(const GemmArgs& g, const EpiKV<bf16_t>& e, hipStream_t s) { launch(g, e, s); }
 void gemm_kv_f32(const GemmArgs& g, const EpiKV<float>& e, hipStream_t s) { launch(g, e, s); }
+
+void gemm_merge_resid(const GemmArgs& g, const AttnParts& ap, const EpiResid& e, hipStream_t s) {
+  const int tiles = ((g.NPT + 3) / 4) * ((g.R + 15) / 16) * (g.K / 256);
+  const dim3 grid(8 * ((tiles + 7) / 8));
+  const bool fp8 = g.kind == W_FP8;
+  auto go = [&](auto ns) {
+    constexpr int NS = decltype(ns)::value;
+    if (fp8) hipLaunchKernelGGL((merge_gemm_kernel<EpiResid, true, NS>), grid, dim3(512), 0, s, g, ap, e);
+    else hipLaunchKernelGGL((merge_gemm_kernel<EpiResid, false, NS>), grid, dim3(512), 0, s, g, ap, e);
+  };
+  if (ap.n_split <= 4) go(std::integral_constant<int, 4>{});
+  else if (ap.n_split <= 8) go(std::integral_constant<int, 8>{});
+  else go(std::integral_constant<int, 16>{});
+}
 
 }  // namespace phyai

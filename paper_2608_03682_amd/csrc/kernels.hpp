@@ -416,6 +416,7 @@ struct AttnArgs {
   float* part;              // split partials (n_split > 1)
   int64_t part_ml_off;      // set by the launcher
   int n_split;
+  int defer_merge;          // n_split > 1: leave the partials for gemm_merge_resid
   const CallDesc* desc;
   int B, M, nq, nkv, D;
   float scale;              // 1/sqrt(D)
@@ -424,6 +425,25 @@ struct AttnArgs {
 void attention_bf16(const AttnArgs&, hipStream_t);
 void attention_f32(const AttnArgs&, hipStream_t);
 int64_t attention_partial_floats(int B, int M, int nq, int nkv, int D, int n_split);
+
+// Key-split partials of one bf16 attention launch: O rows [tile][split][rows_per_tile][D]
+// (bf16, each split normalised by its own softmax sum) and (m, l) [tile][split][rows_per_tile]
+// (float2).  Query row qr = token * G + (head % G) of group b * nkv + head / G sits in tile
+// group * ntiles + qr / rows_per_tile.
+struct AttnParts {
+  const bf16_t* o;
+  const float* ml;
+  int n_split, ntiles, rows_per_tile;
+  int M, G, nkv, D;
+};
+AttnParts attention_parts(const AttnArgs&);
+
+// Output projection that takes its A operand (the attention output, [R][nq*D]) straight
+// from the key-split partials, merging them on the way in (small row counts).  K runs in
+// slices of 256 (blockIdx.z); with g.split_out set each slice goes there raw (g.split_k =
+// K / 256 slices), otherwise the epilogue adds into h.  Needs K % 256 == 0, 256 % D == 0,
+// 2 <= n_split <= 16 and bf16 or fp8 weights.
+void gemm_merge_resid(const GemmArgs&, const AttnParts&, const EpiResid&, hipStream_t);
 
 // Copy the caller's prefix K and transpose its V ([L][2][B][P][nkv*D]) into
 // the per-layer key ranges (layer l at K/Vt + l * layer_stride).

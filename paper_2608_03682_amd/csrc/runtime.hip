@@ -325,11 +325,32 @@ int attn_splits(int B, int rows, int nkv, int keys) {
   return s < 1 ? 1 : s;
 }
 
+// key splits of block l's attention at batch B (DiT: even blocks attend to
+// the features, odd ones to the suffix)
+int attn_split_of(const phyai_expert& e, int l, int B) {
+  if (e.f32) return 1;
+  const int rows = e.M * (e.nq / e.nkv);
+  const int keys = e.c.variant != PHYAI_VARIANT_DIT ? e.P + e.M : (l % 2 == 0 ? e.P : e.M);
+  return attn_splits(B, rows, e.nkv, keys);
+}
+
+// Whether block l's output projection merges the attention's key splits
+// itself (small row counts; PHYAI_ATTN_MERGE=kernel keeps the separate merge
+// kernel, read at enqueue time).  It then splits K into 256-wide slices.
+bool oproj_merges(const phyai_expert& e, int l, int B) {
+  if (e.f32 || B * e.M >= 256) return false;
+  const char* f = getenv("PHYAI_ATTN_MERGE");
+  if (f && strcmp(f, "kernel") == 0) return false;
+  const int K = e.nq * e.D;
+  return attn_split_of(e, l, B) > 1 && K % 256 == 0 && K / 256 <= 8 && 256 % e.D == 0;
+}
+
 // Split over K used for a residual GEMM of block l (which: 0 = O projection,
 // 1 = down / MLP-out projection) at batch B; 1 means the epilogue adds into h
 // directly.
 int resid_split(const phyai_expert& e, int which, int l, int B) {
   if (e.f32) return 1;
+  if (which == 0 && oproj_merges(e, l, B)) return e.nq * e.D / 256;
   const Lin& w = which == 0 ? e.layers[l].o : e.layers[l].down;
   return gemm_split_k(B * e.M, w.NPT, w.K);
 }
@@ -383,7 +404,6 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   const int S = 2 * L + 1;   // pi0.5 norm sites
   const LayerW& w = e.layers[l];
   const float inv_sqrt_d = 1.0f / std::sqrt((float)D);
-  const int rows = M * (e.nq / e.nkv);
   AttnArgs at{};
   at.q = q; at.ldq = e.qd;
   at.K = kl; at.Vt = vl; at.ldk = e.ldk;
@@ -392,6 +412,15 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   at.desc = e.desc;
   at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
   at.scale = inv_sqrt_d;
+  at.n_split = attn_split_of(e, l, B);
+  const bool merge_in_o = oproj_merges(e, l, B);
+  at.defer_merge = merge_in_o ? 1 : 0;
+  // output projection: from the merged attention output, or from its key-split partials
+  auto oproj = [&](const EpiResid& er) {
+    const GemmArgs ga = with_split(gargs(w.o, o, e.qd, R), 0);
+    if (merge_in_o) gemm_merge_resid(ga, attention_parts(at), er, s);
+    else gemm_resid(ga, er, s);
+  };
 
   if (variant != PHYAI_VARIANT_DIT) {
     const float* mul1 = w.attn_norm;
@@ -419,11 +448,10 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
         at.keys_from_prefix = 1;
         at.n_suffix = M;
         at.mask_mode = e.c.state_token ? 1 : 0;
-        at.n_split = e.f32 ? 1 : attn_splits(B, rows, e.nkv, e.P + M);
         if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
         break;
       }
-      case ST_OPROJ: gemm_resid(with_split(gargs(w.o, o, e.qd, R), 0), EpiResid{e.h, d, nullptr, nullptr}, s); break;
+      case ST_OPROJ: oproj(EpiResid{e.h, d, nullptr, nullptr}); break;
       case ST_NORM2:
         norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul2, sh2, pending_of(e, 0, l, k, B), s);
         break;
@@ -455,11 +483,10 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
       at.keys_from_prefix = cross ? 1 : 0;
       at.n_suffix = cross ? 0 : M;
       at.mask_mode = 0;
-      at.n_split = e.f32 ? 1 : attn_splits(B, rows, e.nkv, cross ? e.P : M);
       if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
       break;
     }
-    case ST_OPROJ: gemm_resid(with_split(gargs(w.o, o, e.qd, R), 0), EpiResid{e.h, d, nullptr, g1}, s); break;
+    case ST_OPROJ: oproj(EpiResid{e.h, d, nullptr, g1}); break;
     case ST_NORM2: norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, sc2, sh2, pending_of(e, 0, l, k, B), s); break;
     case ST_MLP_UP:
       gemm_store(with_lo(gargs(w.gu, n, d, R), n_lo), store_epi<T>(g, e.F, w.mlp_b1, nullptr, ACT_GELU), s);
@@ -817,7 +844,9 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
         const int R = B * e->M;
         for (int l = 0; l < L; ++l)
           for (int which = 0; which < 2; ++which) {
-            const int sk = resid_split(*e, which, l, B);
+            // either O-projection form (the merge one may be switched off per call)
+            const Lin& w = which == 0 ? e->layers[l].o : e->layers[l].down;
+            const int sk = std::max(resid_split(*e, which, l, B), gemm_split_k(R, w.NPT, w.K));
             if (sk > 1) pend = std::max(pend, (int64_t)sk * R * d);
           }
       }

@@ -58,6 +58,27 @@ def test_small_parity(variant, kw):
     compare(f"small_{variant}_{kw}", gpu, _oracle(cfg, case), cfg)
 
 
+@pytest.mark.parametrize("variant,kw", [
+    ("pi0", {}),
+    ("pi0", dict(head_dim=256, n_q_heads=2, weight_dtype="fp8")),
+    ("dit", {}),
+])
+def test_separate_attention_merge(variant, kw):
+    """At small row counts the output projection merges the attention's key
+    splits itself; PHYAI_ATTN_MERGE=kernel keeps the separate merge kernel,
+    which must agree with the oracle as well."""
+    cfg = small_cfg(variant, **kw)
+    print(f"[case] separate merge {variant} {kw}", flush=True)
+    case = wl.make_case(cfg, seed=5)
+    os.environ["PHYAI_ATTN_MERGE"] = "kernel"
+    try:
+        ex = _expert(cfg, case)
+        gpu = run_gpu(ex, case)
+    finally:
+        del os.environ["PHYAI_ATTN_MERGE"]
+    compare(f"separate merge {variant} {kw}", gpu, _oracle(cfg, case), cfg)
+
+
 def test_tiny_fp32_full_config():
     cfg = wl.CONFIGS["tiny_fp32"]
     print("[case] tiny_fp32", flush=True)
