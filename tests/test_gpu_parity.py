@@ -1,6 +1,7 @@
 """GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
 same seeded inputs.  Bars: max-abs <= tol * max(1, rms(oracle)) with tol
 1e-4 (fp32 path), 2e-2 (bf16), 5e-2 (fp8 weights)."""
+import dataclasses
 import os
 
 import numpy as np
@@ -77,6 +78,29 @@ def test_separate_attention_merge(variant, kw):
     finally:
         del os.environ["PHYAI_ATTN_MERGE"]
     compare(f"separate merge {variant} {kw}", gpu, _oracle(cfg, case), cfg)
+
+
+@pytest.mark.parametrize("variant,kw,plen", [
+    ("pi0", {}, [0, 1, 100, 64]),
+    ("pi0", dict(weight_dtype="fp8"), [0, 1, 100, 64]),
+    ("pi0", dict(batch=7), [0, 100, 1, 64, 63, 65, 0]),   # 357 rows: the many-row GEMMs, no key split
+    ("pi05", {}, [0, 1, 100, 64]),
+    ("dit", {}, [1, 40]),
+])
+def test_edge_prefix_lengths(variant, kw, plen):
+    """Prefix lengths at the edges of the key range: none (the suffix keys
+    only; a DiT request needs at least one feature row), a single key, the
+    full capacity, and whole 64-key tiles with one key more or less."""
+    kw = dict(kw)
+    kw.setdefault("batch", len(plen))
+    cfg = small_cfg(variant, **kw)
+    pl = np.array(plen, np.int32)
+    print(f"[case] edge prefixes {variant} {kw} {plen}", flush=True)
+    case = wl.make_case(cfg, seed=6)
+    case = dataclasses.replace(case, prefix_len=pl, prefix=wl.make_prefix(cfg, pl, 6))
+    ex = _expert(cfg, case)
+    gpu = run_gpu(ex, case)
+    compare(f"edge prefixes {variant} {kw} {plen}", gpu, _oracle(cfg, case), cfg)
 
 
 def test_tiny_fp32_full_config():
