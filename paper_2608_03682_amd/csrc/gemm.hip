@@ -30,12 +30,12 @@ __device__ __forceinline__ u32x4_t gload16(const void* p) { return *(gu32x4_t*)(
 // load issued (as global loads, so that the compiler can count them) before
 // the first MFMA; `hook` runs between the loads and the MFMAs.  Columns past
 // N re-read the last pair tile.
-template <int U, bool FP8, bool SPLIT, int NT, class Hook>
+template <int U, bool FP8, bool SPLIT, int NT, int MT, class Hook>
 __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int lane, int kb,
-                                        const bf16_t* const (&arp)[kMT], const bf16_t* const (&alp)[kMT],
-                                        f32x4 (&acc)[kMT][NT], const Hook& hook) {
+                                        const bf16_t* const (&arp)[MT], const bf16_t* const (&alp)[MT],
+                                        f32x4 (&acc)[MT][NT], const Hook& hook) {
   bf16x8 b[U][NT][2];
-  bf16x8 a[U][kMT][2], al[U][kMT][2];
+  bf16x8 a[U][MT][2], al[U][MT][2];
 #pragma unroll
   for (int u = 0; u < U; ++u) {
     const int kk = kb + u;
@@ -54,7 +54,7 @@ __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int
       }
     }
 #pragma unroll
-    for (int mt = 0; mt < kMT; ++mt)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int s = 0; s < 2; ++s) {
         a[u][mt][s] = __builtin_bit_cast(bf16x8, gload16(arp[mt] + kk * 64 + s * 32));
@@ -68,7 +68,7 @@ __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int
 #pragma unroll
     for (int s = 0; s < 2; ++s)
 #pragma unroll
-      for (int mt = 0; mt < kMT; ++mt)
+      for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int t = 0; t < NT; ++t) {
           acc[mt][t] = mfma16x16x32(a[u][mt][s], b[u][t][s], acc[mt][t]);
@@ -76,19 +76,22 @@ __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int
         }
 }
 
-// Small-row GEMM (batch-1 style): one block = 4 waves computing 64 rows x
+// Small-row GEMM (batch-1 style): one block = 4 waves computing 16*MT rows x
 // 32*NP columns; the block's K range is split between the 4 waves, whose
-// partial sums are added through LDS.  With g.split_out set, blockIdx.z
+// partial sums are added through LDS, and wave w < MT finishes row tile w.
+// Fewer row tiles per block mean fewer activation bytes per block; the row
+// blocks of one column tile share its weights in their XCD's L2.  With g.split_out set, blockIdx.z
 // selects a slice of K and the block writes its raw partial sums to
 // split_out[z] (fp32 [R][32*NPT]) instead of running the epilogue; the
 // consumer adds the slices in a fixed order.
-template <class Epi, bool FP8, bool SPLIT, int NP>
+template <class Epi, bool FP8, bool SPLIT, int NP, int MT>
 __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   constexpr int NT = 2 * NP;
-  __shared__ float red[4][kMT * NT * 4][kWave];
+  static_assert(MT >= 1 && MT <= 4, "at most one row tile per wave");
+  __shared__ float red[4][MT * NT * 4][kWave];
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int pt0 = blockIdx.x * NP;
-  const int m0 = blockIdx.y * 16 * kMT;
+  const int m0 = blockIdx.y * 16 * MT;
   const bf16_t* A = g.A_ind ? static_cast<const bf16_t*>(*g.A_ind) + g.a_off
                             : static_cast<const bf16_t*>(g.A);
   const int nkb = g.K / 64;
@@ -102,10 +105,10 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   // MFMA result depends on row i of A only, so such rows (and rows past a
   // request's prefix length, see the epilogue) are simply never used, which
   // keeps the loads free of branches the compiler could not count through.
-  const bf16_t* arp[kMT];
-  const bf16_t* alp[kMT];
+  const bf16_t* arp[MT];
+  const bf16_t* alp[MT];
 #pragma unroll
-  for (int mt = 0; mt < kMT; ++mt) {
+  for (int mt = 0; mt < MT; ++mt) {
     const int row = m0 + 16 * mt + arow;
     const int lr = row < g.R ? row : 0;
     arp[mt] = A + (int64_t)lr * g.lda + akg * 8;
@@ -114,8 +117,9 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
 
   // Epilogue inputs of the rows this wave finishes (wave w finishes row
   // tile w): they do not depend on the products, so the first trip requests
-  // them right behind its operands and they land together.  Rows past R read
-  // row 0 and columns past N the last pair tile; neither is stored.
+  // them right behind its operands and they land together.  Rows past R (and
+  // the rows of waves with no row tile) read row 0, columns past N the last
+  // pair tile; none of them is stored.
   const int c = lane % 16;
   typename Epi::ColPre cq[NP];
   typename Epi::Pre pre[NP][4];
@@ -130,15 +134,15 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
 #pragma unroll
       for (int v = 0; v < 4; ++v) {
         const int row = m0 + 16 * wave + 4 * akg + v;
-        pre[pp][v] = epi.pre(row < g.R ? row : 0, p, c);
+        pre[pp][v] = epi.pre(row < g.R && wave < MT ? row : 0, p, c);
       }
     }
   };
   auto no_loads = []() {};
 
-  f32x4 acc[kMT][NT];
+  f32x4 acc[MT][NT];
 #pragma unroll
-  for (int mt = 0; mt < kMT; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int t = 0; t < NT; ++t) acc[mt][t] = f32x4{0.f, 0.f, 0.f, 0.f};
 
@@ -146,24 +150,24 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   // first trip carries the epilogue loads
   int kb = kb0;
   if (kb + 4 <= kb1) {
-    b1_trip<4, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
-    for (kb += 4; kb + 4 <= kb1; kb += 4) b1_trip<4, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+    b1_trip<4, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+    for (kb += 4; kb + 4 <= kb1; kb += 4) b1_trip<4, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
     if (kb + 2 <= kb1) {
-      b1_trip<2, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+      b1_trip<2, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
       kb += 2;
     }
-    if (kb < kb1) b1_trip<1, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+    if (kb < kb1) b1_trip<1, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
   } else if (kb + 2 <= kb1) {
-    b1_trip<2, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
-    if (kb + 3 == kb1) b1_trip<1, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb + 2, arp, alp, acc, no_loads);
+    b1_trip<2, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+    if (kb + 3 == kb1) b1_trip<1, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb + 2, arp, alp, acc, no_loads);
   } else if (kb < kb1) {
-    b1_trip<1, FP8, SPLIT, NT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+    b1_trip<1, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
   } else {
     epi_loads();
   }
 
 #pragma unroll
-  for (int mt = 0; mt < kMT; ++mt)
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int t = 0; t < NT; ++t)
 #pragma unroll
@@ -171,6 +175,7 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   __syncthreads();
 
   // wave w finishes row tile w
+  if (wave >= MT) return;
   const int mt = wave;
   const int N = 32 * g.NPT;
   float* sp = g.split_out ? g.split_out + (int64_t)z * g.split_stride : nullptr;
@@ -812,6 +817,27 @@ __global__ __launch_bounds__(512) void merge_gemm_kernel(GemmArgs g, AttnParts a
   }
 }
 
+// Row tiles per small-row block without a K split: the fewest that keep the
+// grid within 384 blocks.  Fewer rows per block cut the activation bytes each
+// block re-reads for its columns (batch 1: QKV 7.9 -> 6.0 us with 16-row
+// blocks); past ~384 blocks the weight re-reads of the extra row blocks
+// cost more than that saves (gate/up keeps 64 rows).  Split-K GEMMs keep 64
+// rows: their blocks already read one K slice each.  PHYAI_SMALL_MT (tests,
+// read at enqueue time): a positive value forces the row tiles, a negative
+// one sets the block limit.
+int small_row_tiles(int R, int NPT) {
+  const char* f = getenv("PHYAI_SMALL_MT");
+  int lim = 384;
+  if (f) {
+    const int v = atoi(f);
+    if (v > 0) return v;
+    lim = -v;
+  }
+  for (int mt = 1; mt < kMT; mt *= 2)
+    if (NPT * ((R + 16 * mt - 1) / (16 * mt)) <= lim) return mt;
+  return kMT;
+}
+
 template <class Epi>
 void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
   if (g.kind == W_F32) {
@@ -844,18 +870,25 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
       else hipLaunchKernelGGL((gemm_tiled_kernel<Epi, false>), grid, dim3(256), 0, s, g, epi);
     }
   } else {
-    // 32 columns per block; K split over blockIdx.z only when the caller
-    // provides a partial-sum buffer (linear epilogues)
+    // 32 columns and 16 * MT rows per block; K split over blockIdx.z only
+    // when the caller provides a partial-sum buffer (linear epilogues)
     const int nz = g.split_out ? g.split_k : 1;
-    dim3 grid(g.NPT, (g.R + 16 * kMT - 1) / (16 * kMT), nz);
     const bool two = g.A_lo != nullptr;
-    if (g.kind == W_FP8) {
-      if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, true, 1>), grid, dim3(256), 0, s, g, epi);
-      else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, false, 1>), grid, dim3(256), 0, s, g, epi);
-    } else {
-      if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, true, 1>), grid, dim3(256), 0, s, g, epi);
-      else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, false, 1>), grid, dim3(256), 0, s, g, epi);
-    }
+    auto go = [&](auto mtag) {
+      constexpr int MT = decltype(mtag)::value;
+      const dim3 grid(g.NPT, (g.R + 16 * MT - 1) / (16 * MT), nz);
+      if (g.kind == W_FP8) {
+        if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, true, 1, MT>), grid, dim3(256), 0, s, g, epi);
+        else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, false, 1, MT>), grid, dim3(256), 0, s, g, epi);
+      } else {
+        if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, true, 1, MT>), grid, dim3(256), 0, s, g, epi);
+        else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, false, 1, MT>), grid, dim3(256), 0, s, g, epi);
+      }
+    };
+    const int mt = nz > 1 ? kMT : small_row_tiles(g.R, g.NPT);
+    if (mt == 1) go(std::integral_constant<int, 1>{});
+    else if (mt == 2) go(std::integral_constant<int, 2>{});
+    else go(std::integral_constant<int, kMT>{});
   }
 }
 

@@ -140,6 +140,28 @@ def test_full_size_batch64_fp8_sampled():
     compare(f"pi0_fp8_b64 requests {sample}", gpu[sample], ref, cfg)
 
 
+@pytest.mark.parametrize("variant,kw", [
+    ("pi0", {}),
+    ("pi0", dict(weight_dtype="fp8", batch=4)),
+    ("pi05", {}),
+])
+@pytest.mark.parametrize("mt", ["2", "4"])
+def test_small_row_gemm_row_blocks(variant, kw, mt):
+    """The small-row GEMMs with 32- and 64-row blocks forced (the default
+    picks 16-row blocks for these shapes): rows 153 and 204 leave a partial
+    last block either way."""
+    cfg = small_cfg(variant, **kw)
+    print(f"[case] small-row blocks {mt} x 16 rows {variant} {kw}", flush=True)
+    case = wl.make_case(cfg, seed=7)
+    os.environ["PHYAI_SMALL_MT"] = mt
+    try:
+        ex = _expert(cfg, case)
+        gpu = run_gpu(ex, case)
+    finally:
+        del os.environ["PHYAI_SMALL_MT"]
+    compare(f"small-row blocks {mt} {variant} {kw}", gpu, _oracle(cfg, case), cfg)
+
+
 @pytest.mark.parametrize("wdt", ["bf16", "fp8"])
 @pytest.mark.parametrize("tile", ["ring", "deep", "strided"])
 def test_many_row_gemm_tiles(tile, wdt):
