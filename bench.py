@@ -45,12 +45,12 @@ _GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/ke
              "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
 _MERGE_SRC = _GEMM_SRC + ("paper_2608_03682_amd/csrc/attention.hip",)
 MEASURED_TRAFFIC = {
-    ("pi0_bf16_b1", "attn"): {"bytes": 6658944, "sources": _ATTN_SRC, "sha256": "4b427f98572ff8c5"},
-    ("pi0_bf16_b1", "qkv"): {"bytes": 6594056, "sources": _GEMM_SRC, "sha256": "028e954043599b7f"},
-    ("pi0_bf16_b1", "oproj"): {"bytes": 9306117, "sources": _MERGE_SRC, "sha256": "c6ba183bb3719e3c"},
-    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18185233, "sources": _GEMM_SRC, "sha256": "028e954043599b7f"},
-    ("pi0_bf16_b1", "mlp_down"): {"bytes": 13741064, "sources": _GEMM_SRC, "sha256": "028e954043599b7f"},
-    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90147101, "sources": _GEMM_SRC, "sha256": "028e954043599b7f"},
+    ("pi0_bf16_b1", "attn"): {"bytes": 6658952, "sources": _ATTN_SRC, "sha256": "4b427f98572ff8c5"},
+    ("pi0_bf16_b1", "qkv"): {"bytes": 6559240, "sources": _GEMM_SRC, "sha256": "0fe268f34b577e1c"},
+    ("pi0_bf16_b1", "oproj"): {"bytes": 9306122, "sources": _MERGE_SRC, "sha256": "2794d93ed59980c9"},
+    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18188304, "sources": _GEMM_SRC, "sha256": "0fe268f34b577e1c"},
+    ("pi0_bf16_b1", "mlp_down"): {"bytes": 13732873, "sources": _GEMM_SRC, "sha256": "0fe268f34b577e1c"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90516140, "sources": _GEMM_SRC, "sha256": "0fe268f34b577e1c"},
 }
 
 
