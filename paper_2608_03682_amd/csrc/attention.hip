@@ -21,13 +21,16 @@
 // as 16x16, which is what a single wave per SIMD needs to keep the matrix
 // core busy.
 //
-// Block: 4 waves x 32 query rows; 64-key tiles double-buffered in LDS and
-// filled by direct global->LDS loads, the next tile in flight while the
-// current one is computed.
+// Block: 4 waves x 32 query rows (2 waves when the grid is small, see
+// attention_rows_per_block); 64-key tiles double-buffered in LDS and filled
+// by direct global->LDS loads, the next tile in flight while the current one
+// is computed.
 // With n_split > 1 the key range is split over blocks, whose partials a
 // second kernel merges in a fixed order.
 #include "kernels.hpp"
 
+#include <algorithm>
+#include <cstdlib>
 #include <type_traits>
 
 namespace phyai {
@@ -35,7 +38,6 @@ namespace phyai {
 namespace {
 
 constexpr int kKT = 64;          // keys per tile
-constexpr int kRows = 128;       // query rows per block
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -244,11 +246,12 @@ __device__ __forceinline__ void attn_tile(const bf16_t* TK, const bf16_t* TVt, c
   lds_mfma_pipeline<D / 8, PHYAI_ATTN_PD>();
 }
 
-template <int D>
-__global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
+template <int D, int NWB>
+__global__ __launch_bounds__(64 * NWB) void attn_mfma_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) AttnLds<D> sm;
+  constexpr int kRows = 32 * NWB;             // query rows per block
   constexpr int CPR = D / 8;                  // 16-byte chunks per K row
-  constexpr int NLD = kKT * D / 8 / 256;      // loads per thread per operand per tile
+  constexpr int NLD = kKT * D / 8 / (64 * NWB);   // loads per thread per operand per tile
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int lr = lane % 32, hl = lane / 32;
   const int G = a.nq / a.nkv;
@@ -292,13 +295,13 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   const bf16_t* Vb = static_cast<const bf16_t*>(a.Vt) + (int64_t)grp * a.ldk * D;
 
   // Direct global->LDS loads of one tile (the key range always holds whole,
-  // finite 64-key tiles).  Wave w's i-th load fills 1 KiB block 4i + w; the
-  // per-thread source offsets (elements) do not depend on the tile.
+  // finite 64-key tiles).  Wave w's i-th load fills 1 KiB block NWB i + w;
+  // the per-thread source offsets (elements) do not depend on the tile.
   const int wv = __builtin_amdgcn_readfirstlane(wave);
   int koff[NLD], voff[NLD];
 #pragma unroll
   for (int i = 0; i < NLD; ++i) {
-    const int pos = (4 * i + wave) * 64 + lane;
+    const int pos = (NWB * i + wave) * 64 + lane;
     const int r = pos / CPR, pc = pos % CPR;
     koff[i] = r * D + 8 * (pc ^ kswz<D>(r));
     const int d = pos / 8, vc = pos % 8;
@@ -309,10 +312,10 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
     const bf16_t* vbase = Vb + kt0;
 #pragma unroll
     for (int i = 0; i < NLD; ++i)
-      lds_dma16(kbase + koff[i], (lds_void*)(sm.K[buf] + (4 * i + wv) * 512));
+      lds_dma16(kbase + koff[i], (lds_void*)(sm.K[buf] + (NWB * i + wv) * 512));
 #pragma unroll
     for (int i = 0; i < NLD; ++i)
-      lds_dma16(vbase + voff[i], (lds_void*)(sm.Vt[buf] + (4 * i + wv) * 512));
+      lds_dma16(vbase + voff[i], (lds_void*)(sm.Vt[buf] + (NWB * i + wv) * 512));
   };
 
   // first tile in flight while the Q fragments land.  The first tile's
@@ -376,7 +379,7 @@ __global__ __launch_bounds__(256) void attn_mfma_kernel(AttnArgs a) {
   // covers 64 / CPR complete rows.
   const float inv = l_run > 0.f ? 1.f / l_run : 0.f;
   bf16_t* stage = reinterpret_cast<bf16_t*>(&sm) + wave * 32 * D;
-  static_assert(sizeof(AttnLds<D>) >= 4 * 32 * D * sizeof(bf16_t), "staging needs 4 waves x 32 rows");
+  static_assert(sizeof(AttnLds<D>) >= NWB * 32 * D * sizeof(bf16_t), "staging needs NWB waves x 32 rows");
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
@@ -426,6 +429,7 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
   const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
   const int G = a.nq / a.nkv;
   const int rows = a.M * G;
+  const int kRows = a.rows_per_tile;
   const int ntiles = (rows + kRows - 1) / kRows;
   const int grp = blockIdx.y;
   const int r = blockIdx.x * 4 + wave;
@@ -590,19 +594,37 @@ __global__ __launch_bounds__(256) void prefix_relayout_kernel(RelayoutArgs r) {
 
 }  // namespace
 
-// Partials: bf16 O [tiles][split][kRows][D] followed (at part_ml_off floats)
-// by float (m, l) [tiles][split][kRows][2].
+// Query rows per block: 128 (4 waves), or 64 (2 waves) when the 128-row
+// blocks of all requests number fewer than 64 (batch 1), so that with the
+// key splits the kernel spreads over more CUs and each block loads half the
+// queries and stores half the partials.  PHYAI_ATTN_ROWS=64|128 (tests, read
+// at enqueue time) forces it.
+int attention_rows_per_block(int B, int rows, int nkv) {
+  const char* f = getenv("PHYAI_ATTN_ROWS");
+  if (f) return atoi(f) == 64 ? 64 : 128;
+  return (int64_t)((rows + 127) / 128) * B * nkv < 64 ? 64 : 128;
+}
+
+// Partials: bf16 O [tiles][split][rows_per_block][D] followed (at part_ml_off
+// floats) by float (m, l) [tiles][split][rows_per_block][2].  The buffer is
+// sized for the larger of the 64- and 128-row layouts, so that forcing either
+// fits.
 int64_t attention_partial_ml_off(int B, int M, int nq, int nkv, int D, int n_split) {
   const int rows = M * (nq / nkv);
-  const int64_t tiles = (int64_t)B * nkv * ((rows + kRows - 1) / kRows);
-  return (tiles * n_split * kRows * D + 1) / 2;
+  const int rpt = attention_rows_per_block(B, rows, nkv);
+  const int64_t tiles = (int64_t)B * nkv * ((rows + rpt - 1) / rpt);
+  return (tiles * n_split * rpt * D + 1) / 2;
 }
 
 int64_t attention_partial_floats(int B, int M, int nq, int nkv, int D, int n_split) {
   if (n_split <= 1) return 0;
   const int rows = M * (nq / nkv);
-  const int64_t tiles = (int64_t)B * nkv * ((rows + kRows - 1) / kRows);
-  return attention_partial_ml_off(B, M, nq, nkv, D, n_split) + tiles * n_split * kRows * 2;
+  int64_t most = 0;
+  for (int rpt = 64; rpt <= 128; rpt += 64) {
+    const int64_t tiles = (int64_t)B * nkv * ((rows + rpt - 1) / rpt);
+    most = std::max(most, (tiles * n_split * rpt * D + 1) / 2 + tiles * n_split * rpt * 2);
+  }
+  return most;
 }
 
 AttnParts attention_parts(const AttnArgs& a) {
@@ -610,9 +632,9 @@ AttnParts attention_parts(const AttnArgs& a) {
   p.o = reinterpret_cast<const bf16_t*>(a.part);
   p.ml = a.part + attention_partial_ml_off(a.B, a.M, a.nq, a.nkv, a.D, a.n_split);
   p.n_split = a.n_split;
-  p.rows_per_tile = kRows;
   p.G = a.nq / a.nkv;
-  p.ntiles = (a.M * p.G + kRows - 1) / kRows;
+  p.rows_per_tile = attention_rows_per_block(a.B, a.M * p.G, a.nkv);
+  p.ntiles = (a.M * p.G + p.rows_per_tile - 1) / p.rows_per_tile;
   p.M = a.M;
   p.nkv = a.nkv;
   p.D = a.D;
@@ -622,13 +644,19 @@ AttnParts attention_parts(const AttnArgs& a) {
 void attention_bf16(const AttnArgs& a0, hipStream_t s) {
   AttnArgs a = a0;
   const int rows = a.M * (a.nq / a.nkv);
-  const int ntiles = (rows + kRows - 1) / kRows;
+  a.rows_per_tile = attention_rows_per_block(a.B, rows, a.nkv);
+  const int ntiles = (rows + a.rows_per_tile - 1) / a.rows_per_tile;
   const int ngroups = a.B * a.nkv * a.n_split;
   a.part_ml_off = attention_partial_ml_off(a.B, a.M, a.nq, a.nkv, a.D, a.n_split);
   dim3 grid(8 * ntiles * ((ngroups + 7) / 8));
-  if (a.D == 256) hipLaunchKernelGGL(attn_mfma_kernel<256>, grid, dim3(256), 0, s, a);
-  else if (a.D == 128) hipLaunchKernelGGL(attn_mfma_kernel<128>, grid, dim3(256), 0, s, a);
-  else if (a.D == 64) hipLaunchKernelGGL(attn_mfma_kernel<64>, grid, dim3(256), 0, s, a);
+  auto go = [&](auto dtag) {
+    constexpr int DD = decltype(dtag)::value;
+    if (a.rows_per_tile == 64) hipLaunchKernelGGL((attn_mfma_kernel<DD, 2>), grid, dim3(128), 0, s, a);
+    else hipLaunchKernelGGL((attn_mfma_kernel<DD, 4>), grid, dim3(256), 0, s, a);
+  };
+  if (a.D == 256) go(std::integral_constant<int, 256>{});
+  else if (a.D == 128) go(std::integral_constant<int, 128>{});
+  else if (a.D == 64) go(std::integral_constant<int, 64>{});
   if (a.n_split > 1 && !a.defer_merge) {
     dim3 g2((rows + 3) / 4, a.B * a.nkv);
     auto comb = [&](auto dtag) {

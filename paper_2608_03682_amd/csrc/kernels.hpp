@@ -415,6 +415,7 @@ struct AttnArgs {
   void* out; int ldo;
   float* part;              // split partials (n_split > 1)
   int64_t part_ml_off;      // set by the launcher
+  int rows_per_tile;        // query rows per block, set by the launcher
   int n_split;
   int defer_merge;          // n_split > 1: leave the partials for gemm_merge_resid
   const CallDesc* desc;
@@ -425,6 +426,7 @@ struct AttnArgs {
 void attention_bf16(const AttnArgs&, hipStream_t);
 void attention_f32(const AttnArgs&, hipStream_t);
 int64_t attention_partial_floats(int B, int M, int nq, int nkv, int D, int n_split);
+int attention_rows_per_block(int B, int rows, int nkv);
 
 // Key-split partials of one bf16 attention launch: O rows [tile][split][rows_per_tile][D]
 // (bf16, each split normalised by its own softmax sum) and (m, l) [tile][split][rows_per_tile]

@@ -317,7 +317,8 @@ template <typename T> EpiStore<T> store_epi(T* out, int ldo, const float* bias, 
 
 // split of the keys across blocks so that small batches still fill the chip
 int attn_splits(int B, int rows, int nkv, int keys) {
-  const int base = ((rows + 127) / 128) * B * nkv;     // blocks without a split
+  const int rpb = attention_rows_per_block(B, rows, nkv);
+  const int base = ((rows + rpb - 1) / rpb) * B * nkv;   // blocks without a split
   int s = (256 + base - 1) / base;
   const int cap = (keys + 63) / 64;                     // at least one 64-key tile per split
   if (s > cap) s = cap;

@@ -142,6 +142,27 @@ def test_full_size_batch64_fp8_sampled():
 
 @pytest.mark.parametrize("variant,kw", [
     ("pi0", {}),
+    ("pi0", dict(batch=7)),
+    ("dit", {}),
+])
+def test_attention_128_row_blocks(variant, kw):
+    """Attention with four-wave, 128-row blocks and key splits (small batches
+    default to two-wave, 64-row blocks; the rollout batch uses 128-row blocks
+    without splits)."""
+    cfg = small_cfg(variant, **kw)
+    print(f"[case] attention 128-row blocks {variant} {kw}", flush=True)
+    case = wl.make_case(cfg, seed=8)
+    os.environ["PHYAI_ATTN_ROWS"] = "128"
+    try:
+        ex = _expert(cfg, case)
+        gpu = run_gpu(ex, case)
+    finally:
+        del os.environ["PHYAI_ATTN_ROWS"]
+    compare(f"attention 128-row blocks {variant} {kw}", gpu, _oracle(cfg, case), cfg)
+
+
+@pytest.mark.parametrize("variant,kw", [
+    ("pi0", {}),
     ("pi0", dict(weight_dtype="fp8", batch=4)),
     ("pi05", {}),
 ])
