@@ -137,15 +137,22 @@ __device__ __forceinline__ float apply_act(int act, float v) {
 
 // Activation storage: bf16 on the MFMA path, f32 on the fp32 path.
 template <typename T> struct ActIO;
+// store4: four consecutive values in one store (p aligned to 4 elements)
 template <> struct ActIO<float> {
   static __device__ __forceinline__ float round(float v) { return v; }
   static __device__ __forceinline__ float load(const float* p) { return *p; }
   static __device__ __forceinline__ void store(float* p, float v) { *p = v; }
+  static __device__ __forceinline__ void store4(float* p, const float (&v)[4]) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  }
 };
 template <> struct ActIO<bf16_t> {
   static __device__ __forceinline__ float round(float v) { return bf16_to_f32(f32_to_bf16(v)); }
   static __device__ __forceinline__ float load(const bf16_t* p) { return bf16_to_f32(*p); }
   static __device__ __forceinline__ void store(bf16_t* p, float v) { *p = f32_to_bf16(v); }
+  static __device__ __forceinline__ void store4(bf16_t* p, const float (&v)[4]) {
+    *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+  }
 };
 
 }  // namespace phyai

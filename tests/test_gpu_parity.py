@@ -46,7 +46,9 @@ def test_fp8_decode_all_codes_bit_exact():
     ("pi0", dict(weight_dtype="fp8", batch=7)),
     ("pi0", dict(batch=21)),                        # 1071 rows, 1050 action rows: the row-blocked
                                                     # embedding and readout, each with a partial last block
+    ("pi0", dict(d_model=1024, batch=2)),           # width 1024: the four-column norm kernel
     ("pi05", {}),
+    ("pi05", dict(d_model=1024)),                   # the same with adaRMS shift and compensated output
     ("dit", {}),
     ("pi0", dict(weight_dtype="f32", kv_dtype="f32", state_token=False, rope=False)),
 ])
