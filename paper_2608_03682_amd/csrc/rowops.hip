@@ -108,31 +108,25 @@ __global__ __launch_bounds__(256) void norm_rows_kernel(float* __restrict__ h, O
 // row (h, each pending slice, the factors) is one 16-byte request per thread
 // and the normalised values leave in one store, where the scalar layout above
 // needs four of each.
-template <typename OutT>
-__global__ __launch_bounds__(256) void norm_rows_v4_kernel(float* __restrict__ h, OutT* __restrict__ n,
-                                                           OutT* __restrict__ n_lo, int d, float eps, int mode,
-                                                           const float* __restrict__ mul,
-                                                           const float* __restrict__ shift, PendingResid pend) {
-  __shared__ float scratch[4];
+// Columns c .. c+3 of row `row` (c a multiple of 4) with the pending residual
+// folded in and written back, as load_row_with_pending does for one column:
+// every request (the row, each slice, bias, gate) is one 16-byte load.
+__device__ __forceinline__ void load_row4_with_pending(float* hr, int64_t row, int d, int c, const PendingResid& pd,
+                                                       float (&v)[4]) {
   constexpr int kMaxSplit = 8;
-  const int row = blockIdx.x;
-  const int c = 4 * threadIdx.x;
-  float* hr = h + (int64_t)row * d;
-  const int np = pend.n;
-  const float4 mv = *reinterpret_cast<const float4*>(mul + c);
-  const float4 sv = shift ? *reinterpret_cast<const float4*>(shift + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  const int np = pd.n;
   const float4 hv = *reinterpret_cast<const float4*>(hr + c);
   float4 sl[kMaxSplit], bs = make_float4(0.f, 0.f, 0.f, 0.f), gt = make_float4(1.f, 1.f, 1.f, 1.f);
   if (np > 0) {
 #pragma unroll
     for (int sp = 0; sp < kMaxSplit; ++sp) {
       const int ss = sp < np ? sp : np - 1;
-      sl[sp] = *reinterpret_cast<const float4*>(pend.part + ss * pend.stride + (int64_t)row * d + c);
+      sl[sp] = *reinterpret_cast<const float4*>(pd.part + ss * pd.stride + row * d + c);
     }
-    if (pend.bias) bs = *reinterpret_cast<const float4*>(pend.bias + c);
-    if (pend.gate) gt = *reinterpret_cast<const float4*>(pend.gate + c);
+    if (pd.bias) bs = *reinterpret_cast<const float4*>(pd.bias + c);
+    if (pd.gate) gt = *reinterpret_cast<const float4*>(pd.gate + c);
   }
-  float v[4] = {hv.x, hv.y, hv.z, hv.w};
+  v[0] = hv.x; v[1] = hv.y; v[2] = hv.z; v[3] = hv.w;
   if (np > 0) {
     const float b4[4] = {bs.x, bs.y, bs.z, bs.w}, g4[4] = {gt.x, gt.y, gt.z, gt.w};
 #pragma unroll
@@ -147,6 +141,20 @@ __global__ __launch_bounds__(256) void norm_rows_v4_kernel(float* __restrict__ h
     }
     *reinterpret_cast<float4*>(hr + c) = make_float4(v[0], v[1], v[2], v[3]);
   }
+}
+
+template <typename OutT>
+__global__ __launch_bounds__(256) void norm_rows_v4_kernel(float* __restrict__ h, OutT* __restrict__ n,
+                                                           OutT* __restrict__ n_lo, int d, float eps, int mode,
+                                                           const float* __restrict__ mul,
+                                                           const float* __restrict__ shift, PendingResid pend) {
+  __shared__ float scratch[4];
+  const int row = blockIdx.x;
+  const int c = 4 * threadIdx.x;
+  const float4 mv = *reinterpret_cast<const float4*>(mul + c);
+  const float4 sv = shift ? *reinterpret_cast<const float4*>(shift + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+  float v[4];
+  load_row4_with_pending(h + (int64_t)row * d, row, d, c, pend, v);
   float mu = 0.f;
   if (mode == NORM_LN) mu = block_sum<256>(v[0] + v[1] + v[2] + v[3], scratch) / d;
   float ss = 0.f;
@@ -522,11 +530,23 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
     for (int i = 0; i < NG; ++i)
       w4[q][i] = *reinterpret_cast<const float4*>(r.out_w + (int64_t)a * d + 4 * lane + 256 * i);
   }
+  // one row of width 1024: thread t holds columns 4t .. 4t+3 (16-byte
+  // requests for the row and each pending slice); otherwise columns
+  // t + 256 i
+  constexpr bool V4 = RB == 1 && NG == 4;
   float mv[NG], sv[NG];
+  if constexpr (V4) {
+    const float4 m = *reinterpret_cast<const float4*>(r.mul + 4 * threadIdx.x);
+    const float4 q = r.shift ? *reinterpret_cast<const float4*>(r.shift + 4 * threadIdx.x)
+                             : make_float4(0.f, 0.f, 0.f, 0.f);
+    mv[0] = m.x; mv[1] = m.y; mv[2] = m.z; mv[3] = m.w;
+    sv[0] = q.x; sv[1] = q.y; sv[2] = q.z; sv[3] = q.w;
+  } else {
 #pragma unroll
-  for (int i = 0; i < NG; ++i) {
-    mv[i] = r.mul[threadIdx.x + 256 * i];
-    sv[i] = r.shift ? r.shift[threadIdx.x + 256 * i] : 0.f;
+    for (int i = 0; i < NG; ++i) {
+      mv[i] = r.mul[threadIdx.x + 256 * i];
+      sv[i] = r.shift ? r.shift[threadIdx.x + 256 * i] : 0.f;
+    }
   }
   const int ur = threadIdx.x / r.A, ua = threadIdx.x % r.A;
   const bool upd = threadIdx.x < RB * r.A && ar0 + ur < nrows;
@@ -534,7 +554,11 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
   const float xv = r.x[xi], bv = r.out_b[upd ? ua : 0], dtv = r.dt[0];
 
   float v[RB][NG];
-  if constexpr (RB == 1) {
+  if constexpr (V4) {
+    const int b = ar0 / r.H, j = ar0 % r.H;
+    const int64_t hrow = (int64_t)b * r.M + r.off + j;
+    load_row4_with_pending(r.h + hrow * d, hrow, d, 4 * threadIdx.x, r.pend, v[0]);
+  } else if constexpr (RB == 1) {
     const int b = ar0 / r.H, j = ar0 % r.H;
     const int64_t hrow = (int64_t)b * r.M + r.off + j;
     float vv[kMaxPer];
@@ -585,7 +609,7 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
     for (int i = 0; i < NG; ++i) {
       float t = (v[rr][i] - mu[rr]) * rs * (1.f + mv[i]);
       if (r.shift) t += sv[i];
-      nrm[rr * d + threadIdx.x + 256 * i] = t;
+      nrm[rr * d + (V4 ? 4 * threadIdx.x + i : threadIdx.x + 256 * i)] = t;
     }
   }
   __syncthreads();
