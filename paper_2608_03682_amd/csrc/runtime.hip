@@ -316,14 +316,21 @@ template <typename T> EpiStore<T> store_epi(T* out, int ldo, const float* bias, 
 }
 
 // split of the keys across blocks so that small batches still fill the chip
-int attn_splits(int B, int rows, int nkv, int keys) {
-  const int rpb = attention_rows_per_block(B, rows, nkv);
+int attn_splits_for(int B, int rows, int nkv, int keys, int rpb) {
   const int base = ((rows + rpb - 1) / rpb) * B * nkv;   // blocks without a split
   int s = (256 + base - 1) / base;
   const int cap = (keys + 63) / 64;                     // at least one 64-key tile per split
   if (s > cap) s = cap;
   if (s > 16) s = 16;                                   // the merge kernel takes up to 16
   return s < 1 ? 1 : s;
+}
+int attn_splits(int B, int rows, int nkv, int keys) {
+  return attn_splits_for(B, rows, nkv, keys, attention_rows_per_block(B, rows, nkv));
+}
+// the most splits either block height can ask for (buffers are sized with it,
+// so that forcing the other height at a later call still fits)
+int attn_splits_max(int B, int rows, int nkv, int keys) {
+  return std::max(attn_splits_for(B, rows, nkv, keys, 64), attn_splits_for(B, rows, nkv, keys, 128));
 }
 
 // key splits of block l's attention at batch B (DiT: even blocks attend to
@@ -829,8 +836,8 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     const int keys_main = c.variant == PHYAI_VARIANT_DIT ? e->M : e->P + e->M;
     for (int B = 1; B <= e->Bmax; ++B) {
       const int rows = e->M * (e->nq / e->nkv);
-      const int s1 = attn_splits(B, rows, e->nkv, keys_main);
-      const int s2 = attn_splits(B, rows, e->nkv, e->P);
+      const int s1 = attn_splits_max(B, rows, e->nkv, keys_main);
+      const int s2 = attn_splits_max(B, rows, e->nkv, e->P);
       int64_t need = attention_partial_floats(B, e->M, e->nq, e->nkv, D, s1);
       if (c.variant == PHYAI_VARIANT_DIT)
         need = std::max(need, attention_partial_floats(B, e->M, e->nq, e->nkv, D, s2));

@@ -150,13 +150,14 @@ def test_full_size_batch64_fp8_sampled():
 def test_attention_128_row_blocks(variant, kw):
     """Attention with four-wave, 128-row blocks and key splits (small batches
     default to two-wave, 64-row blocks; the rollout batch uses 128-row blocks
-    without splits)."""
+    without splits).  The switch is set after the expert is loaded, so its
+    buffers were sized without it."""
     cfg = small_cfg(variant, **kw)
     print(f"[case] attention 128-row blocks {variant} {kw}", flush=True)
     case = wl.make_case(cfg, seed=8)
+    ex = _expert(cfg, case)
     os.environ["PHYAI_ATTN_ROWS"] = "128"
     try:
-        ex = _expert(cfg, case)
         gpu = run_gpu(ex, case)
     finally:
         del os.environ["PHYAI_ATTN_ROWS"]
