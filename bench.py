@@ -45,12 +45,12 @@ _GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/ke
              "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
 _MERGE_SRC = _GEMM_SRC + ("paper_2608_03682_amd/csrc/attention.hip",)
 MEASURED_TRAFFIC = {
-    ("pi0_bf16_b1", "attn"): {"bytes": 6231938, "sources": _ATTN_SRC, "sha256": "9af2bc65cddf399d"},
-    ("pi0_bf16_b1", "qkv"): {"bytes": 6559240, "sources": _GEMM_SRC, "sha256": "a190c9e3b7efdd0a"},
-    ("pi0_bf16_b1", "oproj"): {"bytes": 9306121, "sources": _MERGE_SRC, "sha256": "0775a26e26ab22a5"},
-    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18188304, "sources": _GEMM_SRC, "sha256": "a190c9e3b7efdd0a"},
-    ("pi0_bf16_b1", "mlp_down"): {"bytes": 13732873, "sources": _GEMM_SRC, "sha256": "a190c9e3b7efdd0a"},
-    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90797934, "sources": _GEMM_SRC, "sha256": "a190c9e3b7efdd0a"},
+    ("pi0_bf16_b1", "attn"): {"bytes": 6231938, "sources": _ATTN_SRC, "sha256": "e685413a2b9f7003"},
+    ("pi0_bf16_b1", "qkv"): {"bytes": 6559240, "sources": _GEMM_SRC, "sha256": "4909f222b312dd1b"},
+    ("pi0_bf16_b1", "oproj"): {"bytes": 9306118, "sources": _MERGE_SRC, "sha256": "c9f58b0cfed3d2f0"},
+    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18188304, "sources": _GEMM_SRC, "sha256": "4909f222b312dd1b"},
+    ("pi0_bf16_b1", "mlp_down"): {"bytes": 13732872, "sources": _GEMM_SRC, "sha256": "4909f222b312dd1b"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90684867, "sources": _GEMM_SRC, "sha256": "4909f222b312dd1b"},
 }
 
 
