@@ -399,6 +399,29 @@ __device__ __forceinline__ void tile_epilogue(const GemmArgs& g, const Epi& epi,
   }
 }
 
+// The generic epilogue with the row inputs and column scales requested
+// before the k-loop (four-stage ring); rows past R were loaded from row R-1
+// and are not stored.
+template <class Epi, int NT>
+__device__ __forceinline__ void tile_epilogue_early(const GemmArgs& g, const Epi& epi, const f32x4 (&acc)[4][NT],
+                                                    int r0, int p0, int lc, int lg,
+                                                    const typename Epi::Pre (&pre)[NT / 2][4][4],
+                                                    const float (&sc)[NT / 2][2]) {
+#pragma unroll
+  for (int pp = 0; pp < NT / 2; ++pp) {
+    const typename Epi::ColPre cq = epi.colpre(p0 + pp, lc);
+#pragma unroll
+    for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = r0 + 16 * mt + 4 * lg + v;
+        if (row < g.R)
+          epi.apply(row, p0 + pp, lc, cq, pre[pp][mt][v], acc[mt][2 * pp][v] * sc[pp][0],
+                    acc[mt][2 * pp + 1][v] * sc[pp][1]);
+      }
+  }
+}
+
 template <bool FP8>
 struct TiledSmem {
   bf16_t A[128 * 64];
@@ -584,6 +607,29 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
       dma16(bsrc[i] + (int64_t)kb * 2 * C::FB, (lds_void_t*)(base + (C::A_KB + NW * i + wv) * 1024));
   };
 
+  // With one tile per CU (four-stage ring) nothing hides the round trip of
+  // the epilogue's row inputs (the residual rows) after the last k-block, so
+  // they and the fp8 column scales are requested here, before the first
+  // tile load: as the wave's oldest loads, every in-order wait of the loop
+  // covers them.  Unconditional (rows past R read row R-1), so that no
+  // branch makes the compiler wait for them early.
+  constexpr bool kEarly = NS == 4 && !Epi::kWaveTile;
+  typename Epi::Pre epre[NT / 2][4][4];
+  float esc[NT / 2][2];
+  if constexpr (kEarly) {
+#pragma unroll
+    for (int pp = 0; pp < NT / 2; ++pp) {
+      const int p = pt0 + (NT / 2) * wn + pp;
+      esc[pp][0] = FP8 ? g.scale[32 * p + lc] : 1.f;
+      esc[pp][1] = FP8 ? g.scale[32 * p + 16 + lc] : 1.f;
+#pragma unroll
+      for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+          epre[pp][mt][v] = epi.pre(min(m0 + 64 * wm + 16 * mt + 4 * lg + v, g.R - 1), p, lc);
+    }
+  }
+
   f32x4 acc[4][NT];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
@@ -655,8 +701,10 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
     static_assert(NW * Epi::kVStage * 2 <= NS * C::STAGE, "V staging fits the ring");
     bare_barrier();
     epi.wave_tile(g, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg, reinterpret_cast<bf16_t*>(ring) + wave * Epi::kVStage);
+  } else if constexpr (kEarly) {
+    tile_epilogue_early<Epi, NT>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg, epre, esc);
   } else {
-    tile_epilogue<NS == 2 ? 0 : 4>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg);
+    tile_epilogue<0>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg);
   }
 }
 
