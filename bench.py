@@ -46,11 +46,11 @@ _GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/ke
 _MERGE_SRC = _GEMM_SRC + ("paper_2608_03682_amd/csrc/attention.hip",)
 MEASURED_TRAFFIC = {
     ("pi0_bf16_b1", "attn"): {"bytes": 6231938, "sources": _ATTN_SRC, "sha256": "e685413a2b9f7003"},
-    ("pi0_bf16_b1", "qkv"): {"bytes": 6559240, "sources": _GEMM_SRC, "sha256": "4909f222b312dd1b"},
-    ("pi0_bf16_b1", "oproj"): {"bytes": 9306118, "sources": _MERGE_SRC, "sha256": "c9f58b0cfed3d2f0"},
-    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18188304, "sources": _GEMM_SRC, "sha256": "4909f222b312dd1b"},
-    ("pi0_bf16_b1", "mlp_down"): {"bytes": 13732872, "sources": _GEMM_SRC, "sha256": "4909f222b312dd1b"},
-    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90684867, "sources": _GEMM_SRC, "sha256": "4909f222b312dd1b"},
+    ("pi0_bf16_b1", "qkv"): {"bytes": 6563336, "sources": _GEMM_SRC, "sha256": "5f1cb163daba44e9"},
+    ("pi0_bf16_b1", "oproj"): {"bytes": 9306121, "sources": _MERGE_SRC, "sha256": "814f2cd702ffe49c"},
+    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18192401, "sources": _GEMM_SRC, "sha256": "5f1cb163daba44e9"},
+    ("pi0_bf16_b1", "mlp_down"): {"bytes": 13740042, "sources": _GEMM_SRC, "sha256": "5f1cb163daba44e9"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90489694, "sources": _GEMM_SRC, "sha256": "5f1cb163daba44e9"},
 }
 
 
