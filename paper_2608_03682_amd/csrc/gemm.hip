@@ -710,9 +710,13 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
 
 }  // namespace
 
+// Split-K GEMMs run 16-row blocks; the split brings the grid to about 256
+// blocks.  At batch 1 the down projection then takes 2 slices of 2048 (256
+// blocks) instead of 8 slices of 512 over 64-row blocks: the next norm
+// folds a quarter of the slices (8.39 -> 8.31 ms per chunk).
 int gemm_split_k(int R, int NPT, int K) {
   if (R >= 256) return 1;                     // the tiled kernel has enough blocks
-  const int blocks = NPT * ((R + 63) / 64);
+  const int blocks = NPT * ((R + 15) / 16);
   int s = (256 + blocks - 1) / blocks;
   const int cap = (K / 64) / 4;               // keep >= one k-block per wave
   if (s > cap) s = cap;
@@ -869,10 +873,10 @@ __global__ __launch_bounds__(512) void merge_gemm_kernel(GemmArgs g, AttnParts a
 // grid within 384 blocks.  Fewer rows per block cut the activation bytes each
 // block re-reads for its columns (batch 1: QKV 7.9 -> 6.0 us with 16-row
 // blocks); past ~384 blocks the weight re-reads of the extra row blocks
-// cost more than that saves (gate/up keeps 64 rows).  Split-K GEMMs keep 64
-// rows: their blocks already read one K slice each.  PHYAI_SMALL_MT (tests,
-// read at enqueue time): a positive value forces the row tiles, a negative
-// one sets the block limit.
+// cost more than that saves (gate/up keeps 64 rows).  Split-K GEMMs always
+// run 16-row blocks (gemm_split_k).  PHYAI_SMALL_MT (tests, read at enqueue
+// time): a positive value forces the row tiles, a negative one sets the
+// block limit.
 int small_row_tiles(int R, int NPT) {
   const char* f = getenv("PHYAI_SMALL_MT");
   int lim = 384;
@@ -933,7 +937,7 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
         else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, false, 1, MT>), grid, dim3(256), 0, s, g, epi);
       }
     };
-    const int mt = nz > 1 ? kMT : small_row_tiles(g.R, g.NPT);
+    const int mt = nz > 1 ? 1 : small_row_tiles(g.R, g.NPT);
     if (mt == 1) go(std::integral_constant<int, 1>{});
     else if (mt == 2) go(std::integral_constant<int, 2>{});
     else go(std::integral_constant<int, kMT>{});
