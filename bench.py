@@ -45,12 +45,12 @@ _GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/ke
              "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
 _MERGE_SRC = _GEMM_SRC + ("paper_2608_03682_amd/csrc/attention.hip",)
 MEASURED_TRAFFIC = {
-    ("pi0_bf16_b1", "attn"): {"bytes": 6231938, "sources": _ATTN_SRC, "sha256": "e685413a2b9f7003"},
-    ("pi0_bf16_b1", "qkv"): {"bytes": 6563336, "sources": _GEMM_SRC, "sha256": "5f1cb163daba44e9"},
-    ("pi0_bf16_b1", "oproj"): {"bytes": 9306121, "sources": _MERGE_SRC, "sha256": "814f2cd702ffe49c"},
-    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18192401, "sources": _GEMM_SRC, "sha256": "5f1cb163daba44e9"},
-    ("pi0_bf16_b1", "mlp_down"): {"bytes": 13740042, "sources": _GEMM_SRC, "sha256": "5f1cb163daba44e9"},
-    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90489694, "sources": _GEMM_SRC, "sha256": "5f1cb163daba44e9"},
+    ("pi0_bf16_b1", "attn"): {"bytes": 6231937, "sources": _ATTN_SRC, "sha256": "e685413a2b9f7003"},
+    ("pi0_bf16_b1", "qkv"): {"bytes": 6563336, "sources": _GEMM_SRC, "sha256": "5db3ad0a4ad3fe70"},
+    ("pi0_bf16_b1", "oproj"): {"bytes": 9306119, "sources": _MERGE_SRC, "sha256": "0baa552e408fe7ac"},
+    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18192401, "sources": _GEMM_SRC, "sha256": "5db3ad0a4ad3fe70"},
+    ("pi0_bf16_b1", "mlp_down"): {"bytes": 12477449, "sources": _GEMM_SRC, "sha256": "5db3ad0a4ad3fe70"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90359725, "sources": _GEMM_SRC, "sha256": "5db3ad0a4ad3fe70"},
 }
 
 
