@@ -78,7 +78,9 @@ __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int
 
 // Small-row GEMM (batch-1 style): one block = 4 waves computing 16*MT rows x
 // 32*NP columns; the block's K range is split between the 4 waves, whose
-// partial sums are added through LDS, and wave w < MT finishes row tile w.
+// partial sums are added through LDS.  Wave w finishes row tile w % MT, the
+// MT of its accumulator rows starting at (w / MT) * MT: with fewer row tiles
+// than waves, the waves share each tile's epilogue.
 // Fewer row tiles per block mean fewer activation bytes per block; the row
 // blocks of one column tile share its weights in their XCD's L2.  With g.split_out set, blockIdx.z
 // selects a slice of K and the block writes its raw partial sums to
@@ -115,14 +117,14 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
     alp[mt] = SPLIT ? static_cast<const bf16_t*>(g.A_lo) + (int64_t)lr * g.lda + akg * 8 : nullptr;
   }
 
-  // Epilogue inputs of the rows this wave finishes (wave w finishes row
-  // tile w): they do not depend on the products, so the first trip requests
-  // them right behind its operands and they land together.  Rows past R (and
-  // the rows of waves with no row tile) read row 0, columns past N the last
-  // pair tile; none of them is stored.
+  // Epilogue inputs of the rows this wave finishes: they do not depend on the
+  // products, so the first trip requests them right behind its operands and
+  // they land together.  Rows past R read row 0, columns past N the last pair
+  // tile; neither is stored.
   const int c = lane % 16;
+  const int emt = wave % MT, ev0 = (wave / MT) * MT;   // row tile, first accumulator row
   typename Epi::ColPre cq[NP];
-  typename Epi::Pre pre[NP][4];
+  typename Epi::Pre pre[NP][MT];
   float sc[NP][2];
   auto epi_loads = [&]() {
 #pragma unroll
@@ -132,9 +134,9 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
       sc[pp][0] = g.scale ? g.scale[32 * p + c] : 1.f;
       sc[pp][1] = g.scale ? g.scale[32 * p + 16 + c] : 1.f;
 #pragma unroll
-      for (int v = 0; v < 4; ++v) {
-        const int row = m0 + 16 * wave + 4 * akg + v;
-        pre[pp][v] = epi.pre(row < g.R && wave < MT ? row : 0, p, c);
+      for (int vv = 0; vv < MT; ++vv) {
+        const int row = m0 + 16 * emt + 4 * akg + ev0 + vv;
+        pre[pp][vv] = epi.pre(row < g.R ? row : 0, p, c);
       }
     }
   };
@@ -174,47 +176,45 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
       for (int v = 0; v < 4; ++v) red[wave][(mt * NT + t) * 4 + v][lane] = acc[mt][t][v];
   __syncthreads();
 
-  // wave w finishes row tile w
-  if (wave >= MT) return;
-  const int mt = wave;
+  const int mt = emt;
   const int N = 32 * g.NPT;
   float* sp = g.split_out ? g.split_out + (int64_t)z * g.split_stride : nullptr;
   // rows of a request past its prefix length (rows_per_req > 0) count as zero
-  bool rowok[4];
+  bool rowok[MT];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int row = m0 + 16 * mt + 4 * akg + v;
-    rowok[v] = true;
-    if (g.rows_per_req > 0 && row < g.R) rowok[v] = (row % g.rows_per_req) < g.desc->prefix_len[row / g.rows_per_req];
+  for (int vv = 0; vv < MT; ++vv) {
+    const int row = m0 + 16 * mt + 4 * akg + ev0 + vv;
+    rowok[vv] = true;
+    if (g.rows_per_req > 0 && row < g.R) rowok[vv] = (row % g.rows_per_req) < g.desc->prefix_len[row / g.rows_per_req];
   }
 #pragma unroll
   for (int pp = 0; pp < NP; ++pp) {
     const int p = pt0 + pp;
     if (p >= g.NPT) break;
-    float s0[4], s1[4];
+    float s0[MT], s1[MT];
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      s0[v] = s1[v] = 0.f;
+    for (int vv = 0; vv < MT; ++vv) {
+      s0[vv] = s1[vv] = 0.f;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        s0[v] += red[w][(mt * NT + 2 * pp) * 4 + v][lane];
-        s1[v] += red[w][(mt * NT + 2 * pp + 1) * 4 + v][lane];
+        s0[vv] += red[w][(mt * NT + 2 * pp) * 4 + ev0 + vv][lane];
+        s1[vv] += red[w][(mt * NT + 2 * pp + 1) * 4 + ev0 + vv][lane];
       }
-      if (!rowok[v]) s0[v] = s1[v] = 0.f;   // what a zero A row gives
+      if (!rowok[vv]) s0[vv] = s1[vv] = 0.f;   // what a zero A row gives
     }
     // the epilogue loads landed with the operands; saying so here keeps the
     // compiler from waiting again, stores included, in front of each row's
     // guarded stores
     __builtin_amdgcn_s_waitcnt(0xF70);        // vmcnt(0), other counters open
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int row = m0 + 16 * mt + 4 * akg + v;
+    for (int vv = 0; vv < MT; ++vv) {
+      const int row = m0 + 16 * mt + 4 * akg + ev0 + vv;
       if (row < g.R) {
         if (sp) {
-          sp[(int64_t)row * N + 32 * p + c] = s0[v] * sc[pp][0];
-          sp[(int64_t)row * N + 32 * p + 16 + c] = s1[v] * sc[pp][1];
+          sp[(int64_t)row * N + 32 * p + c] = s0[vv] * sc[pp][0];
+          sp[(int64_t)row * N + 32 * p + 16 + c] = s1[vv] * sc[pp][1];
         } else {
-          epi.apply(row, p, c, cq[pp], pre[pp][v], s0[v] * sc[pp][0], s1[v] * sc[pp][1]);
+          epi.apply(row, p, c, cq[pp], pre[pp][vv], s0[vv] * sc[pp][0], s1[vv] * sc[pp][1]);
         }
       }
     }
