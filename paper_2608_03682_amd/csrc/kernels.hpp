@@ -501,8 +501,16 @@ struct ReadoutArgs {
   const float* out_b;       // [A]
   const float* dt;          // t_{k+1} - t_k (device scalar)
   float* x;                 // [B][H][A], updated in place
+  // With has_next, the next step's embedding of the updated rows (and the
+  // state rows' reset) as embed_actions would do it with `next`; only where
+  // readout_fuses_embedding says so.
+  int has_next;
+  EmbedArgs next;
 };
 void readout_euler(const ReadoutArgs&, hipStream_t);
+// Whether readout_euler can take has_next for these sizes: only its one-row
+// blocks (the four-row form needs too many registers with the embedding).
+bool readout_fuses_embedding(int A, int d, int rows, bool pending);
 
 void copy_noise_to_state(const CallDesc* desc, float* x, int64_t n, hipStream_t);
 void copy_state_to_out(const CallDesc* desc, const float* x, int64_t n, hipStream_t);

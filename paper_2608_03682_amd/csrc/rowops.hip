@@ -511,7 +511,7 @@ __device__ __forceinline__ void block_sums(float (&v)[K], float (*scratch)[K]) {
 // trip.  RB = 1 adds the pending split partials of the last block; RB > 1
 // (rows without them) shares each W_out load among RB rows.  Per output the
 // products are summed in the order of readout_kernel.
-template <int RB, int NG>
+template <int RB, int NG, bool FUSE>
 __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
   constexpr int QA = 8;                      // outputs per wave
   __shared__ float4 nrm4[RB][NG * kWave];
@@ -576,6 +576,31 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
     }
   }
 
+  // Fused with the next step's embedding: its inputs that do not depend on
+  // the update (the embedding weights for this thread's four columns, bias,
+  // row vector, position and state rows) are requested with the rows.
+  const EmbedArgs& e = r.next;
+  const int ec = 4 * threadIdx.x;              // d <= 1024: one group of four columns
+  const bool ecv = ec < d;
+  const int ecc = ecv ? ec : 0;
+  float4 ew[FUSE ? 32 : 1], ebias = make_float4(0.f, 0.f, 0.f, 0.f), erv = ebias;
+  float4 epv[FUSE ? RB : 1], esv[FUSE ? RB : 1];
+  if constexpr (FUSE) {
+#pragma unroll
+    for (int a = 0; a < 32; ++a)
+      ew[a] = *reinterpret_cast<const float4*>(e.in_w + (int64_t)min(a, e.A - 1) * d + ecc);
+    ebias = *reinterpret_cast<const float4*>(e.in_b + ecc);
+    if (e.rowvec) erv = *reinterpret_cast<const float4*>(e.rowvec + ecc);
+#pragma unroll
+    for (int rr = 0; rr < RB; ++rr) {
+      const int ar = min(ar0 + rr, nrows - 1);
+      const int b = ar / r.H, j = ar % r.H;
+      epv[rr] = e.pos ? *reinterpret_cast<const float4*>(e.pos + (int64_t)j * d + ecc) : make_float4(0.f, 0.f, 0.f, 0.f);
+      esv[rr] = e.off ? *reinterpret_cast<const float4*>(e.e_state + (int64_t)b * d + ecc)
+                      : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  }
+
   float mu[RB], st[RB];
 #pragma unroll
   for (int rr = 0; rr < RB; ++rr) {
@@ -636,7 +661,59 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
     }
   }
   __syncthreads();
-  if (upd) r.x[xi] = xv + dtv * (red[ur][ua] + bv);
+  const float xn = xv + dtv * (red[ur][ua] + bv);
+  if (upd) r.x[xi] = xn;
+  if constexpr (FUSE) {
+    // y = act(x_new . in_w + in_b + rowvec + pos[j]) into the next step's
+    // embedding destination (embed_rows_kernel's arithmetic), and the state
+    // row of request b reset with the row of its first action
+    __shared__ __attribute__((aligned(16))) float xs[RB][32];
+    if (threadIdx.x < RB * 32 && threadIdx.x % 32 >= r.A) xs[threadIdx.x / 32][threadIdx.x % 32] = 0.f;
+    if (upd) xs[ur][ua] = xn;
+    __syncthreads();
+    if (!ecv) return;
+#pragma unroll
+    for (int rr = 0; rr < RB; ++rr) {
+      const int ar = ar0 + rr;
+      if (ar >= nrows) break;
+      const int b = ar / r.H, j = ar % r.H;
+      float y[4] = {ebias.x, ebias.y, ebias.z, ebias.w};
+      float xr[32];
+#pragma unroll
+      for (int a4 = 0; a4 < 8; ++a4) {
+        const float4 x4 = reinterpret_cast<const float4*>(xs[rr])[a4];
+        xr[4 * a4] = x4.x; xr[4 * a4 + 1] = x4.y; xr[4 * a4 + 2] = x4.z; xr[4 * a4 + 3] = x4.w;
+      }
+#pragma unroll
+      for (int a = 0; a < 32; ++a) {
+        y[0] = fmaf(xr[a], ew[a].x, y[0]);
+        y[1] = fmaf(xr[a], ew[a].y, y[1]);
+        y[2] = fmaf(xr[a], ew[a].z, y[2]);
+        y[3] = fmaf(xr[a], ew[a].w, y[3]);
+      }
+      const float r4[4] = {erv.x, erv.y, erv.z, erv.w}, p4[4] = {epv[rr].x, epv[rr].y, epv[rr].z, epv[rr].w};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        if (e.rowvec) y[q] += r4[q];
+        if (e.pos) y[q] += p4[q];
+        y[q] = apply_act(e.act, y[q]);
+      }
+      if (e.act_out) {
+        const int64_t o = ((int64_t)b * e.H + j) * d + ec;
+        if (e.act_is_bf16) {
+          uint2 u;
+          u.x = pack_bf16x2(y[0], y[1]);
+          u.y = pack_bf16x2(y[2], y[3]);
+          *reinterpret_cast<uint2*>(static_cast<bf16_t*>(e.act_out) + o) = u;
+        } else {
+          *reinterpret_cast<float4*>(static_cast<float*>(e.act_out) + o) = make_float4(y[0], y[1], y[2], y[3]);
+        }
+      } else {
+        *reinterpret_cast<float4*>(e.h + ((int64_t)b * e.M + e.off + j) * d + ec) = make_float4(y[0], y[1], y[2], y[3]);
+      }
+      if (e.off && j == 0) *reinterpret_cast<float4*>(e.h + (int64_t)b * e.M * d + ec) = esv[rr];
+    }
+  }
 }
 
 __global__ __launch_bounds__(128) void rope_table_kernel(const CallDesc* desc, const float* inv_freq, float2* tab,
@@ -717,14 +794,25 @@ void embed_state(const CallDesc* desc, const float* w, const float* b, float* e,
                  hipStream_t s) {
   hipLaunchKernelGGL(state_embed_kernel, dim3(B), dim3(256), 0, s, desc, w, b, e, A, d);
 }
+// the readout rows kernel takes four rows per block for many rows without a
+// pending residual, one otherwise
+static bool readout_four_rows(int rows, bool pending) { return !pending && rows >= 1024; }
+
+bool readout_fuses_embedding(int A, int d, int rows, bool pending) {
+  return A <= 32 && (d == 1024 || d == 256) && !readout_four_rows(rows, pending);
+}
+
 void readout_euler(const ReadoutArgs& r, hipStream_t s) {
   const int rows = r.B * r.H;
+  const bool four = readout_four_rows(rows, r.pend.n > 0);
   auto rows_kernel = [&](auto ng) {
     constexpr int NG = decltype(ng)::value;
-    if (r.pend.n == 0 && rows >= 1024)
-      hipLaunchKernelGGL((readout_rows_kernel<4, NG>), dim3((rows + 3) / 4), dim3(256), 0, s, r);
+    if (four)
+      hipLaunchKernelGGL((readout_rows_kernel<4, NG, false>), dim3((rows + 3) / 4), dim3(256), 0, s, r);
+    else if (r.has_next)
+      hipLaunchKernelGGL((readout_rows_kernel<1, NG, true>), dim3(rows), dim3(256), 0, s, r);
     else
-      hipLaunchKernelGGL((readout_rows_kernel<1, NG>), dim3(rows), dim3(256), 0, s, r);
+      hipLaunchKernelGGL((readout_rows_kernel<1, NG, false>), dim3(rows), dim3(256), 0, s, r);
   };
   if (r.A <= 32 && r.d == 1024) rows_kernel(std::integral_constant<int, 4>{});
   else if (r.A <= 32 && r.d == 256) rows_kernel(std::integral_constant<int, 1>{});

@@ -528,8 +528,8 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
     prefix_relayout(ra, static_cast<T*>(nullptr), s);
   }
 
-  for (int k = 0; k < K; ++k) {
-    // ---- action tokens -> h
+  // the action-token embedding of step k (state rows of h reset too)
+  auto embed_args = [&](int k) {
     EmbedArgs em{};
     em.x = e.x;
     em.in_w = e.in_w;
@@ -541,14 +541,22 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
     em.B = B; em.H = H; em.M = M; em.A = e.A; em.d = d; em.off = e.off;
     if (variant == PHYAI_VARIANT_PI0) {
       // z = swish(W1a (W_in x + b_in) + (W1t tau(t_k) + b1)), the embedding
-      // folded into W1a (tin_w, tin_b); the state rows of h are reset too
+      // folded into W1a (tin_w, tin_b)
       em.in_w = e.tin_w;
       em.in_b = e.tin_b;
       em.rowvec = e.T + (int64_t)k * d;
       em.act = ACT_SWISH;
       em.act_out = e.zbuf;
     }
-    embed_actions(em, s);
+    return em;
+  };
+  // the readout of step k also embeds the updated rows for step k + 1 where
+  // its kernel can (one launch less per step)
+  bool embedded = false;
+
+  for (int k = 0; k < K; ++k) {
+    // ---- action tokens -> h
+    if (!embedded) embed_actions(embed_args(k), s);
     if (variant == PHYAI_VARIANT_PI0) {
       // u = W2 z + b2, written into the action rows of h
       EpiStore<float> ep = store_epi<float>(e.h, d, e.time_b2, nullptr, ACT_NONE);
@@ -564,6 +572,11 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
     ro.eps = e.c.rms_eps;
     ro.out_w = e.out_w; ro.out_b = e.out_b; ro.dt = e.dt + k; ro.x = e.x;
     ro.pend = pending_of(e, 1, L - 1, k, B);
+    embedded = k + 1 < K && readout_fuses_embedding(e.A, d, B * H, ro.pend.n > 0);
+    if (embedded) {
+      ro.has_next = 1;
+      ro.next = embed_args(k + 1);
+    }
     if (variant == PHYAI_VARIANT_PI0) { ro.mode = NORM_RMS; ro.mul = e.final_norm; ro.shift = nullptr; }
     else if (variant == PHYAI_VARIANT_PI05) {
       ro.mode = NORM_RMS;
