@@ -164,9 +164,10 @@ int phyai_debug_hidden(phyai_expert* e, float* dst, int32_t batch, void* stream)
  * current schedule, the batch of the last phyai_denoise call), eagerly on
  * `stream`, so that a caller can time a single kernel with events.
  * Stages: 0 norm before attention, 1 QKV GEMM (+RoPE, KV write),
- * 2 attention (+split combine), 3 O-projection GEMM + residual, 4 norm
- * before the MLP, 5 gate/up GEMM + GeGLU (DiT: MLP-in + GELU), 6 down GEMM
- * + residual.  Requires a previous phyai_denoise on this handle (the stage
+ * 2 attention (with key splits, the merge kernel too when the O projection
+ * does not merge them), 3 O-projection GEMM + residual (at small batch it
+ * merges the attention's key splits on the way in), 4 norm before the MLP,
+ * 5 gate/up GEMM + GeGLU (DiT: MLP-in + GELU), 6 down GEMM + residual.  Requires a previous phyai_denoise on this handle (the stage
  * reads the buffers it left); it overwrites working buffers only, never the
  * caller's.  Loop semantics (Section "PhyAI Architecture", paragraph
  * "Kernel fusion", lists these fused operators). */
