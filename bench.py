@@ -7,12 +7,19 @@ Euler update), i.e. one action chunk per request.
 
 Headline (value): pi0-shaped expert, bf16 weights, batch 1 -- ms per chunk.
 Also measured in the same run and reported in the same JSON line:
+  * chunk_roofline: algorithmic bytes of a chunk (weights, prefix K/V,
+    small per-step weights and boundary I/O; setup-only work excluded) over
+    the chunk time, against the HBM datasheet roof and the measured copy roof.
   * batch64: the pi0-shaped expert at rollout batch 64 with ragged prefixes
-    and fp8 weights -- chunks/s = B / T_sync (the paper's Q(B)).
-  * roofline: the dominant kernel of each leg, its algorithmic bytes (B=1,
-    HBM-bound) or FLOPs (B=64, MFMA-bound) per launch over its average
-    duration, timed with HIP events on the stream it runs on.
-  * cpu_baseline: the fp64 oracle on this host's cores, one chunk.
+    and fp8 weights -- chunks/s = B / T_sync (the paper's Q(B)), with the
+    whole batch's MFMA fraction of the bf16 peak.
+  * legs: the pi0.5-shaped and DiT-shaped batch-1 workloads and the tiny
+    fp32 expert, ms per chunk each with its chunk roofline.
+  * roofline: the dominant kernel of the batch-1 leg, its algorithmic bytes
+    per launch over its average duration, timed with HIP events on the stream
+    it runs on.
+  * cpu_baseline: the oracle on this host's cores (float64, the parity
+    reference, and its float32 timing mode), with the CPU model and BLAS.
 
 Inputs are seeded synthetic tensors resident in HBM before the timed region.
 """
@@ -115,14 +122,37 @@ def stage_bytes_flops(cfg, B, plen_sum):
 
 
 def chunk_bytes(cfg, B, plen_sum):
-    """Algorithmic bytes of one phyai_denoise call (K steps): every step
-    streams all trunk weights, the prefix K/V of every layer and the
-    activations; per-step small weights (embedding, time MLP, readout)."""
-    per_layer = stage_bytes_flops(cfg, B, plen_sum)
-    step = sum(v[0] for v in per_layer.values()) * cfg.n_layers
-    d, A = cfg.d_model, cfg.action_dim
-    small = (2 * d * d * 2 if cfg.variant == "pi0" else 0) + (A * d + d * A) * 4
-    return (step + small) * cfg.n_steps
+    """Algorithmic bytes of one phyai_denoise call (K steps), counted as in
+    the paper's phase roofline (weights + K/V + boundary I/O; setup-only work
+    and redundant recompute excluded): every step streams the trunk weights,
+    the prefix K/V of every layer and the small per-step weights (time-MLP
+    action half and second layer, input and output projections); activations
+    that a fused implementation keeps on chip are not counted.  DiT: the
+    cross-attention K/V projection of the features runs once per call (its
+    weights and the features are counted once), and every step reads the
+    projected K/V of each cross block."""
+    d, A, F, L, K = cfg.d_model, cfg.action_dim, cfg.d_mlp, cfg.n_layers, cfg.n_steps
+    D, nq, nkv = cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
+    qd, kd = nq * D, nkv * D
+    wb = 1 if cfg.weight_dtype == "fp8" else (4 if cfg.weight_dtype == "f32" else 2)
+    sb = 4 if cfg.weight_dtype == "fp8" else 0          # per-column fp32 scales
+    ab = 4 if cfg.weight_dtype == "f32" else 2          # small weights and K/V
+    io = B * cfg.horizon * A * 4 * 2 + (B * A * 4 if cfg.state_token else 0)
+    if cfg.variant == "dit":
+        step_w = 0
+        for l in range(L):
+            cross = l % 2 == 0
+            n_qkv = qd if cross else qd + 2 * kd
+            step_w += (d * n_qkv + qd * d + d * F + F * d) * wb
+        cross_kv_read = (L // 2) * plen_sum * 2 * kd * ab
+        small = 2 * A * d * ab + cfg.horizon * d * 4
+        per_call = (L // 2) * cfg.d_feat * 2 * kd * wb + plen_sum * cfg.d_feat * ab
+        return K * (step_w + cross_kv_read + small) + per_call + io
+    step_w = L * ((d * (qd + 2 * kd) + qd * d + d * 2 * F + F * d) * wb
+                  + ((qd + 2 * kd) + d + 2 * F + d) * sb)
+    prefix_kv = L * plen_sum * 2 * kd * ab
+    small = 2 * A * d * ab + (2 * d * d * ab if cfg.variant == "pi0" else 0)
+    return K * (step_w + prefix_kv + small) + io
 
 
 def time_calls(fn, steps, warmup):
@@ -176,27 +206,74 @@ def time_stages(ex, reps=5):
     return res
 
 
-def cpu_baseline(cfg, case):
-    import oracle
+def _host_info():
+    """Threads the oracle's BLAS uses, the CPU model and the BLAS library."""
+    cores, blas = os.cpu_count() or 1, "unknown"
     try:
         from threadpoolctl import threadpool_info
-        cores = max((p.get("num_threads", 1) for p in threadpool_info()), default=1)
+        pools = [p for p in threadpool_info() if p.get("user_api") == "blas"]
+        if pools:
+            cores = max(p.get("num_threads", 1) for p in pools)
+            blas = ", ".join(f"{p.get('internal_api')} {p.get('version')}" for p in pools)
     except Exception:
-        cores = os.cpu_count() or 1
-    W = oracle.DecodedWeights(case.weights)
-    runs = []
-    t_total = 0.0
-    while len(runs) < 3 and (t_total < 10.0 or not runs):
+        pass
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return int(cores), model, blas
+
+
+def _time_oracle(cfg, case, dtype, budget_s, max_runs=3, prefix=None, n_req=None):
+    """Median wall time of oracle.denoise over up to max_runs runs (at least
+    one; stops adding runs once budget_s is spent).  With n_req, only the
+    first n_req requests run, against `prefix` holding just their slots."""
+    import oracle
+    W = oracle.DecodedWeights(case.weights, dtype)
+    n = case.noise.shape[0] if n_req is None else n_req
+    pre = case.prefix if prefix is None else prefix
+    runs, spent = [], 0.0
+    while len(runs) < max_runs and (spent < budget_s or not runs):
         t0 = time.perf_counter()
-        oracle.denoise(cfg, case.weights, case.prefix, case.prefix_len, case.noise, case.timesteps,
-                       case.state, decoded=W)
+        oracle.denoise(cfg, case.weights, pre, case.prefix_len[:n], case.noise[:n], case.timesteps,
+                       None if case.state is None else case.state[:n], decoded=W, dtype=dtype)
         dt = time.perf_counter() - t0
         runs.append(dt)
-        t_total += dt
-    ms = float(np.median(runs)) * 1e3
-    return {"value": ms, "unit": "ms/chunk", "cores": int(cores), "kind": "oracle",
-            "sample": f"{len(runs)} full chunk(s) of the batch-1 pi0 workload (K={cfg.n_steps} Euler steps, "
-                      f"L={cfg.n_layers}), float64 NumPy oracle, median"}
+        spent += dt
+    return float(np.median(runs)), len(runs)
+
+
+def cpu_baseline(cfg, case):
+    """The oracle on the host cores: float64 (the parity reference, `value`)
+    and its float32 timing mode, full chunks of the batch-1 pi0 workload."""
+    cores, model, blas = _host_info()
+    t64, n64 = _time_oracle(cfg, case, np.float64, 8.0)
+    t32, n32 = _time_oracle(cfg, case, np.float32, 6.0)
+    return {"value": round(t64 * 1e3, 1), "unit": "ms/chunk", "cores": cores, "kind": "oracle",
+            "sample": f"{n64} full chunk(s) of the batch-1 pi0 workload (K={cfg.n_steps} Euler steps, "
+                      f"L={cfg.n_layers}), float64 NumPy oracle, median; float32 mode {n32} chunk(s)",
+            "fp32_ms_per_chunk": round(t32 * 1e3, 1), "cpu_model": model, "blas": blas}
+
+
+def cpu_baseline_batch(cfg, case, seed, n_req=2):
+    """The float64 oracle on the first n_req requests of a batch, scaled to
+    the batch (requests are independent, so the oracle's time is linear in
+    them): chunks/s and ms per batch."""
+    import workloads as wl
+    cores, model, blas = _host_info()
+    pre = wl.make_prefix(cfg, case.prefix_len, seed, requests=list(range(n_req)))
+    t, _ = _time_oracle(cfg, case, np.float64, 0.0, max_runs=1, prefix=pre, n_req=n_req)
+    per_req = t / n_req
+    return {"value": round(1.0 / per_req, 3), "unit": "chunks/s", "cores": cores,
+            "kind": "oracle", "ms_per_batch": round(per_req * cfg.batch * 1e3, 1),
+            "sample": f"{n_req} of the {cfg.batch} requests (prefix lengths "
+                      f"{', '.join(str(int(p)) for p in case.prefix_len[:n_req])}), one run, float64 NumPy "
+                      f"oracle, scaled to the batch", "cpu_model": model, "blas": blas}
 
 
 def measured_roofs():
@@ -233,6 +310,15 @@ def measured_roofs():
     return out
 
 
+def chunk_roofline(cfg, B, plen_sum, ms, copy_gbs=None):
+    cb = chunk_bytes(cfg, B, plen_sum)
+    ach = cb / (ms * 1e-3) / 1e9
+    out = {"bytes_per_chunk": int(cb), "achieved_GBs": round(ach, 1), "frac_of_hbm_peak": round(ach / HBM_PEAK_GBS, 4)}
+    if copy_gbs:
+        out["frac_of_measured_copy"] = round(ach / copy_gbs, 4)
+    return out
+
+
 def leg_batch1(args, px, wl, K, W):
     import torch
     cfg = wl.CONFIGS["pi0_bf16_b1"]
@@ -248,7 +334,6 @@ def leg_batch1(args, px, wl, K, W):
     ms = wall * 1e3 / K
     assert np.isfinite(out.cpu().numpy()).all()
     plen_sum = int(case.prefix_len.sum())
-    cb = chunk_bytes(cfg, 1, plen_sum)
     roof, stages = None, {}
     if not args.no_stages:
         stages = time_stages(ex)
@@ -258,7 +343,8 @@ def leg_batch1(args, px, wl, K, W):
         ach = dom_bytes / (stages[dom] * 1e-6) / 1e9
         roof = {"bound": "hbm", "achieved": round(ach, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                 "frac": round(ach / HBM_PEAK_GBS, 4), "traffic": measured_traffic(cfg.name, dom),
-                "kernel": dom, "bytes_per_launch": int(dom_bytes), "avg_us": round(stages[dom], 2)}
+                "kernel": dom, "bytes_per_launch": int(dom_bytes), "avg_us": round(stages[dom], 2),
+                "timing": "graph replay of the stage over all layers, HIP events on the replay stream"}
     rec = {
         "metric": "pi0-shape action-chunk latency ms @B=1 + chunks/s @B=64; % HBM / MFMA peak",
         "value": round(ms, 4), "unit": "ms/chunk", "n_gpus": 1, "steps": K, "warmup": W,
@@ -269,21 +355,94 @@ def leg_batch1(args, px, wl, K, W):
                    "batch": 1, "prefix_len": int(case.prefix_len[0]), "euler_steps": cfg.n_steps},
         "latency_ms": {"mean": round(float(per.mean()), 4), "p50": round(float(np.median(per)), 4),
                        "p99": round(float(np.percentile(per, 99)), 4)},
+        "chunks_per_s": round(1e3 / ms, 1),
         "stage_us_per_launch": {k: round(v, 2) for k, v in stages.items()},
         "roofline": roof,
-        "chunk_roofline": {"bytes_per_chunk": int(cb), "achieved_GBs": round(cb / (ms * 1e-3) / 1e9, 1),
-                           "frac_of_hbm_peak": round(cb / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4)},
     }
     if not args.no_roofs:
         _log("measuring the copy and GEMM roofs")
         rec["measured_roofs"] = measured_roofs()
+    copy = rec.get("measured_roofs", {}).get("copy_GBs")
+    rec["chunk_roofline"] = chunk_roofline(cfg, 1, plen_sum, ms, copy)
     if not args.no_cpu_baseline:
         _log("timing the CPU oracle baseline")
         rec["cpu_baseline"] = cpu_baseline(cfg, case)
     ex.close()
     del prefix, noise, state, out, case
     torch.cuda.empty_cache()
+    return rec
 
+
+def leg_plain(args, px, wl, name, K, W, copy_gbs):
+    """ms per chunk of another batch-1 workload, with its chunk roofline."""
+    import torch
+    cfg = wl.CONFIGS[name]
+    _log(f"generating {name}")
+    case = wl.make_case(cfg, seed=args.seed)
+    ex = px.Expert(cfg, case.weights)
+    prefix, noise, state = _upload(case)
+    out = torch.empty_like(noise)
+    ex.prepare(cfg.batch, cfg.n_steps)
+    fn = lambda: ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=out)
+    _log(f"timing {name}: {W} warmup + {K} timed")
+    wall, per = time_calls(fn, K, W)
+    ms = wall * 1e3 / K
+    assert np.isfinite(out.cpu().numpy()).all()
+    rec = {"ms_per_chunk": round(ms, 4), "p50_ms": round(float(np.median(per)), 4), "steps": K, "warmup": W,
+           "dtype": "f32" if cfg.weight_dtype == "f32" else "bf16",
+           "chunk_roofline": chunk_roofline(cfg, cfg.batch, int(case.prefix_len.sum()), ms, copy_gbs)}
+    ex.close()
+    del prefix, noise, state, out, case
+    torch.cuda.empty_cache()
+    return rec
+
+
+def leg_batch64(args, px, wl, K, W):
+    import torch
+    cfg = wl.CONFIGS["pi0_fp8_b64"]
+    _log(f"generating {cfg.name}")
+    case = wl.make_case(cfg, seed=args.seed)
+    ex = px.Expert(cfg, case.weights)
+    prefix, noise, state = _upload(case)
+    out = torch.empty_like(noise)
+    ex.prepare(cfg.batch, cfg.n_steps)
+    fn = lambda: ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=out)
+    K64 = K if K < 5 else max(5, K // 5)
+    W64 = W if W < 2 else max(2, W // 5)
+    _log(f"timing {cfg.name}: {W64} warmup + {K64} timed")
+    wall, per = time_calls(fn, K64, W64)
+    ms64 = wall * 1e3 / K64
+    assert np.isfinite(out.cpu().numpy()).all()
+    plen_sum = int(case.prefix_len.sum())
+    sb = stage_bytes_flops(cfg, cfg.batch, plen_sum)
+    chunk_flops = sum(v[1] for v in sb.values()) * cfg.n_layers * cfg.n_steps
+    roof, stages = None, {}
+    if not args.no_stages:
+        stages = time_stages(ex, reps=2)
+        dom = max(("qkv", "attn", "oproj", "mlp_up", "mlp_down"), key=lambda s: stages[s])
+        fl = sb[dom][1]
+        ach = fl / (stages[dom] * 1e-6) / 1e12
+        roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(cfg.name, dom),
+                "kernel": dom, "flops_per_launch": int(fl), "avg_us": round(stages[dom], 2)}
+    tf = chunk_flops / (ms64 * 1e-3) / 1e12
+    rec = {
+        "workload": "pi0_fp8_b64: pi0 shape, B=64, ragged prefixes U[600,1000], fp8 e4m3 trunk weights "
+                    "(per-output-channel scales), bf16 prefix K/V, K=10",
+        "steps": K64, "warmup": W64, "ms_per_batch": round(ms64, 3),
+        "chunks_per_s": round(cfg.batch / (ms64 * 1e-3), 1),
+        "stage_us_per_launch": {k: round(v, 2) for k, v in stages.items()},
+        "roofline": roof,
+        "batch_roofline": {"bound": "mfma", "flops_per_batch": int(chunk_flops), "achieved_TFLOPs": round(tf, 1),
+                           "peak": BF16_PEAK_TFLOPS, "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4)},
+        "batch_TFLOPs": round(tf, 1),
+    }
+    if not args.no_cpu_baseline:
+        _log("timing the CPU oracle baseline on a sample of the batch")
+        rec["cpu_baseline"] = cpu_baseline_batch(cfg, case, args.seed)
+    ex.close()
+    del prefix, noise, state, out, case
+    torch.cuda.empty_cache()
     return rec
 
 
@@ -296,6 +455,7 @@ def main():
     ap.add_argument("--no-batch64", action="store_true")
     ap.add_argument("--no-batch1", action="store_true",
                     help="only the batch-64 leg (for counter passes; the line then has no batch-1 value)")
+    ap.add_argument("--no-legs", action="store_true", help="skip the pi0.5, DiT and tiny fp32 workloads")
     ap.add_argument("--no-stages", action="store_true",
                     help="skip the per-stage graph timings and the rooflines built on them (counter passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -313,52 +473,19 @@ def main():
     torch.cuda.set_device(0)
     K, W = args.steps, args.warmup
 
-    # ---------------- batch 1, pi0-shaped, bf16 ----------------
     rec = {}
     if not args.no_batch1:
         rec = leg_batch1(args, px, wl, K, W)
     elif not args.no_roofs:
         _log("measuring the copy and GEMM roofs")
         rec["measured_roofs"] = measured_roofs()      # counter passes calibrate on its copy
-
-    # ---------------- batch 64, ragged prefixes, fp8 weights ----------------
+    copy = rec.get("measured_roofs", {}).get("copy_GBs")
+    if not args.no_legs:
+        Kl, Wl = max(1, min(K, 20)), min(W, 5)
+        rec["legs"] = {n: leg_plain(args, px, wl, n, Kl, Wl, copy)
+                       for n in ("pi05_bf16_b1", "dit_bf16_b1", "tiny_fp32")}
     if not args.no_batch64:
-        cfg = wl.CONFIGS["pi0_fp8_b64"]
-        _log(f"generating {cfg.name}")
-        case = wl.make_case(cfg, seed=args.seed)
-        ex = px.Expert(cfg, case.weights)
-        prefix, noise, state = _upload(case)
-        out = torch.empty_like(noise)
-        ex.prepare(cfg.batch, cfg.n_steps)
-        fn = lambda: ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=out)
-        K64 = K if K < 5 else max(5, K // 5)
-        W64 = W if W < 2 else max(2, W // 5)
-        _log(f"timing {cfg.name}: {W64} warmup + {K64} timed")
-        wall, per = time_calls(fn, K64, W64)
-        ms64 = wall * 1e3 / K64
-        assert np.isfinite(out.cpu().numpy()).all()
-        plen_sum = int(case.prefix_len.sum())
-        sb = stage_bytes_flops(cfg, cfg.batch, plen_sum)
-        chunk_flops = sum(v[1] for v in sb.values()) * cfg.n_layers * cfg.n_steps
-        roof, stages = None, {}
-        if not args.no_stages:
-            stages = time_stages(ex, reps=2)
-            dom = max(("qkv", "attn", "oproj", "mlp_up", "mlp_down"), key=lambda s: stages[s])
-            fl = sb[dom][1]
-            ach = fl / (stages[dom] * 1e-6) / 1e12
-            roof = {"bound": "mfma", "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
-                    "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": measured_traffic(cfg.name, dom),
-                    "kernel": dom, "flops_per_launch": int(fl), "avg_us": round(stages[dom], 2)}
-        rec["batch64"] = {
-            "workload": "pi0_fp8_b64: pi0 shape, B=64, ragged prefixes U[600,1000], fp8 e4m3 trunk weights "
-                        "(per-output-channel scales), bf16 prefix K/V, K=10",
-            "steps": K64, "warmup": W64, "ms_per_batch": round(ms64, 3),
-            "chunks_per_s": round(cfg.batch / (ms64 * 1e-3), 1),
-            "stage_us_per_launch": {k: round(v, 2) for k, v in stages.items()},
-            "roofline": roof,
-            "batch_TFLOPs": round(chunk_flops / (ms64 * 1e-3) / 1e12, 1),
-        }
-        ex.close()
+        rec["batch64"] = leg_batch64(args, px, wl, K, W)
     print(json.dumps(rec), flush=True)
 
 

@@ -62,7 +62,7 @@ typedef enum {
 typedef struct {
   int32_t variant;          /* phyai_variant                                                      */
   int32_t n_layers;         /* L                                                                  */
-  int32_t d_model;          /* d (multiple of 64)                                                 */
+  int32_t d_model;          /* d (multiple of 256, at most 2048)                                  */
   int32_t n_q_heads;        /* query heads                                                        */
   int32_t n_kv_heads;       /* key/value heads (1 for MQA)                                        */
   int32_t head_dim;         /* 64, 128 or 256                                                     */
@@ -129,6 +129,16 @@ int phyai_load_expert(const phyai_config* cfg, const phyai_tensor* tensors, int3
 
 /* Produce one action chunk per request (the K-step Euler loop).
  *
+ * Operation: the policy map from an observation to an action chunk of
+ * Section "Embodied Task Formulation", subsection "From Observation to
+ * Action", for flow policies: x_0 = noise, x_{k+1} = x_k + (t_{k+1} - t_k)
+ * v(x_k, t_k) for k < K, output x_K.  The vision-language prefix state is
+ * computed once per chunk and stays fixed across the K steps while only the
+ * action tokens change; the timestep tables are built before denoising; the
+ * whole loop is captured once per shape bucket and replayed (Section "PhyAI
+ * Architecture", subsection "Optimization Methods", paragraph "Graph
+ * replay").  Requests of a batch are independent (Section "Cloud Batching").
+ *
  *   prefix      device, read-only, caller-owned.  PI0/PI05: the frozen prefix
  *               K/V cache, [L][2][B][prefix_cap][n_kv*head_dim] (index 0 = K,
  *               1 = V; keys already rotated), dtype kv_dtype.  DIT: the VLM
@@ -143,15 +153,39 @@ int phyai_load_expert(const phyai_config* cfg, const phyai_tensor* tensors, int3
  *   batch       B, 1 <= B <= max_batch.
  *   state       device float32 [B][A] when state_token = 1, else ignored.
  *   out_actions device float32 [B][H][A]: x at t_K.  May alias `noise`.
- *   stream      work is enqueued on it; the call returns after enqueueing.
+ *   stream      work is enqueued on it; the call returns after enqueueing
+ *               (it waits on the host only for a schedule change that
+ *               arrives while the previous change's table upload is still
+ *               pending).
+ *
+ * Device pointers (prefix, noise, state, out_actions) must be 16-byte
+ * aligned: the kernels read and write them with 16-byte accesses.  A
+ * misaligned pointer fails with PHYAI_EINVAL before anything is enqueued.
+ * The prefix validity scope is the call: the library keeps no reference to
+ * it after the enqueued work ends.  Calls on one handle must be ordered on
+ * the device (the same stream, or streams the caller orders): they share
+ * the handle's working buffers and timestep tables.
  *
  * The first call for a (batch, n_steps) pair captures a HIP graph of the
- * whole loop; later calls replay it and allocate nothing. */
+ * whole loop (the graph bucket of paragraph "Graph replay"); later calls
+ * replay it and allocate nothing.  Errors: PHYAI_EINVAL for a NULL handle or
+ * argument, a size out of range, a prefix length outside 0..prefix_cap (DiT:
+ * 1..prefix_cap), a non-finite timestep or a misaligned pointer; PHYAI_EHIP
+ * if a HIP call fails (capture, instantiation, launch). */
 int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len,
                   const float* noise, const float* timesteps, int32_t n_steps, int32_t batch,
                   const float* state, float* out_actions, void* stream);
 
-/* Capture the graph for (batch, n_steps) ahead of the first phyai_denoise. */
+/* Capture the graph of the K-step loop for the (batch, n_steps) bucket ahead
+ * of the first phyai_denoise with that shape, so that the first prediction
+ * does not pay for the capture (the runner captures the full loop in the
+ * matching graph bucket once buffers and control flow are stable: Section
+ * "PhyAI Architecture", paragraph "Graph replay").  The graph reads its
+ * per-call pointers and prefix lengths from a device descriptor that
+ * phyai_denoise writes, so one bucket serves every call of that shape.
+ * `stream` is unused (capture runs on a private stream).  Errors:
+ * PHYAI_EINVAL for a NULL handle or a size out of range; PHYAI_EHIP if
+ * capture or instantiation fails.  Idempotent. */
 int phyai_prepare(phyai_expert* e, int32_t batch, int32_t n_steps, void* stream);
 
 /* Copy the residual stream h [B*M][d] (float32) left by the last

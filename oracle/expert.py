@@ -58,10 +58,13 @@ from .numerics import (attention, decode_stored, euler, gelu_tanh, layer_normali
 
 
 class DecodedWeights:
-    """float64 view of the stored weights (decoded once)."""
+    """float64 view of the stored weights (decoded once).  dtype=float32 gives
+    the timing-only single-precision mode (the decode is exact in float64,
+    then rounded once to float32)."""
 
-    def __init__(self, stored: Dict[str, object]):
-        self.w = {k: decode_stored(v) for k, v in stored.items()}
+    def __init__(self, stored: Dict[str, object], dtype=np.float64):
+        self.dtype = np.dtype(dtype)
+        self.w = {k: decode_stored(v).astype(dtype, copy=False) for k, v in stored.items()}
 
     def __getitem__(self, k):
         return self.w[k]
@@ -117,7 +120,7 @@ def velocity_pi0(cfg, W: DecodedWeights, x, t, kv_rows, P, state=None) -> np.nda
     """pi0 expert velocity v(x, t) for one request.  x: [H, A]."""
     d = cfg.d_model
     a = x @ W["in_w"] + W.vec("in_b")
-    tau = sinusoid(t, cfg.time_dim, cfg.sin_min_period, cfg.sin_max_period)
+    tau = sinusoid(t, cfg.time_dim, cfg.sin_min_period, cfg.sin_max_period).astype(W.dtype)
     z = np.concatenate([a, np.broadcast_to(tau, (a.shape[0], cfg.time_dim))], axis=1)
     u = swish(z @ W["time_w1"] + W.vec("time_b1")) @ W["time_w2"] + W.vec("time_b2")
     if cfg.state_token:
@@ -138,7 +141,7 @@ def velocity_pi0(cfg, W: DecodedWeights, x, t, kv_rows, P, state=None) -> np.nda
 
 
 def pi05_condition(cfg, W: DecodedWeights, t) -> np.ndarray:
-    tau = sinusoid(t, cfg.time_dim, cfg.sin_min_period, cfg.sin_max_period)
+    tau = sinusoid(t, cfg.time_dim, cfg.sin_min_period, cfg.sin_max_period).astype(W.dtype)
     return swish(swish(tau @ W["cond_w1"] + W.vec("cond_b1")) @ W["cond_w2"] + W.vec("cond_b2"))
 
 
@@ -165,7 +168,7 @@ def velocity_pi05(cfg, W: DecodedWeights, x, t, kv_rows, P, state=None) -> np.nd
 def velocity_dit(cfg, W: DecodedWeights, x, t, feats, P, state=None) -> np.ndarray:
     """DiT action-head velocity.  feats: [P, d_feat] VLM features."""
     d, nh, D = cfg.d_model, cfg.n_q_heads, cfg.head_dim
-    tau = sinusoid(t, cfg.time_dim, cfg.sin_min_period, cfg.sin_max_period)
+    tau = sinusoid(t, cfg.time_dim, cfg.sin_min_period, cfg.sin_max_period).astype(W.dtype)
     c = swish(tau @ W["cond_w1"] + W.vec("cond_b1")) @ W["cond_w2"] + W.vec("cond_b2")
     sc = swish(c)
     act = x @ W["in_w"] + W.vec("in_b") + W["pos_emb"]
@@ -196,7 +199,7 @@ _VELOCITY = {"pi0": velocity_pi0, "pi05": velocity_pi05, "dit": velocity_dit}
 
 def denoise(cfg, weights, prefix: np.ndarray, prefix_len: Sequence[int], noise: np.ndarray,
             timesteps, state: Optional[np.ndarray] = None, decoded: Optional[DecodedWeights] = None,
-            slots: Optional[Sequence[int]] = None) -> np.ndarray:
+            slots: Optional[Sequence[int]] = None, dtype=np.float64) -> np.ndarray:
     """Run the K-step denoising loop for each request.
 
     prefix: the prefix buffer in the library's layout ([L][2][B][P_cap][n_kv*d_h]
@@ -205,22 +208,25 @@ def denoise(cfg, weights, prefix: np.ndarray, prefix_len: Sequence[int], noise: 
     prefix_len[b], noise[b], state[b] belong to request b.  ``slots`` maps
     request b to its slot in ``prefix`` (default: identity), so a subset of a
     large batch can be checked without materialising the rest.
-    Returns x_K: [B, H, A] float64.
+    ``dtype`` float64 is the parity reference; float32 runs the same steps in
+    single precision (a CPU timing baseline only, never a parity reference).
+    Returns x_K: [B, H, A] in ``dtype``.
     """
     from .numerics import decode_bf16
-    W = decoded if decoded is not None else DecodedWeights(weights)
+    W = decoded if decoded is not None else DecodedWeights(weights, dtype)
     vel = _VELOCITY[cfg.variant]
     B = noise.shape[0]
-    out = np.empty(noise.shape, dtype=np.float64)
-    pre = decode_bf16(prefix) if prefix.dtype == np.uint16 else np.asarray(prefix, np.float64)
+    out = np.empty(noise.shape, dtype=dtype)
+    pre = (decode_bf16(prefix) if prefix.dtype == np.uint16 else np.asarray(prefix, np.float64)).astype(
+        dtype, copy=False)
     for b in range(B):
         i = b if slots is None else slots[b]
         P = int(prefix_len[b])
-        s = None if state is None else np.asarray(state[b], np.float64)
+        s = None if state is None else np.asarray(state[b], dtype)
         if cfg.variant == "dit":
             ctx = pre[i, :P]
         else:
             def ctx(l, i=i, P=P):
                 return _prefix_rows(cfg, pre, i, P, l)
-        out[b] = euler(lambda x, t: vel(cfg, W, x, t, ctx, P, s), noise[b], timesteps)
+        out[b] = euler(lambda x, t: vel(cfg, W, x, t, ctx, P, s), noise[b], timesteps, dtype)
     return out

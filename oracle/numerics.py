@@ -116,8 +116,8 @@ def rope(x: np.ndarray, pos: np.ndarray, base: float) -> np.ndarray:
     inv = base ** (-2.0 * np.arange(half, dtype=np.float64) / D)
     theta = np.asarray(pos, dtype=np.float64)[:, None] * inv[None, :]        # [M, half]
     shape = (x.shape[0],) + (1,) * (x.ndim - 2) + (half,)
-    c = np.cos(theta).reshape(shape)
-    s = np.sin(theta).reshape(shape)
+    c = np.cos(theta).reshape(shape).astype(x.dtype, copy=False)
+    s = np.sin(theta).reshape(shape).astype(x.dtype, copy=False)
     x1, x2 = x[..., :half], x[..., half:]
     return np.concatenate([x1 * c - x2 * s, x2 * c + x1 * s], axis=-1)
 
@@ -177,7 +177,7 @@ def attention_bruteforce(q, k, v, allowed):
     return out
 
 
-def euler(velocity, x0: np.ndarray, timesteps) -> np.ndarray:
+def euler(velocity, x0: np.ndarray, timesteps, dtype=np.float64) -> np.ndarray:
     """Fixed-step explicit Euler integration of dx/dt = velocity(x, t) along the
     caller's schedule t_0 .. t_K, evaluating the velocity at the left end of
     each step: x_{k+1} = x_k + (t_{k+1} - t_k) * velocity(x_k, t_k).
@@ -185,8 +185,8 @@ def euler(velocity, x0: np.ndarray, timesteps) -> np.ndarray:
     The paper's policy refines an action latent over several steps (Section
     "Embodied Task Formulation", "From Observation to Action") and its pi0.5
     configuration takes ten Euler steps (paragraph "Graph replay")."""
-    x = np.array(x0, dtype=np.float64)
+    x = np.array(x0, dtype=dtype)
     ts = [float(t) for t in timesteps]
     for k in range(len(ts) - 1):
-        x = x + (ts[k + 1] - ts[k]) * velocity(x, ts[k])
+        x = x + dtype(ts[k + 1] - ts[k]) * velocity(x, ts[k])
     return x

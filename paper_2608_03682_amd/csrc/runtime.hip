@@ -120,6 +120,10 @@ struct phyai_expert {
   void *tau = nullptr, *c1 = nullptr, *cact = nullptr;
   float *T = nullptr, *modtab = nullptr, *adatab = nullptr, *fintab = nullptr, *dt = nullptr;
   std::vector<float> ts_cached;
+  // pinned staging of the host-built tables (sinusoid, dt): a schedule change
+  // enqueues its upload from here; stage_ev marks the last upload's end
+  void* stage = nullptr;
+  hipEvent_t stage_ev = nullptr;
   int last_batch = 0;       // batch of the last phyai_denoise (0: none yet)
   std::map<std::pair<int, int>, Bucket> buckets;
   hipStream_t cap = nullptr;
@@ -130,6 +134,8 @@ struct phyai_expert {
       if (kv.second.graph) (void)hipGraphDestroy(kv.second.graph);
     }
     if (cap) (void)hipStreamDestroy(cap);
+    if (stage_ev) (void)hipEventDestroy(stage_ev);
+    if (stage) (void)hipHostFree(stage);
   }
 };
 
@@ -607,19 +613,23 @@ void build_tables(phyai_expert& e, const float* ts, int K, hipStream_t s) {
       tau[(size_t)k * td + i] = std::sin(ang);
       tau[(size_t)k * td + half + i] = std::cos(ang);
     }
-  std::vector<float> dts(K);
+  // the staging buffer is rewritten only once the previous upload from it has
+  // run (normally long done, so this does not wait)
+  HIPC(hipEventSynchronize(e.stage_ev));
+  float* dts = static_cast<float*>(e.stage);
   for (int k = 0; k < K; ++k) dts[k] = ts[k + 1] - ts[k];
-  HIPC(hipMemcpyAsync(e.dt, dts.data(), K * 4, hipMemcpyHostToDevice, s));
+  HIPC(hipMemcpyAsync(e.dt, dts, K * 4, hipMemcpyHostToDevice, s));
+  void* tst = dts + e.Kmax;
   if (e.f32) {
-    std::vector<float> tf(tau.begin(), tau.end());
-    HIPC(hipMemcpyAsync(e.tau, tf.data(), tf.size() * 4, hipMemcpyHostToDevice, s));
-    HIPC(hipStreamSynchronize(s));
+    float* tf = static_cast<float*>(tst);
+    for (size_t i = 0; i < tau.size(); ++i) tf[i] = (float)tau[i];
+    HIPC(hipMemcpyAsync(e.tau, tf, tau.size() * 4, hipMemcpyHostToDevice, s));
   } else {
-    std::vector<uint16_t> tb(tau.size());
+    uint16_t* tb = static_cast<uint16_t*>(tst);
     for (size_t i = 0; i < tau.size(); ++i) tb[i] = f2bf((float)tau[i]);
-    HIPC(hipMemcpyAsync(e.tau, tb.data(), tb.size() * 2, hipMemcpyHostToDevice, s));
-    HIPC(hipStreamSynchronize(s));
+    HIPC(hipMemcpyAsync(e.tau, tb, tau.size() * 2, hipMemcpyHostToDevice, s));
   }
+  HIPC(hipEventRecord(e.stage_ev, s));
   T* tau_d = static_cast<T*>(e.tau);
   if (e.c.variant == PHYAI_VARIANT_PI0) {
     gemm_store(gargs(e.time_w1t, tau_d, td, K), store_epi<float>(e.T, d, e.time_b1, nullptr, ACT_NONE), s);
@@ -647,7 +657,6 @@ void build_tables(phyai_expert& e, const float* ts, int K, hipStream_t s) {
     }
   }
   HIPC(hipGetLastError());
-  HIPC(hipStreamSynchronize(s));
   e.ts_cached.assign(ts, ts + K + 1);
 }
 
@@ -657,7 +666,8 @@ void check_config(const phyai_config& c) {
   req(c.n_layers >= 1 && c.d_model >= 64 && c.n_q_heads >= 1 && c.n_kv_heads >= 1, "non-positive size");
   req(c.n_q_heads % c.n_kv_heads == 0, "n_q_heads must be a multiple of n_kv_heads");
   req(c.head_dim == 64 || c.head_dim == 128 || c.head_dim == 256, "head_dim must be 64, 128 or 256");
-  req(c.d_model % 64 == 0 && c.d_model <= 2048, "d_model must be a multiple of 64, at most 2048");
+  // the row kernels take whole 256-column groups per thread block
+  req(c.d_model % 256 == 0 && c.d_model <= 2048, "d_model must be a multiple of 256, at most 2048");
   req(c.d_mlp >= 64 && c.d_mlp % 64 == 0, "d_mlp must be a positive multiple of 64");
   req(c.horizon >= 1 && c.action_dim >= 1 && c.action_dim <= 64, "horizon >= 1 and 1 <= action_dim <= 64");
   req(c.max_steps >= 1 && c.max_steps <= 1024, "max_steps out of range");
@@ -888,10 +898,13 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     e->fintab = e->mem.alloc_n<float>(Km * 2 * d);
   }
   HIPC(hipStreamCreateWithFlags(&e->cap, hipStreamNonBlocking));
+  HIPC(hipHostMalloc(&e->stage, (size_t)Km * 4 + (size_t)Km * c.time_dim * ab, hipHostMallocDefault));
+  HIPC(hipEventCreateWithFlags(&e->stage_ev, hipEventDisableTiming));
   std::vector<float> ts(e->Kmax + 1);
   for (int k = 0; k <= e->Kmax; ++k) ts[k] = (float)(1.0 - (double)k / e->Kmax);
   if (e->f32) build_tables<float>(*e, ts.data(), e->Kmax, s);
   else build_tables<bf16_t>(*e, ts.data(), e->Kmax, s);
+  HIPC(hipStreamSynchronize(s));
 }
 
 Bucket& get_bucket(phyai_expert& e, int B, int K) {
@@ -999,6 +1012,10 @@ int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len
     }
     for (int k = 0; k <= n_steps; ++k)
       if (!std::isfinite(timesteps[k])) fail(PHYAI_EINVAL, "non-finite timestep");
+    // the kernels move these buffers in 16-byte accesses
+    auto aligned16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+    if (!aligned16(prefix) || !aligned16(noise) || !aligned16(out_actions) || (e->c.state_token && !aligned16(state)))
+      fail(PHYAI_EINVAL, "prefix, noise, state and out_actions must be 16-byte aligned");
     hipStream_t s = static_cast<hipStream_t>(stream);
     const bool same = (int)e->ts_cached.size() >= n_steps + 1 &&
                       std::memcmp(e->ts_cached.data(), timesteps, (n_steps + 1) * 4) == 0;

@@ -47,6 +47,7 @@ def test_null_arguments_are_rejected():
 @pytest.mark.parametrize("field,value,needle", [
     ("head_dim", 96, b"head_dim"),
     ("d_model", 100, b"d_model"),
+    ("d_model", 320, b"multiple of 256"),       # the row kernels take whole 256-column groups
     ("action_dim", 65, b"action_dim"),
     ("max_batch", 513, b"max_batch"),
     ("n_kv_heads", 3, b"multiple"),

@@ -168,5 +168,12 @@ def test_invalid_arguments_leave_output_untouched():
         ex.denoise(prefix, case.prefix_len, noise, wl.default_timesteps(cfg.n_steps + 1), state, out=out)
     with pytest.raises(px.PhyaiError, match="non-finite"):
         ex.denoise(prefix, case.prefix_len, noise, np.float32([1.0, np.nan, 0.5, 0.0]), state, out=out)
+    # a contiguous view 4 bytes past a 16-byte boundary
+    shifted = torch.empty(noise.numel() + 1, dtype=noise.dtype, device=noise.device)[1:].view(noise.shape)
+    shifted.copy_(noise)
+    with pytest.raises(px.PhyaiError, match="16-byte aligned"):
+        ex.denoise(prefix, case.prefix_len, shifted, case.timesteps, state, out=out)
+    with pytest.raises(px.PhyaiError, match="16-byte aligned"):
+        ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=shifted)
     torch.cuda.synchronize()
     assert bool((out == 7.0).all())

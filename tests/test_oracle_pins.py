@@ -449,3 +449,15 @@ def test_wiring_probe_catches_planted_mistakes(mistake, monkeypatch):
     out = oracle.denoise(cfg, case.weights, case.prefix, case.prefix_len, case.noise, case.timesteps,
                          case.state, **kw)
     assert not np.allclose(out[0], expected, atol=1e-6)
+
+
+def test_single_precision_timing_mode_tracks_float64():
+    """The float32 mode (a CPU timing baseline only) runs the same steps: it
+    returns float32 and stays within float32 rounding of the reference."""
+    cfg = wl.CONFIGS["tiny_fp32"]
+    case = wl.make_case(cfg, seed=1)
+    ref = oracle.denoise(cfg, case.weights, case.prefix, case.prefix_len, case.noise, case.timesteps, case.state)
+    got = oracle.denoise(cfg, case.weights, case.prefix, case.prefix_len, case.noise, case.timesteps, case.state,
+                         dtype=np.float32)
+    assert got.dtype == np.float32 and ref.dtype == np.float64
+    assert np.abs(got - ref).max() < 1e-5
