@@ -176,6 +176,24 @@ int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len
                   const float* noise, const float* timesteps, int32_t n_steps, int32_t batch,
                   const float* state, float* out_actions, void* stream);
 
+/* phyai_denoise for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the same arguments, validation, kernels and results, with two differences.
+ * It never allocates (no hipMalloc, hipFree or allocating library routine):
+ * it launches the loop's kernels directly instead of capturing and
+ * instantiating a graph, and the scratch those kernels need between launches
+ * (split-K partial sums of the residual GEMMs, key-split attention partials)
+ * lives in a static device array of 32 MiB, one per device, held until the
+ * process ends.  A call that would need more (large batches with key-split
+ * attention) fails with PHYAI_EINVAL before anything is enqueued.  Every call
+ * on a device shares that device's array: calls that overlap on one device
+ * race, so they must be ordered (one stream, or streams the caller orders),
+ * whatever handle they use.  Nothing in the array needs to start at zero:
+ * each call writes every partial before reading it. */
+int phyai_denoise_static(phyai_expert* e, const void* prefix, const int32_t* prefix_len,
+                         const float* noise, const float* timesteps, int32_t n_steps, int32_t batch,
+                         const float* state, float* out_actions, void* stream);
+
 /* Capture the graph of the K-step loop for the (batch, n_steps) bucket ahead
  * of the first phyai_denoise with that shape, so that the first prediction
  * does not pay for the capture (the runner captures the full loop in the

@@ -21,7 +21,7 @@ _VARIANT = {"pi0": 0, "pi05": 1, "dit": 2}
 _DTYPE = {"f32": 0, "bf16": 1, "fp8": 2}
 
 # Every symbol include/phyai.h declares.
-EXPORTS = ("phyai_load_expert", "phyai_denoise", "phyai_prepare", "phyai_debug_hidden",
+EXPORTS = ("phyai_load_expert", "phyai_denoise", "phyai_denoise_static", "phyai_prepare", "phyai_debug_hidden",
            "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_free_expert", "phyai_last_error",
            "phyai_version")
 STAGES = {"norm1": 0, "qkv": 1, "attn": 2, "oproj": 3, "norm2": 4, "mlp_up": 5, "mlp_down": 6}
@@ -60,6 +60,7 @@ def lib() -> ctypes.CDLL:
         L.phyai_load_expert.argtypes = [ctypes.POINTER(Config), ctypes.POINTER(Tensor), i32, vp,
                                         ctypes.POINTER(vp)]
         L.phyai_denoise.argtypes = [vp, vp, vp, vp, vp, i32, i32, vp, vp, vp]
+        L.phyai_denoise_static.argtypes = [vp, vp, vp, vp, vp, i32, i32, vp, vp, vp]
         L.phyai_prepare.argtypes = [vp, i32, i32, vp]
         L.phyai_debug_hidden.argtypes = [vp, vp, i32, vp]
         L.phyai_fp8_to_bf16.argtypes = [vp, vp, i64, vp]
@@ -67,7 +68,7 @@ def lib() -> ctypes.CDLL:
         L.phyai_free_expert.argtypes = [vp]
         L.phyai_free_expert.restype = None
         L.phyai_last_error.restype = ctypes.c_char_p
-        for f in ("phyai_load_expert", "phyai_denoise", "phyai_prepare", "phyai_debug_hidden",
+        for f in ("phyai_load_expert", "phyai_denoise", "phyai_denoise_static", "phyai_prepare", "phyai_debug_hidden",
                   "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_version"):
             getattr(L, f).restype = ctypes.c_int
         _lib_handle = L
@@ -135,18 +136,23 @@ class Expert:
     def prepare(self, batch: int, n_steps: int, stream=None):
         _check(lib().phyai_prepare(self._h, batch, n_steps, _stream(stream)))
 
-    def denoise(self, prefix, prefix_len, noise, timesteps, state=None, out=None, stream=None):
-        """prefix, noise, state, out: device tensors; prefix_len, timesteps: host arrays."""
-        import torch
+    def denoise(self, prefix, prefix_len, noise, timesteps, state=None, out=None, stream=None,
+                static: bool = False):
+        """prefix, noise, state, out: device tensors; prefix_len, timesteps: host arrays.
+        static=True calls phyai_denoise_static (allocates nothing; `out` must then be given)."""
         plen = np.ascontiguousarray(prefix_len, dtype=np.int32)
         ts = np.ascontiguousarray(timesteps, dtype=np.float32)
         B = int(noise.shape[0])
         if plen.shape[0] < B:
             raise ValueError("prefix_len shorter than the batch")
         if out is None:
+            if static:
+                raise ValueError("the allocation-free entry point needs a caller-provided `out`")
+            import torch
             out = torch.empty_like(noise)
-        _check(lib().phyai_denoise(self._h, _ptr(prefix), plen.ctypes.data, _ptr(noise), ts.ctypes.data,
-                                   len(ts) - 1, B, _ptr(state), _ptr(out), _stream(stream)))
+        fn = lib().phyai_denoise_static if static else lib().phyai_denoise
+        _check(fn(self._h, _ptr(prefix), plen.ctypes.data, _ptr(noise), ts.ctypes.data,
+                  len(ts) - 1, B, _ptr(state), _ptr(out), _stream(stream)))
         return out
 
     def debug_hidden(self, batch: int, stream=None):

@@ -11,6 +11,7 @@
 #include <functional>
 #include <cstring>
 #include <map>
+#include <mutex>
 #include <stdexcept>
 #include <string>
 #include <utility>
@@ -110,6 +111,10 @@ struct phyai_expert {
   // per-layer key ranges: K [L][Bmax][nkv][ldk][D], V transposed [L][Bmax][nkv][D][ldk]
   void *kall = nullptr, *vt = nullptr;
   float* pend = nullptr;    // split-K partial sums of the residual GEMMs (small batches)
+  // the partial buffers the next enqueue uses: part/pend, or the static
+  // scratch for phyai_denoise_static
+  float *part_cur = nullptr, *pend_cur = nullptr;
+  float* static_scratch = nullptr;   // this device's copy of the static scratch array
   int ldk = 0;
   int64_t kv_layer = 0;     // elements per layer
   // two-term activations (hi + lo bf16) for the GEMMs fed by a norm or by GeGLU
@@ -140,6 +145,33 @@ struct phyai_expert {
 };
 
 namespace {
+
+// ---------------------------------------------------------------------------
+// Static scratch of phyai_denoise_static: the split-K and attention key-split
+// partials of one call, in a file-scope device array (32 MiB, one copy per
+// device, held until the process ends).  Host code never uses the array's
+// name as an address: its device address is looked up once per device with
+// that device current and kept in g_scratch.
+// ---------------------------------------------------------------------------
+constexpr int64_t kStaticScratchFloats = int64_t(8) << 20;
+constexpr int kMaxDevices = 64;
+__device__ __align__(256) float scratch[kStaticScratchFloats];
+std::mutex g_scratch_mu;
+float* g_scratch[kMaxDevices] = {};
+
+float* static_scratch_ptr() {
+  int dev = 0;
+  HIPC(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) fail(PHYAI_EUNSUPPORTED, "device index beyond the static scratch table");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    HIPC(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) fail(PHYAI_EHIP, "hipGetSymbolAddress(scratch) returned NULL");
+    g_scratch[dev] = static_cast<float*>(p);
+  }
+  return g_scratch[dev];
+}
 
 // ---------------------------------------------------------------------------
 // parameter lookup and packing
@@ -374,7 +406,7 @@ PendingResid pending_of(const phyai_expert& e, int which, int l, int k, int B) {
   PendingResid p{};
   const int S = resid_split(e, which, l, B);
   if (S <= 1) return p;
-  p.part = e.pend;
+  p.part = e.pend_cur;
   p.n = S;
   p.stride = (int64_t)B * e.M * e.d;
   if (e.c.variant == PHYAI_VARIANT_DIT) {
@@ -408,7 +440,7 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   auto with_split = [&](GemmArgs ga, int which) {
     const int sk = resid_split(e, which, l, B);
     if (sk > 1) {
-      ga.split_out = e.pend;
+      ga.split_out = e.pend_cur;
       ga.split_stride = (int64_t)R * d;
       ga.split_k = sk;
     }
@@ -422,7 +454,7 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   at.q = q; at.ldq = e.qd;
   at.K = kl; at.Vt = vl; at.ldk = e.ldk;
   at.out = o; at.ldo = e.qd;
-  at.part = e.part;
+  at.part = e.part_cur;
   at.desc = e.desc;
   at.B = B; at.M = M; at.nq = e.nq; at.nkv = e.nkv; at.D = D;
   at.scale = inv_sqrt_d;
@@ -883,6 +915,9 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
       }
     e->pend = e->mem.alloc_n<float>(pend);
   }
+  e->part_cur = e->part;
+  e->pend_cur = e->pend;
+  e->static_scratch = static_scratch_ptr();
   HIPC(hipStreamSynchronize(s));
   e->desc = static_cast<CallDesc*>(e->mem.alloc(sizeof(CallDesc)));
   // tables
@@ -934,6 +969,85 @@ Bucket& get_bucket(phyai_expert& e, int B, int K) {
 bool use_graphs() {
   const char* v = std::getenv("PHYAI_NO_GRAPH");
   return !(v && v[0] == '1');
+}
+
+}  // namespace
+
+namespace {
+
+// Host validation shared by the denoising entry points (nothing enqueued yet).
+void check_call(phyai_expert* e, const void* prefix, const int32_t* prefix_len, const float* noise,
+                const float* timesteps, int n_steps, int batch, const float* state, const float* out_actions) {
+  if (!e) fail(PHYAI_EINVAL, "NULL handle");
+  if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range 1..max_batch");
+  if (n_steps < 1 || n_steps > e->Kmax) fail(PHYAI_EINVAL, "n_steps out of range 1..max_steps");
+  if (!prefix_len || !noise || !timesteps || !out_actions) fail(PHYAI_EINVAL, "NULL argument");
+  if (!prefix && e->P > 0) fail(PHYAI_EINVAL, "NULL prefix");
+  if (e->c.state_token && !state) fail(PHYAI_EINVAL, "state is required when state_token = 1");
+  for (int b = 0; b < batch; ++b) {
+    if (prefix_len[b] < 0 || prefix_len[b] > e->P)
+      fail(PHYAI_EINVAL, "prefix_len[" + std::to_string(b) + "] = " + std::to_string(prefix_len[b]) +
+                             " outside 0..prefix_cap");
+    if (e->c.variant == PHYAI_VARIANT_DIT && prefix_len[b] < 1)
+      fail(PHYAI_EINVAL, "DiT requests need at least one feature row");
+  }
+  for (int k = 0; k <= n_steps; ++k)
+    if (!std::isfinite(timesteps[k])) fail(PHYAI_EINVAL, "non-finite timestep");
+  // the kernels move these buffers in 16-byte accesses
+  auto aligned16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+  if (!aligned16(prefix) || !aligned16(noise) || !aligned16(out_actions) || (e->c.state_token && !aligned16(state)))
+    fail(PHYAI_EINVAL, "prefix, noise, state and out_actions must be 16-byte aligned");
+}
+
+// Rebuild the schedule-keyed tables when the timesteps differ from the last call's.
+void refresh_tables(phyai_expert& e, const float* timesteps, int n_steps, hipStream_t s) {
+  const bool same = (int)e.ts_cached.size() >= n_steps + 1 &&
+                    std::memcmp(e.ts_cached.data(), timesteps, (n_steps + 1) * 4) == 0;
+  if (same) return;
+  if (e.f32) build_tables<float>(e, timesteps, n_steps, s);
+  else build_tables<bf16_t>(e, timesteps, n_steps, s);
+}
+
+void write_call_desc(phyai_expert& e, const void* prefix, const int32_t* prefix_len, const float* noise, int batch,
+                     const float* state, float* out_actions, hipStream_t s) {
+  CallDesc hd;
+  std::memset(&hd, 0, sizeof(hd));
+  hd.prefix = prefix;
+  hd.noise = noise;
+  hd.state = state;
+  hd.out = out_actions;
+  for (int b = 0; b < batch; ++b) hd.prefix_len[b] = prefix_len[b];
+  set_call_desc(hd, e.desc, s);
+  HIPC(hipGetLastError());
+  e.last_batch = batch;
+}
+
+int64_t round_up64(int64_t n) { return (n + 63) / 64 * 64; }
+
+// Attention key-split partial floats one call at batch B uses (the larger of
+// the two block heights, as the handle's own buffer is sized).
+int64_t attn_part_floats(const phyai_expert& e, int B) {
+  if (e.f32) return 0;
+  const int rows = e.M * (e.nq / e.nkv);
+  const int keys_main = e.c.variant == PHYAI_VARIANT_DIT ? e.M : e.P + e.M;
+  int64_t need = attention_partial_floats(B, e.M, e.nq, e.nkv, e.D, attn_splits_max(B, rows, e.nkv, keys_main));
+  if (e.c.variant == PHYAI_VARIANT_DIT)
+    need = std::max(need, attention_partial_floats(B, e.M, e.nq, e.nkv, e.D, attn_splits_max(B, rows, e.nkv, e.P)));
+  return need;
+}
+
+// Split-K partial floats of the residual GEMMs at batch B (either O-projection form).
+int64_t pend_floats(const phyai_expert& e, int B) {
+  if (e.f32) return 0;
+  const int R = B * e.M;
+  int64_t need = 0;
+  for (int l = 0; l < e.L; ++l)
+    for (int which = 0; which < 2; ++which) {
+      const Lin& w = which == 0 ? e.layers[l].o : e.layers[l].down;
+      const int sk = std::max(resid_split(e, which, l, B), gemm_split_k(R, w.NPT, w.K));
+      if (sk > 1) need = std::max(need, (int64_t)sk * R * e.d);
+    }
+  return need;
 }
 
 }  // namespace
@@ -997,43 +1111,11 @@ int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len
                   const float* timesteps, int32_t n_steps, int32_t batch, const float* state, float* out_actions,
                   void* stream) {
   return run_guarded([&] {
-    if (!e) fail(PHYAI_EINVAL, "NULL handle");
-    if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range 1..max_batch");
-    if (n_steps < 1 || n_steps > e->Kmax) fail(PHYAI_EINVAL, "n_steps out of range 1..max_steps");
-    if (!prefix_len || !noise || !timesteps || !out_actions) fail(PHYAI_EINVAL, "NULL argument");
-    if (!prefix && e->P > 0) fail(PHYAI_EINVAL, "NULL prefix");
-    if (e->c.state_token && !state) fail(PHYAI_EINVAL, "state is required when state_token = 1");
-    for (int b = 0; b < batch; ++b) {
-      if (prefix_len[b] < 0 || prefix_len[b] > e->P)
-        fail(PHYAI_EINVAL, "prefix_len[" + std::to_string(b) + "] = " + std::to_string(prefix_len[b]) +
-                               " outside 0..prefix_cap");
-      if (e->c.variant == PHYAI_VARIANT_DIT && prefix_len[b] < 1)
-        fail(PHYAI_EINVAL, "DiT requests need at least one feature row");
-    }
-    for (int k = 0; k <= n_steps; ++k)
-      if (!std::isfinite(timesteps[k])) fail(PHYAI_EINVAL, "non-finite timestep");
-    // the kernels move these buffers in 16-byte accesses
-    auto aligned16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
-    if (!aligned16(prefix) || !aligned16(noise) || !aligned16(out_actions) || (e->c.state_token && !aligned16(state)))
-      fail(PHYAI_EINVAL, "prefix, noise, state and out_actions must be 16-byte aligned");
+    check_call(e, prefix, prefix_len, noise, timesteps, n_steps, batch, state, out_actions);
     hipStream_t s = static_cast<hipStream_t>(stream);
-    const bool same = (int)e->ts_cached.size() >= n_steps + 1 &&
-                      std::memcmp(e->ts_cached.data(), timesteps, (n_steps + 1) * 4) == 0;
-    if (!same) {
-      if (e->f32) build_tables<float>(*e, timesteps, n_steps, s);
-      else build_tables<bf16_t>(*e, timesteps, n_steps, s);
-    }
+    refresh_tables(*e, timesteps, n_steps, s);
     Bucket* bk = use_graphs() ? &get_bucket(*e, batch, n_steps) : nullptr;
-    CallDesc hd;
-    std::memset(&hd, 0, sizeof(hd));
-    hd.prefix = prefix;
-    hd.noise = noise;
-    hd.state = state;
-    hd.out = out_actions;
-    for (int b = 0; b < batch; ++b) hd.prefix_len[b] = prefix_len[b];
-    set_call_desc(hd, e->desc, s);
-    HIPC(hipGetLastError());
-    e->last_batch = batch;
+    write_call_desc(*e, prefix, prefix_len, noise, batch, state, out_actions, s);
     if (bk) {
       HIPC(hipGraphLaunch(bk->exec, s));
     } else {
@@ -1041,6 +1123,37 @@ int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len
       else enqueue_loop<bf16_t>(*e, batch, n_steps, s);
       HIPC(hipGetLastError());
     }
+  });
+}
+
+int phyai_denoise_static(phyai_expert* e, const void* prefix, const int32_t* prefix_len, const float* noise,
+                         const float* timesteps, int32_t n_steps, int32_t batch, const float* state,
+                         float* out_actions, void* stream) {
+  return run_guarded([&] {
+    check_call(e, prefix, prefix_len, noise, timesteps, n_steps, batch, state, out_actions);
+    const int64_t part = round_up64(attn_part_floats(*e, batch));
+    const int64_t need = part + pend_floats(*e, batch);
+    if (need > kStaticScratchFloats)
+      fail(PHYAI_EINVAL, "this batch needs " + std::to_string(need * 4) + " bytes of scratch; the static limit is " +
+                             std::to_string(kStaticScratchFloats * 4));
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    refresh_tables(*e, timesteps, n_steps, s);
+    write_call_desc(*e, prefix, prefix_len, noise, batch, state, out_actions, s);
+    // eager launches (no graph: instantiating one allocates), partials in the
+    // device's static scratch; the handle's own buffers are restored after
+    e->part_cur = e->static_scratch;
+    e->pend_cur = e->static_scratch + part;
+    try {
+      if (e->f32) enqueue_loop<float>(*e, batch, n_steps, s);
+      else enqueue_loop<bf16_t>(*e, batch, n_steps, s);
+    } catch (...) {
+      e->part_cur = e->part;
+      e->pend_cur = e->pend;
+      throw;
+    }
+    e->part_cur = e->part;
+    e->pend_cur = e->pend;
+    HIPC(hipGetLastError());
   });
 }
 
