@@ -520,4 +520,62 @@ void set_call_desc(const CallDesc& host_desc, CallDesc* dev, hipStream_t);
 void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B, int M, int D, hipStream_t);
 void fp8_to_bf16(const uint8_t* codes, bf16_t* out, int64_t n, hipStream_t);
 
+// ---------------------------------------------------------------------------
+// Persistent batch-1 loop: one cooperative launch runs all K Euler steps of
+// one pi0 request (bf16 weights, one KV head, at most 64 suffix tokens).
+// Blocks hand activations to each other through write-through device-scope
+// stores and a grid barrier.  Data rewritten within a launch (the residual,
+// partials, the suffix keys) is read back with device-scope loads; the GEMM
+// operands get a fresh copy per step and site, written once per launch, so
+// their readers use plain cached loads (a launch starts with the L2s
+// invalidated).  Residual split-K partials are reduced by the last block to
+// finish each column tile; every norm is folded into the GEMM that consumes
+// it (the producer leaves bf16(h (1 + w)) and per-tile sums of squares, the
+// consumer scales its rows by 1/rms).
+// ---------------------------------------------------------------------------
+struct PersistLayer {
+  const void* qkv; const void* o; const void* gu; const void* down;   // packed bf16 weights
+  const float* attn_norm; const float* mlp_norm;                      // RMSNorm gains w ((1 + w))
+};
+
+struct PersistArgs {
+  const CallDesc* desc;
+  const PersistLayer* layer;   // device array [L]
+  int L, d, D, nq, F, H, A, M, off;
+  int ldk;
+  int64_t kv_layer;            // elements per layer of the key ranges
+  bf16_t* kall; bf16_t* vt;    // key ranges: K [L][ldk][D], V^T [L][D][ldk] (prefix relaid before launch)
+  float* h;                    // residual stream [64][d]
+  // per-step copies, r = the step's place in the launch (< kPersistRing)
+  bf16_t* a;                   // bf16(h (1 + w)) per norm site [R][L+1][2][64][d]
+  float* ss;                   // sums of h^2 per 32-column tile [R][L+1][2][64][d/32]
+  bf16_t* z;                   // time-MLP hidden [R][64][d]
+  bf16_t* q;                   // queries [R][L][64][nq*D]
+  bf16_t* o;                   // merged attention output [R][L][64][nq*D]
+  bf16_t* g;                   // GeGLU output [R][L][64][F]
+  bf16_t* apart;               // key-split attention partials [nq][ntile][64][D] (normalised)
+  float2* aml;                 // (max, sum) of each partial row [nq][ntile][64] (log2 domain)
+  float* part;                 // residual split-K partials [16][64][d]
+  float* x;                    // solver state [H][A]
+  const float* e_state;        // state-token embedding [d] (or null)
+  const float* tin_w; const float* tin_b;   // action embedding folded into the time MLP [A][d], [d]
+  const float* T;              // time-MLP tau half per step [K][d]
+  const void* time_w2; const float* time_b2;
+  const float* out_w;          // [A][d] (transposed)
+  const float* out_b; const float* final_norm; const float* dt;
+  const float2* rope_cs;       // [M][D/2] or null
+  float eps, scale;
+  unsigned* ctr;               // barrier and tile counters, zero at launch
+};
+
+// Whether the persistent loop takes this shape (see the launcher).
+bool persist_supported(int d, int D, int nq, int F, int M, int A);
+// Launch it for steps k0 .. k1 - 1 (k1 - k0 <= kPersistRing) of a K-step
+// schedule, with the arguments at dev_args (device memory holding a copy of
+// `a`, which the launcher reads for the shape).  The counters must be zero.
+// Cooperative: fails with the HIP error if the grid cannot be co-resident.
+hipError_t persist_launch(const PersistArgs& a, const PersistArgs* dev_args, int k0, int k1, int K, hipStream_t);
+constexpr int kPersistCounters = 1024;
+constexpr int kPersistRing = 16;   // steps per launch (per-step copies held)
+
 }  // namespace phyai

@@ -115,6 +115,11 @@ struct phyai_expert {
   // scratch for phyai_denoise_static
   float *part_cur = nullptr, *pend_cur = nullptr;
   float* static_scratch = nullptr;   // this device's copy of the static scratch array
+  // persistent batch-1 loop (pi0, bf16; opt-in): its argument block in device
+  // memory and own buffers, set up on first use
+  bool persist_ok = false, persist_ready = false;
+  PersistArgs pargs{};
+  PersistArgs* pargs_dev = nullptr;
   int ldk = 0;
   int64_t kv_layer = 0;     // elements per layer
   // two-term activations (hi + lo bf16) for the GEMMs fed by a norm or by GeGLU
@@ -541,11 +546,13 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   }
 }
 
+// Per-call work before the step loop: solver state from the noise, RoPE
+// table of the call's positions, state-token embedding, the prefix K/V into
+// the key ranges (DiT: the cross-attention K/V projection of the features).
 template <typename T>
-void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
+void enqueue_prologue(phyai_expert& e, int B, hipStream_t s) {
   const int d = e.d, M = e.M, H = e.H, L = e.L;
   const int variant = e.c.variant;
-
   copy_noise_to_state(e.desc, e.x, (int64_t)B * H * e.A, s);
   if (e.c.rope) rope_table(e.desc, e.inv_freq, e.rope_cs, B, M, e.D, s);
   if (e.c.state_token) embed_state(e.desc, e.state_w, e.state_b, e.e_state, B, e.A, d, s);
@@ -565,6 +572,13 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
     RelayoutArgs ra{e.desc, e.kall, e.vt, e.kv_layer, e.ldk, L, B, e.P, e.nkv, e.D, M};
     prefix_relayout(ra, static_cast<T*>(nullptr), s);
   }
+}
+
+template <typename T>
+void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
+  const int d = e.d, M = e.M, H = e.H, L = e.L;
+  const int variant = e.c.variant;
+  enqueue_prologue<T>(e, B, s);
 
   // the action-token embedding of step k (state rows of h reset too)
   auto embed_args = [&](int k) {
@@ -690,6 +704,90 @@ void build_tables(phyai_expert& e, const float* ts, int K, hipStream_t s) {
   }
   HIPC(hipGetLastError());
   e.ts_cached.assign(ts, ts + K + 1);
+}
+
+// Whether the persistent batch-1 loop takes this handle's shape (pi0, bf16
+// weights, one KV head, at most 64 suffix tokens; decided at load).
+bool persist_eligible(const phyai_expert& e) {
+  const phyai_config& c = e.c;
+  const int ntile_max = (e.P + e.M + 63) / 64;       // one attention block per key tile and head
+  return c.variant == PHYAI_VARIANT_PI0 && c.weight_dtype == PHYAI_DTYPE_BF16 && e.nkv == 1 &&
+         persist_supported(e.d, e.D, e.nq, e.F, e.M, e.A) && e.nq * ntile_max <= 256;
+}
+
+// Its buffers and argument block, on the first call that takes it.
+void setup_persist(phyai_expert& e, hipStream_t s) {
+  const phyai_config& c = e.c;
+  const int ntile_max = (e.P + e.M + 63) / 64;
+  const int d = e.d, L = e.L, D = e.D;
+  PersistArgs& p = e.pargs;
+  p = PersistArgs{};
+  p.desc = e.desc;
+  std::vector<PersistLayer> lt(L);
+  for (int l = 0; l < L; ++l)
+    lt[l] = PersistLayer{e.layers[l].qkv.w, e.layers[l].o.w, e.layers[l].gu.w, e.layers[l].down.w,
+                         e.layers[l].attn_norm, e.layers[l].mlp_norm};
+  PersistLayer* ltd = e.mem.alloc_n<PersistLayer>(L);
+  HIPC(hipMemcpyAsync(ltd, lt.data(), L * sizeof(PersistLayer), hipMemcpyHostToDevice, s));
+  p.layer = ltd;
+  p.L = L; p.d = d; p.D = D; p.nq = e.nq; p.F = e.F; p.H = e.H; p.A = e.A; p.M = e.M; p.off = e.off;
+  p.ldk = e.ldk;
+  p.kv_layer = e.kv_layer;
+  p.kall = static_cast<bf16_t*>(e.kall);
+  p.vt = static_cast<bf16_t*>(e.vt);
+  p.h = e.h;
+  // per-step copies for up to R steps per launch, zeroed once (rows past M
+  // are read as GEMM rows and never written)
+  const size_t R = (size_t)std::min(e.Kmax, kPersistRing);
+  auto zeroed = [&](size_t bytes) {
+    void* q = e.mem.alloc(bytes);
+    HIPC(hipMemsetAsync(q, 0, bytes, s));
+    return q;
+  };
+  const size_t sites = R * (L + 1) * 2;
+  p.a = static_cast<bf16_t*>(zeroed(sites * 64 * d * 2));
+  p.ss = static_cast<float*>(zeroed(sites * 64 * (d / 32) * 4));
+  p.z = static_cast<bf16_t*>(zeroed(R * 64 * d * 2));
+  p.q = static_cast<bf16_t*>(zeroed(R * L * 64 * e.nq * D * 2));
+  p.o = static_cast<bf16_t*>(zeroed(R * L * 64 * e.nq * D * 2));
+  p.g = static_cast<bf16_t*>(zeroed(R * L * 64 * e.F * 2));
+  p.apart = static_cast<bf16_t*>(e.mem.alloc((size_t)e.nq * ntile_max * 64 * D * 2));
+  p.aml = static_cast<float2*>(e.mem.alloc((size_t)e.nq * ntile_max * 64 * sizeof(float2)));
+  p.part = e.mem.alloc_n<float>((size_t)16 * 64 * d);
+  p.x = e.x;
+  p.e_state = c.state_token ? e.e_state : nullptr;
+  p.tin_w = e.tin_w;
+  p.tin_b = e.tin_b;
+  p.T = e.T;
+  p.time_w2 = e.time_w2.w;
+  p.time_b2 = e.time_b2;
+  p.out_w = e.out_w;
+  p.out_b = e.out_b;
+  p.final_norm = e.final_norm;
+  p.dt = e.dt;
+  p.rope_cs = c.rope ? e.rope_cs : nullptr;
+  p.eps = c.rms_eps;
+  p.scale = 1.0f / std::sqrt((float)D);
+  p.ctr = static_cast<unsigned*>(e.mem.alloc(kPersistCounters * 4));
+  e.pargs_dev = static_cast<PersistArgs*>(e.mem.alloc(sizeof(PersistArgs)));
+  HIPC(hipMemcpyAsync(e.pargs_dev, &p, sizeof(PersistArgs), hipMemcpyHostToDevice, s));
+}
+
+// The persistent loop is opt-in (PHYAI_PERSIST=1): on MI355X it measures
+// slower than the captured per-kernel graph at the pi0 shape.
+bool use_persist() {
+  const char* v = std::getenv("PHYAI_PERSIST");
+  return v && v[0] == '1';
+}
+
+// The whole K-step loop of one request in one cooperative launch (after the
+// per-call prologue kernels).
+void enqueue_persist(phyai_expert& e, int K, hipStream_t s) {
+  enqueue_prologue<bf16_t>(e, 1, s);
+  for (int k0 = 0; k0 < K; k0 += kPersistRing) {
+    HIPC(hipMemsetAsync(e.pargs.ctr, 0, kPersistCounters * 4, s));
+    HIPC(persist_launch(e.pargs, e.pargs_dev, k0, std::min(K, k0 + kPersistRing), K, s));
+  }
 }
 
 void check_config(const phyai_config& c) {
@@ -939,6 +1037,7 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
   for (int k = 0; k <= e->Kmax; ++k) ts[k] = (float)(1.0 - (double)k / e->Kmax);
   if (e->f32) build_tables<float>(*e, ts.data(), e->Kmax, s);
   else build_tables<bf16_t>(*e, ts.data(), e->Kmax, s);
+  e->persist_ok = persist_eligible(*e);
   HIPC(hipStreamSynchronize(s));
 }
 
@@ -1114,6 +1213,16 @@ int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len
     check_call(e, prefix, prefix_len, noise, timesteps, n_steps, batch, state, out_actions);
     hipStream_t s = static_cast<hipStream_t>(stream);
     refresh_tables(*e, timesteps, n_steps, s);
+    if (e->persist_ok && batch == 1 && use_persist()) {
+      if (!e->persist_ready) {
+        setup_persist(*e, s);
+        HIPC(hipStreamSynchronize(s));
+        e->persist_ready = true;
+      }
+      write_call_desc(*e, prefix, prefix_len, noise, batch, state, out_actions, s);
+      enqueue_persist(*e, n_steps, s);
+      return;
+    }
     Bucket* bk = use_graphs() ? &get_bucket(*e, batch, n_steps) : nullptr;
     write_call_desc(*e, prefix, prefix_len, noise, batch, state, out_actions, s);
     if (bk) {
