@@ -10,13 +10,14 @@ paper), which is stated there.
 """
 from .expert import (DecodedWeights, denoise, pi05_condition, velocity_dit, velocity_pi0,
                      velocity_pi05)
-from .numerics import (E4M3FN_TABLE, attention, attention_bruteforce, decode_bf16, decode_fp8,
-                       decode_stored, euler, gelu_tanh, layer_normalize, rms_normalize, rope,
+from .numerics import (E2M1_TABLE, E4M3FN_TABLE, attention, attention_bruteforce, decode_bf16,
+                       decode_fp4, decode_fp8, decode_stored, euler, gelu_tanh, layer_normalize, rms_normalize, rope,
                        sinusoid, swish)
 
 __all__ = [
     "DecodedWeights", "denoise", "pi05_condition", "velocity_dit", "velocity_pi0", "velocity_pi05",
-    "E4M3FN_TABLE", "attention", "attention_bruteforce", "decode_bf16", "decode_fp8",
+    "E2M1_TABLE", "E4M3FN_TABLE", "attention", "attention_bruteforce", "decode_bf16", "decode_fp4",
+    "decode_fp8",
     "decode_stored", "euler", "gelu_tanh", "layer_normalize", "rms_normalize", "rope", "sinusoid",
     "swish",
 ]

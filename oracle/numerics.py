@@ -55,6 +55,34 @@ def decode_fp8(codes: np.ndarray, scale: np.ndarray) -> np.ndarray:
     return E4M3FN_TABLE[np.asarray(codes, dtype=np.uint8)] * np.asarray(scale, np.float64)[None, :]
 
 
+def _e2m1_value(code: int) -> float:
+    """Value of one OCP FP4 E2M1 code: 1 sign, 2 exponent (bias 1), 1 mantissa
+    bit; exponent field 0 is subnormal (m/2); no infinities or NaN."""
+    s = -1.0 if code & 0x8 else 1.0
+    e = (code >> 1) & 0x3
+    m = code & 0x1
+    if e == 0:
+        return s * m / 2.0
+    return s * (1.0 + m / 2.0) * 2.0 ** (e - 1)
+
+
+E2M1_TABLE = np.array([_e2m1_value(c) for c in range(16)], dtype=np.float64)
+FP4_GROUP = 32
+
+
+def decode_fp4(packed: np.ndarray, scale: np.ndarray) -> np.ndarray:
+    """4-bit weights (paragraph "Quantization", W4A16): byte (i, j) of `packed`
+    holds the codes of columns 2j (low nibble) and 2j + 1 (high nibble) of row
+    i; W_ij = value(code_ij) * scale[i / 32][j]."""
+    packed = np.asarray(packed, dtype=np.uint8)
+    rows = packed.shape[0]
+    codes = np.empty((rows, packed.shape[1] * 2), dtype=np.uint8)
+    codes[:, 0::2] = packed & 0xF
+    codes[:, 1::2] = packed >> 4
+    sc = np.repeat(np.asarray(scale, np.float64), FP4_GROUP, axis=0)
+    return E2M1_TABLE[codes] * sc
+
+
 def decode_stored(t) -> np.ndarray:
     """Decode a stored tensor (dtype, data[, scale]) to float64."""
     if t.dtype == "f32":
@@ -63,6 +91,8 @@ def decode_stored(t) -> np.ndarray:
         return decode_bf16(t.data)
     if t.dtype == "fp8":
         return decode_fp8(t.data, t.scale)
+    if t.dtype == "fp4":
+        return decode_fp4(t.data, t.scale)
     raise ValueError(f"unknown storage dtype {t.dtype!r}")
 
 

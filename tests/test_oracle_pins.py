@@ -74,6 +74,70 @@ def test_e4m3fn_encode_saturates():
     assert onum.E4M3FN_TABLE[wl.e4m3fn_encode(np.array([1e6, -500.0, 449.0]))].tolist() == [448.0, -448.0, 448.0]
 
 
+# OCP Microscaling Formats spec, FP4 E2M1 element values for codes 0..7
+# (the sign is bit 3): 0, 0.5, 1, 1.5, 2, 3, 4, 6.
+OCP_E2M1_POSITIVE = [0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0]
+
+
+def test_e2m1_table_matches_the_ocp_values():
+    assert onum.E2M1_TABLE[:8].tolist() == OCP_E2M1_POSITIVE
+    assert onum.E2M1_TABLE[8:].tolist() == [-v for v in OCP_E2M1_POSITIVE]
+    assert math.copysign(1, onum.E2M1_TABLE[8]) < 0
+
+
+def test_e2m1_encode_round_trip_and_ties_to_even():
+    codes = np.arange(16, dtype=np.uint8)
+    back = wl.e2m1_encode(onum.E2M1_TABLE[codes])
+    assert np.array_equal(onum.E2M1_TABLE[back], onum.E2M1_TABLE[codes])
+    # midpoints between neighbours round to the neighbour with an even mantissa bit
+    pos = np.array(OCP_E2M1_POSITIVE)
+    mids = (pos[1:] + pos[:-1]) / 2          # 0.25 0.75 1.25 1.75 2.5 3.5 5
+    want = [0.0, 1.0, 1.0, 2.0, 2.0, 4.0, 4.0]
+    assert onum.E2M1_TABLE[wl.e2m1_encode(mids)].tolist() == want
+    assert onum.E2M1_TABLE[wl.e2m1_encode(-mids)].tolist() == [-v for v in want]
+    # everywhere else: the nearest grid value
+    v = np.random.default_rng(3).uniform(-6, 6, 100000)
+    got = onum.E2M1_TABLE[wl.e2m1_encode(v)]
+    grid = np.concatenate([-pos[::-1], pos])
+    nearest = np.abs(v[:, None] - grid[None, :]).min(axis=1)
+    assert np.allclose(np.abs(got - v), nearest, rtol=0, atol=1e-12)
+
+
+def test_fp4_quantizer_groups_scales_and_packing():
+    g = np.random.default_rng(4)
+    w = (g.standard_normal((96, 10)) * 0.02).astype(np.float32)
+    w[32:64, 3] = 0.0                        # an all-zero group
+    w[0, 7] = 0.75                            # amax exactly 6 * 2^-3
+    packed, scale = wl.quantize_fp4_groups(w)
+    assert packed.shape == (96, 5) and scale.shape == (3, 10)
+    # scales are powers of two, the smallest with amax <= 6 * scale
+    amax = np.abs(w.reshape(3, 32, 10)).max(axis=1)
+    assert np.all(np.frexp(scale)[0] == 0.5)
+    assert np.all(amax <= 6 * scale)
+    assert np.all((amax > 3 * scale) | (amax == 0))
+    assert scale[1, 3] == 1.0 and scale[0, 7] == 0.125
+    # unpacking: low nibble is the even column
+    codes = np.empty((96, 10), np.uint8)
+    codes[:, 0::2] = packed & 15
+    codes[:, 1::2] = packed >> 4
+    dec = onum.decode_fp4(packed, scale)
+    assert np.array_equal(dec, onum.E2M1_TABLE[codes] * np.repeat(scale, 32, axis=0))
+    # round to nearest: the error is at most half a quantum of the code's binade
+    r = w / np.repeat(scale, 32, axis=0)
+    q = np.where(np.abs(r) < 2, 0.5, np.where(np.abs(r) < 4, 1.0, 2.0))
+    assert np.all(np.abs(dec - w) <= q / 2 * np.repeat(scale, 32, axis=0) + 1e-12)
+
+
+def test_fp4_decode_hand_example():
+    # two rows x four columns; row 0 codes [1, 15, 7, 8], row 1 codes [4, 0, 11, 6]
+    packed = np.array([[0xF1, 0x87], [0x04, 0x6B]], dtype=np.uint8)
+    scale = np.array([[0.5, 2.0, 1.0, 0.25]], dtype=np.float32)
+    packed = np.repeat(packed, 16, axis=0)    # one 32-row group
+    dec = onum.decode_fp4(packed, scale)
+    assert dec[0].tolist() == [0.5 * 0.5, -6.0 * 2.0, 6.0 * 1.0, -0.0 * 0.25]
+    assert dec[16].tolist() == [2.0 * 0.5, 0.0 * 2.0, -1.5 * 1.0, 4.0 * 0.25]
+
+
 def test_fp8_quantizer_scale_and_error():
     g = np.random.default_rng(2)
     w = (g.standard_normal((64, 48)) * 0.02).astype(np.float32)

@@ -13,6 +13,12 @@ Storage formats produced here (what the library and the oracle consume):
                column (round-to-nearest weight quantisation, as in the
                paper's offline RTN quantiser, Section "Optimization Methods",
                paragraph "Quantization").
+  * ``fp4``  -- 4-bit weights (the paper's W4A16): OCP e2m1 codes, two per
+               byte along the output dimension (even column in the low
+               nibble), with one power-of-two float32 scale per group of 32
+               input rows and output column, chosen so that no code
+               saturates; codes are the round-to-nearest (ties to even)
+               e2m1 values of W / scale.
 
 Linear weights are stored ``[in][out]`` (``y = x @ W + b``).
 """
@@ -28,7 +34,7 @@ __all__ = [
     "ExpertConfig", "CONFIGS", "StoredTensor", "weight_specs", "make_weights",
     "make_prefix", "make_prefix_lengths", "make_noise", "make_state",
     "default_timesteps", "make_case", "bf16_bits_from_f32", "e4m3fn_encode",
-    "quantize_fp8_per_column", "TRUNK_LINEARS",
+    "quantize_fp8_per_column", "e2m1_encode", "quantize_fp4_groups", "FP4_GROUP", "TRUNK_LINEARS",
 ]
 
 
@@ -58,7 +64,7 @@ class ExpertConfig:
     batch: int
     state_token: bool
     rope: bool
-    weight_dtype: str         # f32 | bf16 | fp8
+    weight_dtype: str         # f32 | bf16 | fp8 | fp4
     kv_dtype: str             # f32 | bf16
     d_feat: int = 0           # DiT: width of the VLM feature tokens
     time_dim: int = 0         # width of the sinusoidal timestep embedding
@@ -93,7 +99,8 @@ def _cfg(**kw) -> ExpertConfig:
 
 # The five workloads: a tiny fp32 expert, the pi0-shaped expert at batch 1,
 # the pi0.5-shaped expert (adaRMSNorm), a DiT-style action head, and the
-# pi0-shaped expert at rollout batch 64 with ragged prefixes and fp8 weights.
+# pi0-shaped expert at rollout batch 64 with ragged prefixes and fp8 weights;
+# plus the batch-1 pi0 shape with 4-bit weights.
 CONFIGS: Dict[str, ExpertConfig] = {
     "tiny_fp32": _cfg(
         name="tiny_fp32", cfg_id=1, variant="pi0", n_layers=2, d_model=256,
@@ -121,17 +128,24 @@ CONFIGS: Dict[str, ExpertConfig] = {
         n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=4096, horizon=50,
         action_dim=32, n_steps=10, prefix_cap=1000, prefix_min=600, prefix_max=1000,
         batch=64, state_token=True, rope=True, weight_dtype="fp8", kv_dtype="bf16"),
+    # the pi0-shaped expert at batch 1 with 4-bit weights (the paper's W4A16
+    # quantised path): the trunk linears in fp4, everything else as C2
+    "pi0_fp4_b1": _cfg(
+        name="pi0_fp4_b1", cfg_id=6, variant="pi0", n_layers=18, d_model=1024,
+        n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=4096, horizon=50,
+        action_dim=32, n_steps=10, prefix_cap=816, prefix_min=816, prefix_max=816,
+        batch=1, state_token=True, rope=True, weight_dtype="fp4", kv_dtype="bf16"),
 }
 
-# Per-layer linears that carry the fp8 format when weight_dtype == "fp8".
-TRUNK_LINEARS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down")
+# Per-layer linears that carry the fp8 / fp4 format when weight_dtype is one of those.
+TRUNK_LINEARS = ("wq", "wk", "wv", "wo", "w_gate", "w_up", "w_down", "mlp_w1", "mlp_w2")
 
 
 @dataclasses.dataclass
 class StoredTensor:
-    dtype: str                 # f32 | bf16 | fp8
-    data: np.ndarray           # float32 | uint16 | uint8, shape [rows][cols]
-    scale: Optional[np.ndarray] = None   # fp8: float32 [cols]
+    dtype: str                 # f32 | bf16 | fp8 | fp4
+    data: np.ndarray           # float32 | uint16 | uint8, shape [rows][cols] (fp4: [rows][cols / 2])
+    scale: Optional[np.ndarray] = None   # fp8: float32 [cols]; fp4: float32 [rows / 32][cols]
 
     @property
     def rows(self) -> int:
@@ -139,7 +153,7 @@ class StoredTensor:
 
     @property
     def cols(self) -> int:
-        return int(self.data.shape[1])
+        return int(self.data.shape[1]) * (2 if self.dtype == "fp4" else 1)
 
 
 # ----------------------------------------------------------------------------
@@ -187,6 +201,54 @@ def quantize_fp8_per_column(w: np.ndarray):
     scale = np.where(amax > 0, amax / np.float32(448.0), np.float32(1.0)).astype(np.float32)
     codes = e4m3fn_encode(w / scale[None, :])
     return codes, scale
+
+
+FP4_GROUP = 32          # input rows sharing one fp4 scale
+
+
+def e2m1_encode(v: np.ndarray) -> np.ndarray:
+    """Encode float values (|v| <= 6) as OCP e2m1 codes, round to nearest with
+    ties to even.  The non-negative values are the multiples of 0.5 up to 2,
+    of 1 up to 4 and 6 (codes 0..7: 0, 0.5, 1, 1.5, 2, 3, 4, 6); the sign is
+    bit 3.  With a = |v| the quantum is 0.5 below 2, 1 in [2, 4) and 2 in
+    [4, 6], so a / quantum rounded to even gives the value, and the code
+    follows from the value by the ordering above."""
+    v = np.asarray(v, dtype=np.float64)
+    a = np.abs(v)
+    q = np.where(a < 2.0, 0.5, np.where(a < 4.0, 1.0, 2.0))
+    val = np.rint(a / q) * q                      # numpy rint rounds ties to even
+    # rounding up across a binade boundary lands on the boundary value, which
+    # the table below holds
+    table = np.array([0.0, 0.5, 1.0, 1.5, 2.0, 3.0, 4.0, 6.0])
+    code = np.searchsorted(table, val).astype(np.uint8)
+    assert np.all(table[code] == val), "value outside the e2m1 grid"
+    return (code | (np.signbit(v).astype(np.uint8) << 3)).astype(np.uint8)
+
+
+def quantize_fp4_groups(w: np.ndarray):
+    """Round-to-nearest 4-bit weight quantisation (W4A16): for each group of
+    FP4_GROUP input rows and each output column, scale = 2^ceil(log2(amax / 6))
+    (1 for an all-zero group), so |W / scale| <= 6 and no code saturates; the
+    codes are the e2m1 encodings of W / scale.  Returns (packed codes uint8
+    [rows][cols / 2], even column in the low nibble; scales float32
+    [rows / FP4_GROUP][cols])."""
+    w = np.asarray(w, dtype=np.float32)
+    rows, cols = w.shape
+    assert rows % FP4_GROUP == 0 and cols % 2 == 0
+    g = w.reshape(rows // FP4_GROUP, FP4_GROUP, cols)
+    amax = np.abs(g).max(axis=1).astype(np.float64)
+    e = np.where(amax > 0, np.ceil(np.log2(np.where(amax > 0, amax, 1.0) / 6.0)), 0.0)
+    scale = np.ldexp(1.0, e.astype(np.int32)).astype(np.float32)
+    # an amax just above a power of two times 6 can round log2 down: bump the
+    # exponent until the group fits
+    while True:
+        over = amax > 6.0 * scale.astype(np.float64)
+        if not over.any():
+            break
+        scale = np.where(over, scale * np.float32(2.0), scale).astype(np.float32)
+    codes = e2m1_encode(g / scale[:, None, :].astype(np.float64)).reshape(rows, cols)
+    packed = (codes[:, 0::2] | (codes[:, 1::2] << 4)).astype(np.uint8)
+    return packed, scale
 
 
 # ----------------------------------------------------------------------------
@@ -262,9 +324,9 @@ def weight_specs(cfg: ExpertConfig) -> Dict[str, tuple]:
 
 
 def storage_dtype(cfg: ExpertConfig, name: str) -> str:
-    if cfg.weight_dtype == "fp8":
+    if cfg.weight_dtype in ("fp8", "fp4"):
         leaf = name.rsplit(".", 1)[-1]
-        return "fp8" if (name.startswith("layers.") and leaf in TRUNK_LINEARS) else "bf16"
+        return cfg.weight_dtype if (name.startswith("layers.") and leaf in TRUNK_LINEARS) else "bf16"
     return cfg.weight_dtype
 
 
@@ -277,6 +339,9 @@ def _store(x: np.ndarray, dtype: str) -> StoredTensor:
         return StoredTensor("f32", np.ascontiguousarray(x, dtype=np.float32))
     if dtype == "bf16":
         return StoredTensor("bf16", bf16_bits_from_f32(x))
+    if dtype == "fp4":
+        codes, scale = quantize_fp4_groups(x)
+        return StoredTensor("fp4", codes, scale)
     codes, scale = quantize_fp8_per_column(x)
     return StoredTensor("fp8", codes, scale)
 
