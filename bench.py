@@ -103,7 +103,8 @@ def stage_bytes_flops(cfg, B, plen_sum):
     d, F, D, nq, nkv = cfg.d_model, cfg.d_mlp, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
     M = cfg.tokens
     R = B * M
-    wb = 1 if cfg.weight_dtype == "fp8" else 2
+    # fp4: half a byte per weight plus one E8M0 exponent byte per 32 weights
+    wb = {"fp8": 1.0, "fp4": 0.5 + 1.0 / 32}.get(cfg.weight_dtype, 2.0)
     scale = 4 if cfg.weight_dtype == "fp8" else 0
     qd, kd = nq * D, nkv * D
     Nqkv = qd + 2 * kd
@@ -134,7 +135,8 @@ def chunk_bytes(cfg, B, plen_sum):
     d, A, F, L, K = cfg.d_model, cfg.action_dim, cfg.d_mlp, cfg.n_layers, cfg.n_steps
     D, nq, nkv = cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
     qd, kd = nq * D, nkv * D
-    wb = 1 if cfg.weight_dtype == "fp8" else (4 if cfg.weight_dtype == "f32" else 2)
+    # weight bytes per parameter (fp4: the codes plus one E8M0 exponent per 32)
+    wb = {"fp8": 1.0, "fp4": 0.5 + 1.0 / 32, "f32": 4.0}.get(cfg.weight_dtype, 2.0)
     sb = 4 if cfg.weight_dtype == "fp8" else 0          # per-column fp32 scales
     ab = 4 if cfg.weight_dtype == "f32" else 2          # small weights and K/V
     io = B * cfg.horizon * A * 4 * 2 + (B * A * 4 if cfg.state_token else 0)
@@ -373,8 +375,22 @@ def leg_batch1(args, px, wl, K, W):
     return rec
 
 
-def leg_plain(args, px, wl, name, K, W, copy_gbs):
-    """ms per chunk of another batch-1 workload, with its chunk roofline."""
+def leg_plain(args, px, wl, name, K, W, copy_gbs, env=None):
+    """ms per chunk of another batch-1 workload, with its chunk roofline
+    (`env`: library switches set for the leg, e.g. the persistent loop)."""
+    import os
+    import torch
+    env = env or {}
+    for k, v in env.items():
+        os.environ[k] = v
+    try:
+        return _leg_plain(args, px, wl, name, K, W, copy_gbs, env)
+    finally:
+        for k in env:
+            del os.environ[k]
+
+
+def _leg_plain(args, px, wl, name, K, W, copy_gbs, env):
     import torch
     cfg = wl.CONFIGS[name]
     _log(f"generating {name}")
@@ -390,7 +406,10 @@ def leg_plain(args, px, wl, name, K, W, copy_gbs):
     assert np.isfinite(out.cpu().numpy()).all()
     rec = {"ms_per_chunk": round(ms, 4), "p50_ms": round(float(np.median(per)), 4), "steps": K, "warmup": W,
            "dtype": "f32" if cfg.weight_dtype == "f32" else "bf16",
+           "weights": cfg.weight_dtype,
            "chunk_roofline": chunk_roofline(cfg, cfg.batch, int(case.prefix_len.sum()), ms, copy_gbs)}
+    if env:
+        rec["env"] = dict(env)
     ex.close()
     del prefix, noise, state, out, case
     torch.cuda.empty_cache()
@@ -483,7 +502,10 @@ def main():
     if not args.no_legs:
         Kl, Wl = max(1, min(K, 20)), min(W, 5)
         rec["legs"] = {n: leg_plain(args, px, wl, n, Kl, Wl, copy)
-                       for n in ("pi05_bf16_b1", "dit_bf16_b1", "tiny_fp32")}
+                       for n in ("pi05_bf16_b1", "dit_bf16_b1", "tiny_fp32", "pi0_fp4_b1")}
+        # the persistent batch-1 loop (opt-in) on the pi0 workload
+        rec["legs"]["pi0_bf16_b1_persistent"] = leg_plain(args, px, wl, "pi0_bf16_b1", Kl, Wl, copy,
+                                                           env={"PHYAI_PERSIST": "1"})
     if not args.no_batch64:
         rec["batch64"] = leg_batch64(args, px, wl, K, W)
     print(json.dumps(rec), flush=True)

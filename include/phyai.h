@@ -52,13 +52,19 @@ typedef enum {
 typedef enum {
   PHYAI_DTYPE_F32 = 0,
   PHYAI_DTYPE_BF16 = 1,     /* uint16 bit patterns of bfloat16                                     */
-  PHYAI_DTYPE_FP8E4M3 = 2   /* uint8 OCP e4m3fn codes with one float32 scale per output column     */
+  PHYAI_DTYPE_FP8E4M3 = 2,  /* uint8 OCP e4m3fn codes with one float32 scale per output column     */
+  PHYAI_DTYPE_FP4E2M1 = 3   /* 4-bit weights: OCP e2m1 codes, two per byte, with one power-of-two
+                               float32 scale per group of 32 input rows and output column          */
 } phyai_dtype;
 
 /* Shape of one expert.  Derived sizes: M = horizon + state_token suffix
  * tokens per request.  weight_dtype F32 selects the fp32 path (all compute
- * in fp32); BF16 and FP8E4M3 select the bf16 MFMA path (fp32 accumulate,
- * fp32 residual stream, norms, softmax and solver state). */
+ * in fp32); BF16, FP8E4M3 and FP4E2M1 select the bf16 MFMA path (fp32
+ * accumulate, fp32 residual stream, norms, softmax and solver state).
+ * FP4E2M1 is the 4-bit weight, 16-bit activation (W4A16) path of Section
+ * "PhyAI Architecture", paragraph "Quantization": its GEMMs decode the
+ * codes to bf16 on the fly and run the small-row kernels at every batch
+ * size (it is meant for weight-streaming batches). */
 typedef struct {
   int32_t variant;          /* phyai_variant                                                      */
   int32_t n_layers;         /* L                                                                  */
@@ -87,15 +93,20 @@ typedef struct {
 /* One named parameter, stored [rows][cols] row-major on the host.  Linear
  * weights are [in][out] (y = x W + b); vectors have rows = 1.  dtype must be
  * the config's weight_dtype for the per-layer trunk linears
- * (wq, wk, wv, wo, w_gate, w_up, w_down) and F32 or BF16 (matching the path:
+ * (wq, wk, wv, wo, w_gate, w_up, w_down; DiT: mlp_w1, mlp_w2) and F32 or BF16 (matching the path:
  * F32 for the fp32 path, BF16 otherwise) for every other tensor.  For
- * FP8E4M3, `scale` holds `cols` float32 scales (W_ij = code_ij * scale_j). */
+ * FP8E4M3, `scale` holds `cols` float32 scales (W_ij = code_ij * scale_j).
+ * For FP4E2M1, `data` holds rows x cols/2 bytes (byte (i, j) = the codes of
+ * columns 2j, low nibble, and 2j + 1, high nibble; cols even, rows a multiple
+ * of 32) and `scale` holds (rows/32) x cols float32 powers of two in
+ * 2^-126 .. 2^127 (W_ij = value(code_ij) * scale[i/32][j]); any other scale
+ * is PHYAI_EINVAL. */
 typedef struct {
   const char* name;         /* e.g. "in_w", "layers.3.wq" (see phyai_load_expert)               */
   int32_t dtype;            /* phyai_dtype                                                        */
   int32_t rows, cols;
   const void* data;         /* host                                                               */
-  const float* scale;       /* host, FP8E4M3 only                                                 */
+  const float* scale;       /* host, FP8E4M3 and FP4E2M1 only                                     */
 } phyai_tensor;
 
 typedef struct phyai_expert phyai_expert;

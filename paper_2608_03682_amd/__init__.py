@@ -18,7 +18,7 @@ LIB_PATH = os.path.join(_HERE, "libphyai.so")
 
 PHYAI_OK, PHYAI_EINVAL, PHYAI_ENOMEM, PHYAI_EHIP, PHYAI_EUNSUPPORTED = 0, -1, -2, -3, -4
 _VARIANT = {"pi0": 0, "pi05": 1, "dit": 2}
-_DTYPE = {"f32": 0, "bf16": 1, "fp8": 2}
+_DTYPE = {"f32": 0, "bf16": 1, "fp8": 2, "fp4": 3}
 
 # Every symbol include/phyai.h declares.
 EXPORTS = ("phyai_load_expert", "phyai_denoise", "phyai_denoise_static", "phyai_prepare", "phyai_debug_hidden",
@@ -127,7 +127,9 @@ class Expert:
                 keep.append(sc)
             nm = name.encode()
             keep.append(nm)
-            arr[i] = Tensor(nm, _DTYPE[t.dtype], data.shape[0], data.shape[1], data.ctypes.data,
+            # fp4 data holds two codes per byte: the logical width is twice its columns
+            cols = data.shape[1] * (2 if t.dtype == "fp4" else 1)
+            arr[i] = Tensor(nm, _DTYPE[t.dtype], data.shape[0], cols, data.ctypes.data,
                             None if sc is None else sc.ctypes.data)
         h = ctypes.c_void_p()
         _check(lib().phyai_load_expert(ctypes.byref(c), arr, len(weights), _stream(stream), ctypes.byref(h)))

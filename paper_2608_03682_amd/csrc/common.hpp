@@ -54,6 +54,25 @@ __device__ __forceinline__ bf16x8 fp8x8_to_bf16x8(uint32_t lo, uint32_t hi) {
   return __builtin_bit_cast(bf16x8, r);
 }
 
+// ---------------------------------------------------------------------------
+// fp4 (OCP e2m1) -> bf16 with a power-of-two scale, exact.  gfx950's
+// v_cvt_scalef32_pk_bf16_fp4 decodes the two codes of one byte (low nibble
+// first) and multiplies by 2^(exponent of the scale operand): only the
+// scale's exponent is used, which is why the weight format keeps
+// power-of-two scales (E8M0 bytes, value 2^(e - 127)).
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ float e8m0_to_f32(uint32_t e) { return __uint_as_float(e << 23); }
+
+// 8 fp4 codes (one dword, low nibble of byte 0 first) -> 8 bf16 as an MFMA operand.
+__device__ __forceinline__ bf16x8 fp4x8_to_bf16x8(uint32_t codes, float scale) {
+  uint4 r;
+  r.x = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, scale, 0));
+  r.y = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, scale, 1));
+  r.z = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, scale, 2));
+  r.w = __builtin_bit_cast(uint32_t, __builtin_amdgcn_cvt_scalef32_pk_bf16_fp4(codes, scale, 3));
+  return __builtin_bit_cast(bf16x8, r);
+}
+
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
 // D = A(16x32) * B(32x16) + C, bf16 operands, fp32 accumulate.

@@ -22,15 +22,47 @@ constexpr int kMT = 4;           // 16-row MFMA tiles per block (64 rows)
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef const __attribute__((address_space(1))) u32x4_t gu32x4_t;
 
-// 16-byte load through a global (not generic) pointer, which the compiler
-// counts with vmcnt alone
+// 16-, 8- and 2-byte loads through a global (not generic) pointer, which the
+// compiler counts with vmcnt alone
 __device__ __forceinline__ u32x4_t gload16(const void* p) { return *(gu32x4_t*)(p); }
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x2_t gload8(const void* p) {
+  return *(const __attribute__((address_space(1))) u32x2_t*)(p);
+}
+__device__ __forceinline__ uint32_t gload2(const void* p) {
+  return *(const __attribute__((address_space(1))) uint16_t*)(p);
+}
+
+// The two 8-value k-steps of lane `lane`'s weight fragment (pair tile p,
+// k-block kb, half hf) as bf16 MFMA operands, for the stored weight kinds:
+//   bf16: 32 bytes per lane; fp8: 16 bytes per lane, decoded with a unit
+//   scale (the column scale is applied to the result); fp4: 8 bytes per
+//   lane (4 per k-step) plus one E8M0 exponent per (column, k-step), the
+//   32-row group the step covers.
+template <int WK>
+__device__ __forceinline__ void load_wfrag(const GemmArgs& g, int p, int nkb, int kb, int hf, int lane, bf16x8 (&b)[2]) {
+  const int64_t frag = ((int64_t)(p * nkb + kb) * 2 + hf) * kWave + lane;
+  if constexpr (WK == W_FP8) {
+    const u32x4_t v = gload16(static_cast<const uint4*>(g.W) + frag);
+    b[0] = fp8x8_to_bf16x8(v.x, v.y);
+    b[1] = fp8x8_to_bf16x8(v.z, v.w);
+  } else if constexpr (WK == W_FP4) {
+    const u32x2_t v = gload8(static_cast<const uint2*>(g.W) + frag);
+    const uint32_t ex = gload2(g.mx + ((int64_t)(p * nkb + kb) * 2 + hf) * 32 + 2 * (lane % 16));
+    b[0] = fp4x8_to_bf16x8(v.x, e8m0_to_f32(ex & 0xff));
+    b[1] = fp4x8_to_bf16x8(v.y, e8m0_to_f32(ex >> 8));
+  } else {
+    const uint4* src = static_cast<const uint4*>(g.W) + frag * 2;
+    b[0] = __builtin_bit_cast(bf16x8, gload16(src));
+    b[1] = __builtin_bit_cast(bf16x8, gload16(src + 1));
+  }
+}
 
 // One trip of the small-row GEMM: U k-blocks starting at kb, every operand
 // load issued (as global loads, so that the compiler can count them) before
 // the first MFMA; `hook` runs between the loads and the MFMAs.  Columns past
 // N re-read the last pair tile.
-template <int U, bool FP8, bool SPLIT, int NT, int MT, class Hook>
+template <int U, int WK, bool SPLIT, int NT, int MT, class Hook>
 __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int lane, int kb,
                                         const bf16_t* const (&arp)[MT], const bf16_t* const (&alp)[MT],
                                         f32x4 (&acc)[MT][NT], const Hook& hook) {
@@ -42,16 +74,7 @@ __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
       const int p = min(pt0 + t / 2, g.NPT - 1), hf = t % 2;
-      const int64_t frag = ((int64_t)(p * nkb + kk) * 2 + hf) * kWave + lane;
-      if (FP8) {
-        const u32x4_t v = gload16(static_cast<const uint4*>(g.W) + frag);
-        b[u][t][0] = fp8x8_to_bf16x8(v.x, v.y);
-        b[u][t][1] = fp8x8_to_bf16x8(v.z, v.w);
-      } else {
-        const uint4* src = static_cast<const uint4*>(g.W) + frag * 2;
-        b[u][t][0] = __builtin_bit_cast(bf16x8, gload16(src));
-        b[u][t][1] = __builtin_bit_cast(bf16x8, gload16(src + 1));
-      }
+      load_wfrag<WK>(g, p, nkb, kk, hf, lane, b[u][t]);
     }
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
@@ -86,7 +109,7 @@ __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int
 // selects a slice of K and the block writes its raw partial sums to
 // split_out[z] (fp32 [R][32*NPT]) instead of running the epilogue; the
 // consumer adds the slices in a fixed order.
-template <class Epi, bool FP8, bool SPLIT, int NP, int MT>
+template <class Epi, int WK, bool SPLIT, int NP, int MT>
 __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   constexpr int NT = 2 * NP;
   static_assert(MT >= 1 && MT <= 4, "at most one row tile per wave");
@@ -152,18 +175,18 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   // first trip carries the epilogue loads
   int kb = kb0;
   if (kb + 4 <= kb1) {
-    b1_trip<4, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
-    for (kb += 4; kb + 4 <= kb1; kb += 4) b1_trip<4, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+    b1_trip<4, WK, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+    for (kb += 4; kb + 4 <= kb1; kb += 4) b1_trip<4, WK, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
     if (kb + 2 <= kb1) {
-      b1_trip<2, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+      b1_trip<2, WK, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
       kb += 2;
     }
-    if (kb < kb1) b1_trip<1, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
+    if (kb < kb1) b1_trip<1, WK, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, no_loads);
   } else if (kb + 2 <= kb1) {
-    b1_trip<2, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
-    if (kb + 3 == kb1) b1_trip<1, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb + 2, arp, alp, acc, no_loads);
+    b1_trip<2, WK, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+    if (kb + 3 == kb1) b1_trip<1, WK, SPLIT, NT, MT>(g, pt0, nkb, lane, kb + 2, arp, alp, acc, no_loads);
   } else if (kb < kb1) {
-    b1_trip<1, FP8, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
+    b1_trip<1, WK, SPLIT, NT, MT>(g, pt0, nkb, lane, kb, arp, alp, acc, epi_loads);
   } else {
     epi_loads();
   }
@@ -738,7 +761,7 @@ namespace {
 // stored; splits past n_split re-read the last one and are skipped.  The 1-D
 // grid deals consecutive tiles (slice-major) to one XCD, so each XCD's L2
 // fetches the partials and weights of its own slices only.
-template <class Epi, bool FP8, int NS>
+template <class Epi, int WK, int NS>
 __global__ __launch_bounds__(512) void merge_gemm_kernel(GemmArgs g, AttnParts ap, Epi epi) {
   constexpr int KZ = 256;                     // K per slice
   constexpr int KH = KZ / 128;                // k-blocks of 64 per wave half
@@ -761,18 +784,7 @@ __global__ __launch_bounds__(512) void merge_gemm_kernel(GemmArgs g, AttnParts a
 #pragma unroll
   for (int j = 0; j < KH; ++j)
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int64_t frag = ((int64_t)(p * nkb + z * (KZ / 64) + kh * KH + j) * 2 + hf) * kWave + lane;
-      if (FP8) {
-        const u32x4_t v = gload16(static_cast<const uint4*>(g.W) + frag);
-        b[j][hf][0] = fp8x8_to_bf16x8(v.x, v.y);
-        b[j][hf][1] = fp8x8_to_bf16x8(v.z, v.w);
-      } else {
-        const uint4* src = static_cast<const uint4*>(g.W) + frag * 2;
-        b[j][hf][0] = __builtin_bit_cast(bf16x8, gload16(src));
-        b[j][hf][1] = __builtin_bit_cast(bf16x8, gload16(src + 1));
-      }
-    }
+    for (int hf = 0; hf < 2; ++hf) load_wfrag<WK>(g, p, nkb, z * (KZ / 64) + kh * KH + j, hf, lane, b[j][hf]);
 
   // split partials of row i, elements 8 cc .. 8 cc + 7 of the slice
   const int i = threadIdx.x / 32, cc = threadIdx.x % 32;
@@ -895,7 +907,8 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
   if (g.kind == W_F32) {
     dim3 grid(g.NPT, (g.R + 15) / 16);
     hipLaunchKernelGGL(gemm_f32_kernel<Epi>, grid, dim3(256), 0, s, g, epi);
-  } else if (g.R >= 256 && g.A_lo == nullptr && g.A_ind == nullptr && g.rows_per_req == 0 && g.NPT % 4 == 0) {
+  } else if (g.R >= 256 && g.A_lo == nullptr && g.A_ind == nullptr && g.rows_per_req == 0 && g.NPT % 4 == 0 &&
+             g.kind != W_FP4) {
     const int tiles = gemm_tiles(g);
     const char* force = getenv("PHYAI_GEMM_TILE");   // tests: "ring" / "deep" / "strided" (read at enqueue time)
     // at most one tile per CU: no second block covers the load latency, so
@@ -929,13 +942,14 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
     auto go = [&](auto mtag) {
       constexpr int MT = decltype(mtag)::value;
       const dim3 grid(g.NPT, (g.R + 16 * MT - 1) / (16 * MT), nz);
-      if (g.kind == W_FP8) {
-        if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, true, 1, MT>), grid, dim3(256), 0, s, g, epi);
-        else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, true, false, 1, MT>), grid, dim3(256), 0, s, g, epi);
-      } else {
-        if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, true, 1, MT>), grid, dim3(256), 0, s, g, epi);
-        else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, false, false, 1, MT>), grid, dim3(256), 0, s, g, epi);
-      }
+      auto kind = [&](auto wk) {
+        constexpr int WK = decltype(wk)::value;
+        if (two) hipLaunchKernelGGL((gemm_mfma_kernel<Epi, WK, true, 1, MT>), grid, dim3(256), 0, s, g, epi);
+        else hipLaunchKernelGGL((gemm_mfma_kernel<Epi, WK, false, 1, MT>), grid, dim3(256), 0, s, g, epi);
+      };
+      if (g.kind == W_FP8) kind(std::integral_constant<int, W_FP8>{});
+      else if (g.kind == W_FP4) kind(std::integral_constant<int, W_FP4>{});
+      else kind(std::integral_constant<int, W_BF16>{});
     };
     const int mt = nz > 1 ? 1 : small_row_tiles(g.R, g.NPT);
     if (mt == 1) go(std::integral_constant<int, 1>{});
@@ -959,11 +973,11 @@ void gemm_kv_f32(const GemmArgs& g, const EpiKV<float>& e, hipStream_t s) { laun
 void gemm_merge_resid(const GemmArgs& g, const AttnParts& ap, const EpiResid& e, hipStream_t s) {
   const int tiles = ((g.NPT + 3) / 4) * ((g.R + 15) / 16) * (g.K / 256);
   const dim3 grid(8 * ((tiles + 7) / 8));
-  const bool fp8 = g.kind == W_FP8;
   auto go = [&](auto ns) {
     constexpr int NS = decltype(ns)::value;
-    if (fp8) hipLaunchKernelGGL((merge_gemm_kernel<EpiResid, true, NS>), grid, dim3(512), 0, s, g, ap, e);
-    else hipLaunchKernelGGL((merge_gemm_kernel<EpiResid, false, NS>), grid, dim3(512), 0, s, g, ap, e);
+    if (g.kind == W_FP8) hipLaunchKernelGGL((merge_gemm_kernel<EpiResid, W_FP8, NS>), grid, dim3(512), 0, s, g, ap, e);
+    else if (g.kind == W_FP4) hipLaunchKernelGGL((merge_gemm_kernel<EpiResid, W_FP4, NS>), grid, dim3(512), 0, s, g, ap, e);
+    else hipLaunchKernelGGL((merge_gemm_kernel<EpiResid, W_BF16, NS>), grid, dim3(512), 0, s, g, ap, e);
   };
   if (ap.n_split <= 4) go(std::integral_constant<int, 4>{});
   else if (ap.n_split <= 8) go(std::integral_constant<int, 8>{});

@@ -30,7 +30,7 @@ struct CallDesc {
 // without a shuffle.  Which logical columns a pair tile holds is decided by
 // the packing order chosen on the host.
 // ---------------------------------------------------------------------------
-enum WeightKind { W_F32 = 0, W_BF16 = 1, W_FP8 = 2 };
+enum WeightKind { W_F32 = 0, W_BF16 = 1, W_FP8 = 2, W_FP4 = 3 };
 
 struct GemmArgs {
   const void* A;            // [R][lda], bf16 (MFMA path) or f32 (fp32 path)
@@ -43,6 +43,7 @@ struct GemmArgs {
   int NPT;                  // pair tiles (N / 32)
   const void* W;            // packed weights
   const float* scale;       // fp8: one scale per packed column
+  const uint8_t* mx;        // fp4: E8M0 scale exponents, per (pair tile, k-block, half) [16 columns][2 k-steps]
   int kind;                 // WeightKind
   // optional A-row validity: rows r with (r % rows_per_req) >= prefix_len[r / rows_per_req]
   // read as zero (used for feature rows beyond a request's length)

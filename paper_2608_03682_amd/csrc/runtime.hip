@@ -71,6 +71,7 @@ struct DevMem {
 struct Lin {
   void* w = nullptr;
   float* scale = nullptr;
+  uint8_t* mx = nullptr;    // fp4: E8M0 scale exponents
   int K = 0, NPT = 0, kind = W_BF16;
 };
 
@@ -222,10 +223,26 @@ Lin pack_linear(phyai_expert& e, const std::vector<const phyai_tensor*>& srcs, i
   std::vector<int> src_of, col_of;
   for (size_t i = 0; i < srcs.size(); ++i) {
     if (srcs[i]->rows != K) fail(PHYAI_EINVAL, "fused linear sources disagree in rows");
-    const int want = kind == W_FP8 ? PHYAI_DTYPE_FP8E4M3 : (kind == W_BF16 ? PHYAI_DTYPE_BF16 : PHYAI_DTYPE_F32);
+    const int want = kind == W_FP8   ? PHYAI_DTYPE_FP8E4M3
+                     : kind == W_FP4 ? PHYAI_DTYPE_FP4E2M1
+                     : kind == W_BF16 ? PHYAI_DTYPE_BF16 : PHYAI_DTYPE_F32;
     if (srcs[i]->dtype != want)
       fail(PHYAI_EINVAL, std::string("tensor '") + srcs[i]->name + "' has the wrong dtype for this path");
-    if (kind == W_FP8 && !srcs[i]->scale) fail(PHYAI_EINVAL, std::string("tensor '") + srcs[i]->name + "' needs scales");
+    if ((kind == W_FP8 || kind == W_FP4) && !srcs[i]->scale)
+      fail(PHYAI_EINVAL, std::string("tensor '") + srcs[i]->name + "' needs scales");
+    if (kind == W_FP4) {
+      if (srcs[i]->cols % 2 || K % 32)
+        fail(PHYAI_EINVAL, std::string("fp4 tensor '") + srcs[i]->name + "' needs even cols and rows % 32 == 0");
+      // scales: finite powers of two in the normal range, 2^-126 .. 2^127
+      const int64_t ns = (int64_t)(K / 32) * srcs[i]->cols;
+      for (int64_t q = 0; q < ns; ++q) {
+        uint32_t u;
+        std::memcpy(&u, &srcs[i]->scale[q], 4);
+        const uint32_t ex = (u >> 23) & 0xff;
+        if ((u & 0x807fffffu) != 0 || ex == 0 || ex == 0xff)
+          fail(PHYAI_EINVAL, std::string("fp4 tensor '") + srcs[i]->name + "' has a scale that is not a power of two");
+      }
+    }
     for (int c = 0; c < srcs[i]->cols; ++c) {
       src_of.push_back((int)i);
       col_of.push_back(c);
@@ -249,6 +266,39 @@ Lin pack_linear(phyai_expert& e, const std::vector<const phyai_tensor*>& srcs, i
     }
     L.w = e.mem.alloc(buf.size() * 4);
     HIPC(hipMemcpyAsync(L.w, buf.data(), buf.size() * 4, hipMemcpyHostToDevice, s));
+    HIPC(hipStreamSynchronize(s));
+    return L;
+  }
+  if (kind == W_FP4) {
+    // codes: 8 bytes per (pair tile, k-block, half, lane): k-step 0 in bytes
+    // 0-3, k-step 1 in bytes 4-7, value j of a step in byte j / 2 (low nibble
+    // first); exponents: per (pair tile, k-block, half) [16 columns][2 steps]
+    std::vector<uint8_t> buf((size_t)K * Np / 2, 0);
+    std::vector<uint8_t> mx((size_t)(K / 32) * Np, 127);
+    for (int pc = 0; pc < Np; ++pc) {
+      const int lc = perm(pc);
+      if (lc < 0) continue;
+      const int p = pc / 32, hf = (pc % 32) / 16, c = pc % 16;
+      const phyai_tensor* t = srcs[src_of[lc]];
+      const int cc = col_of[lc];
+      const uint8_t* codes = static_cast<const uint8_t*>(t->data);
+      for (int k = 0; k < K; ++k) {
+        const int kb = k / 64, st = (k % 64) / 32, kg = (k % 32) / 8, j = k % 8;
+        const int lane = kg * 16 + c;
+        const size_t frag = ((size_t)(p * nkb + kb) * 2 + hf) * 64 + lane;
+        const uint8_t code = (codes[(int64_t)k * (t->cols / 2) + cc / 2] >> (4 * (cc & 1))) & 0xF;
+        buf[frag * 8 + st * 4 + j / 2] |= code << (4 * (j & 1));
+        if (k % 32 == 0) {
+          uint32_t u;
+          std::memcpy(&u, &t->scale[(int64_t)(k / 32) * t->cols + cc], 4);
+          mx[((size_t)(p * nkb + kb) * 2 + hf) * 32 + 2 * c + st] = (u >> 23) & 0xff;
+        }
+      }
+    }
+    L.w = e.mem.alloc(buf.size());
+    HIPC(hipMemcpyAsync(L.w, buf.data(), buf.size(), hipMemcpyHostToDevice, s));
+    L.mx = static_cast<uint8_t*>(e.mem.alloc(mx.size()));
+    HIPC(hipMemcpyAsync(L.mx, mx.data(), mx.size(), hipMemcpyHostToDevice, s));
     HIPC(hipStreamSynchronize(s));
     return L;
   }
@@ -344,6 +394,7 @@ GemmArgs gargs(const Lin& w, const void* A, int lda, int R) {
   g.NPT = w.NPT;
   g.W = w.w;
   g.scale = w.scale;
+  g.mx = w.mx;
   g.kind = w.kind;
   return g;
 }
@@ -804,12 +855,12 @@ void check_config(const phyai_config& c) {
   req(c.max_batch >= 1 && c.max_batch <= kMaxBatch, "max_batch out of range (1..512)");
   req(c.prefix_cap >= 0, "prefix_cap < 0");
   req(c.time_dim >= 4 && c.time_dim % 64 == 0, "time_dim must be a multiple of 64");
-  req(c.weight_dtype >= 0 && c.weight_dtype <= 2, "weight_dtype out of range");
+  req(c.weight_dtype >= 0 && c.weight_dtype <= 3, "weight_dtype out of range");
   req(c.rms_eps > 0.f, "rms_eps must be positive");
   req(c.sin_min_period > 0.f && c.sin_max_period > 0.f, "sinusoid periods must be positive");
   const bool f32 = c.weight_dtype == PHYAI_DTYPE_F32;
   req(c.kv_dtype == (f32 ? PHYAI_DTYPE_F32 : PHYAI_DTYPE_BF16),
-      "kv_dtype must be F32 on the fp32 path and BF16 on the bf16/fp8 path");
+      "kv_dtype must be F32 on the fp32 path and BF16 on the bf16/fp8/fp4 path");
   if (c.variant == PHYAI_VARIANT_DIT) {
     req(c.d_feat >= 64 && c.d_feat % 64 == 0, "DiT needs d_feat, a multiple of 64");
     req(c.n_kv_heads == c.n_q_heads, "DiT attention has one key/value head per query head");
@@ -843,7 +894,9 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     P.by_name[tensors[i].name] = &tensors[i];
   }
   const int wk_small = e->f32 ? W_F32 : W_BF16;
-  const int wk_trunk = e->f32 ? W_F32 : (c.weight_dtype == PHYAI_DTYPE_FP8E4M3 ? W_FP8 : W_BF16);
+  const int wk_trunk = e->f32                                   ? W_F32
+                       : c.weight_dtype == PHYAI_DTYPE_FP8E4M3 ? W_FP8
+                       : c.weight_dtype == PHYAI_DTYPE_FP4E2M1 ? W_FP4 : W_BF16;
   auto vec = [&](const std::string& n, int len) { return upload_f32(*e, P.get(n, 1, len), s); };
 
   e->in_w = upload_f32(*e, P.get("in_w", A, d), s);

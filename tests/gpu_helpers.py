@@ -30,7 +30,9 @@ def small_cfg(variant: str, **kw) -> wl.ExpertConfig:
 
 def tolerance(cfg) -> float:
     """Max-abs bar on the final actions (relative to max(1, rms(oracle)))."""
-    return {"f32": 1e-4, "bf16": 2e-2, "fp8": 5e-2}[cfg.weight_dtype]
+    # fp4 weights decode exactly to bf16 on both sides, so only the bf16
+    # activations separate the GPU from the oracle: the bf16 bar
+    return {"f32": 1e-4, "bf16": 2e-2, "fp8": 5e-2, "fp4": 2e-2}[cfg.weight_dtype]
 
 
 def to_device(case):

@@ -177,3 +177,30 @@ def test_invalid_arguments_leave_output_untouched():
         ex.denoise(prefix, case.prefix_len, noise, case.timesteps, state, out=shifted)
     torch.cuda.synchronize()
     assert bool((out == 7.0).all())
+
+
+def test_permutation_equivariance_tiny_fp32_config():
+    """Without positional terms (the tiny fp32 workload has no RoPE and no
+    state token) the action tokens are exchangeable: permuting the noise rows
+    permutes the output rows the same way.  Only the order of the attention
+    sums over the suffix keys changes, so the two runs agree to float32
+    rounding; the oracle checks the unpermuted run to the parity bar."""
+    cfg = wl.CONFIGS["tiny_fp32"]
+    assert not cfg.rope and not cfg.state_token
+    print("[case] permutation equivariance tiny_fp32", flush=True)
+    case = wl.make_case(cfg, seed=9)
+    ex = _px().Expert(cfg, case.weights)
+    ref = run_gpu(ex, case)
+    compare("tiny_fp32 seed 9", ref, oracle.denoise(cfg, case.weights, case.prefix, case.prefix_len, case.noise,
+                                                    case.timesteps, case.state), cfg)
+    for seed in (1, 2):
+        perm = np.random.default_rng(seed).permutation(cfg.horizon)
+        case.noise = case.noise.copy()
+        noise0 = case.noise.copy()
+        case.noise = noise0[:, perm]
+        out = run_gpu(ex, case)
+        case.noise = noise0
+        err = np.abs(out - ref[:, perm]).max()
+        print(f"[parity] permuted run vs permuted reference: max_abs={err:.3e}", flush=True)
+        assert err <= 1e-5 * max(1.0, float(np.sqrt(np.mean(ref ** 2))))
+    ex.close()

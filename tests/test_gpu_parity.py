@@ -1,6 +1,7 @@
 """GPU parity: the HIP path (through the C ABI) against the fp64 oracle on the
 same seeded inputs.  Bars: max-abs <= tol * max(1, rms(oracle)) with tol
-1e-4 (fp32 path), 2e-2 (bf16), 5e-2 (fp8 weights)."""
+1e-4 (fp32 path), 2e-2 (bf16, and fp4 weights, which both sides decode
+exactly), 5e-2 (fp8 weights)."""
 import dataclasses
 import os
 
@@ -51,6 +52,10 @@ def test_fp8_decode_all_codes_bit_exact():
     ("pi05", dict(d_model=1024)),                   # the same with adaRMS shift and compensated output
     ("dit", {}),
     ("pi0", dict(weight_dtype="f32", kv_dtype="f32", state_token=False, rope=False)),
+    ("pi0", dict(weight_dtype="fp4")),              # 4-bit weights: the small-row GEMMs and the merge GEMM
+    ("pi0", dict(weight_dtype="fp4", batch=7)),     # 357 rows: fp4 keeps the small-row kernels
+    ("pi05", dict(weight_dtype="fp4")),
+    ("dit", dict(weight_dtype="fp4")),
 ])
 def test_small_parity(variant, kw):
     cfg = small_cfg(variant, **kw)
@@ -113,7 +118,7 @@ def test_tiny_fp32_full_config():
     compare("tiny_fp32", run_gpu(ex, case), _oracle(cfg, case), cfg)
 
 
-@pytest.mark.parametrize("name", ["pi0_bf16_b1", "pi05_bf16_b1", "dit_bf16_b1"])
+@pytest.mark.parametrize("name", ["pi0_bf16_b1", "pi05_bf16_b1", "dit_bf16_b1", "pi0_fp4_b1"])
 def test_full_size_batch1(name):
     cfg = wl.CONFIGS[name]
     print(f"[case] {name}", flush=True)
@@ -125,8 +130,9 @@ def test_full_size_batch1(name):
 
 def test_full_size_batch64_fp8_sampled():
     """The rollout batch: all 64 requests run on the GPU in the benchmark's
-    launch configuration; the oracle checks a sample of requests one by one
-    (the shortest and the longest prefix, plus the first and last slots)."""
+    launch configuration.  The oracle runs a sample of requests live (the
+    shortest and the longest prefix, plus the first and last slots) and every
+    request is compared with the oracle's stored output for this workload."""
     cfg = wl.CONFIGS["pi0_fp8_b64"]
     print("[case] pi0_fp8_b64 sampled", flush=True)
     case = wl.make_case(cfg, seed=0)
@@ -140,6 +146,13 @@ def test_full_size_batch64_fp8_sampled():
     ref = oracle.denoise(cfg, case.weights, pre, pl[sample], case.noise[sample], case.timesteps,
                          case.state[sample], decoded=W, slots=list(range(len(sample))))
     compare(f"pi0_fp8_b64 requests {sample}", gpu[sample], ref, cfg)
+    # every request against the oracle's stored output (tests/golden/make_c5_expected.py,
+    # which runs only the oracle on the same seeded workload)
+    gold = np.load(os.path.join(os.path.dirname(__file__), "golden", "c5_expected.npz"))
+    assert str(gold["config"]) == cfg.name and int(gold["seed"]) == 0
+    # (equal up to BLAS summation order, which depends on the thread count)
+    assert np.allclose(gold["actions"][sample], ref, rtol=0, atol=1e-9), "stored oracle output is stale"
+    compare("pi0_fp8_b64 all 64 requests", gpu, gold["actions"], cfg)
 
 
 @pytest.mark.parametrize("variant,kw", [
@@ -203,3 +216,20 @@ def test_many_row_gemm_tiles(tile, wdt):
     finally:
         del os.environ["PHYAI_GEMM_TILE"]
     compare(f"gemm tile {tile} {wdt}", gpu, _oracle(cfg, case), cfg)
+
+
+def test_fp4_scales_must_be_powers_of_two():
+    """The fp4 format's scales are applied by the hardware conversion, which
+    uses only their exponent: a scale that is not a power of two is refused
+    at load (PHYAI_EINVAL) instead of being silently rounded."""
+    import paper_2608_03682_amd as px
+    cfg = small_cfg("pi0", weight_dtype="fp4", batch=1)
+    case = wl.make_case(cfg, seed=3)
+    w = dict(case.weights)
+    t = w["layers.0.wo"]
+    bad = t.scale.copy()
+    bad[0, 0] *= 1.5
+    w["layers.0.wo"] = dataclasses.replace(t, scale=bad)
+    with pytest.raises(px.PhyaiError) as ei:
+        px.Expert(cfg, w)
+    assert ei.value.code == px.PHYAI_EINVAL and "power of two" in str(ei.value)
