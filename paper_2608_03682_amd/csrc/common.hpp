@@ -75,6 +75,29 @@ __device__ __forceinline__ bf16x8 fp4x8_to_bf16x8(uint32_t codes, float scale) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(uint4 v) { return __builtin_bit_cast(bf16x8, v); }
 
+// ---------------------------------------------------------------------------
+// Device-scope (sc1) stores and loads, for data another block reads within
+// the same kernel: the store writes through the writer's L2, and the load
+// bypasses a possibly stale line in the reader's (the XCDs' L2s are not
+// coherent with each other).  `base` must be the same for the whole wave (the
+// buffer resource lives in scalar registers; a per-lane base would make the
+// compiler loop over the distinct values); `off` is the lane's element
+// offset, below 2^29.
+// ---------------------------------------------------------------------------
+constexpr int kDeviceScope = 16;   // buffer instruction cache policy: sc1
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t raw_rsrc(const void* p) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, 0x7fffffff, 0x00020000);
+}
+__device__ __forceinline__ void st_device_f32(float* base, int64_t off, float v) {
+  __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), raw_rsrc(base), static_cast<int>(off * 4), 0,
+                                        kDeviceScope);
+}
+__device__ __forceinline__ float4 ld_device_f32x4(const float* base, int64_t off) {
+  typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+  const u4 v = __builtin_amdgcn_raw_buffer_load_b128(raw_rsrc(base), static_cast<int>(off * 4), 0, kDeviceScope);
+  return __builtin_bit_cast(float4, v);
+}
+
 // D = A(16x32) * B(32x16) + C, bf16 operands, fp32 accumulate.
 // Lane l holds A[l%16][k8(l/16) .. +7], B[k8(l/16) .. +7][l%16] and
 // C[4*(l/16) + v][l%16] (v = 0..3).  The k order inside a lane only has to

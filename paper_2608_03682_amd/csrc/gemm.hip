@@ -99,6 +99,70 @@ __device__ __forceinline__ void b1_trip(const GemmArgs& g, int pt0, int nkb, int
         }
 }
 
+// Finishing of a split-K residual tile: rows r0 .. r0 + nr - 1, columns c0 ..
+// c0 + nc - 1 (nc a multiple of 32) of an output whose S blocks each stored
+// one slice with device-scope stores.  Called by every thread of an
+// NTHR-thread block after its own partial stores.  The block whose arrival
+// completes the tile's count adds the slices (in slice order) into h, and
+// with a gain stores the next norm's bf16(h (1 + gain)) and the per-row sums
+// of h^2 over each 32 columns (fused residual-add + RMSNorm, the norm's
+// row scale then applied by the consuming GEMM).  It also puts the counter
+// back to zero for the next launch.
+template <int NTHR>
+__device__ __forceinline__ void finish_split_tile(const GemmArgs& g, int S, int tile, int r0, int nr, int c0, int nc,
+                                                  int* flag) {
+  __builtin_amdgcn_s_waitcnt(0);              // this thread's slice stores are complete
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    const unsigned old = __hip_atomic_fetch_add(g.fin_ctr + tile, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const int last = old + 1 == static_cast<unsigned>(S);
+    if (last) __hip_atomic_store(g.fin_ctr + tile, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    *flag = last;
+  }
+  __syncthreads();
+  if (!*flag) return;
+  const int N = 32 * g.NPT;
+  const int q4 = nc / 4;                      // float4 columns per row; 8 consecutive ones per 32 columns
+  const int items = nr * q4;
+  for (int base = 0; base < items; base += NTHR) {
+    const int it = base + static_cast<int>(threadIdx.x);
+    const int row = r0 + (it < items ? it / q4 : 0);
+    const int col = c0 + 4 * (it < items ? it % q4 : 0);
+    const bool ok = it < items && row < g.R;
+    const int lr = ok ? row : 0;
+    // every load unconditional (slice index clamped, the extra slices not added)
+    float4 hv = *reinterpret_cast<const float4*>(g.fin_h + (int64_t)lr * N + col);
+    float4 ps[16];
+#pragma unroll
+    for (int sl = 0; sl < 16; ++sl)
+      ps[sl] = ld_device_f32x4(g.split_out, min(sl, S - 1) * g.split_stride + (int64_t)lr * N + col);
+#pragma unroll
+    for (int sl = 0; sl < 16; ++sl)
+      if (sl < S) {
+        hv.x += ps[sl].x; hv.y += ps[sl].y; hv.z += ps[sl].z; hv.w += ps[sl].w;
+      }
+    float sq = 0.f;
+    if (ok) {
+      *reinterpret_cast<float4*>(g.fin_h + (int64_t)row * N + col) = hv;
+      if (g.fin_gain) {
+        const float4 gn = *reinterpret_cast<const float4*>(g.fin_gain + col);
+        uint2 a;
+        a.x = pack_bf16x2(hv.x * (1.f + gn.x), hv.y * (1.f + gn.y));
+        a.y = pack_bf16x2(hv.z * (1.f + gn.z), hv.w * (1.f + gn.w));
+        *reinterpret_cast<uint2*>(g.fin_a + (int64_t)row * N + col) = a;
+        sq = (hv.x * hv.x + hv.y * hv.y) + (hv.z * hv.z + hv.w * hv.w);
+      }
+    }
+    if (g.fin_gain) {
+      // the 8 threads of one 32-column group are consecutive lanes
+      sq += __shfl_xor(sq, 1, 64);
+      sq += __shfl_xor(sq, 2, 64);
+      sq += __shfl_xor(sq, 4, 64);
+      if (ok && (col % 32) == 0) g.fin_ss[(int64_t)row * (N / 32) + col / 32] = sq;
+    }
+  }
+}
+
 // Small-row GEMM (batch-1 style): one block = 4 waves computing 16*MT rows x
 // 32*NP columns; the block's K range is split between the 4 waves, whose
 // partial sums are added through LDS.  Wave w finishes row tile w % MT, the
@@ -149,7 +213,27 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   typename Epi::ColPre cq[NP];
   typename Epi::Pre pre[NP][MT];
   float sc[NP][2];
+  float rs[MT];                               // folded norm: 1/rms of the rows this lane finishes
   auto epi_loads = [&]() {
+    if (g.row_ss) {
+      // lanes c % 4 = j share a row's sums: chunks j, j + 4, ... of its row_nt / 4
+      const int nch = g.row_nt / 4;
+#pragma unroll
+      for (int vv = 0; vv < MT; ++vv) {
+        const int row = m0 + 16 * emt + 4 * akg + ev0 + vv;
+        const float* rp = g.row_ss + (int64_t)(row < g.R ? row : 0) * g.row_nt;
+        float sum = 0.f;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int ch = (c % 4) + 4 * i;
+          const float4 v = *reinterpret_cast<const float4*>(rp + 4 * min(ch, nch - 1));
+          if (ch < nch) sum += (v.x + v.y) + (v.z + v.w);
+        }
+        sum += __shfl_xor(sum, 1, 64);
+        sum += __shfl_xor(sum, 2, 64);
+        rs[vv] = 1.0f / sqrtf(sum / (float)(32 * g.row_nt) + g.row_eps);
+      }
+    }
 #pragma unroll
     for (int pp = 0; pp < NP; ++pp) {
       const int p = min(pt0 + pp, g.NPT - 1);
@@ -234,13 +318,24 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
       const int row = m0 + 16 * mt + 4 * akg + ev0 + vv;
       if (row < g.R) {
         if (sp) {
-          sp[(int64_t)row * N + 32 * p + c] = s0[vv] * sc[pp][0];
-          sp[(int64_t)row * N + 32 * p + 16 + c] = s1[vv] * sc[pp][1];
+          if (g.fin_ctr) {
+            st_device_f32(sp, (int64_t)row * N + 32 * p + c, s0[vv] * sc[pp][0]);
+            st_device_f32(sp, (int64_t)row * N + 32 * p + 16 + c, s1[vv] * sc[pp][1]);
+          } else {
+            sp[(int64_t)row * N + 32 * p + c] = s0[vv] * sc[pp][0];
+            sp[(int64_t)row * N + 32 * p + 16 + c] = s1[vv] * sc[pp][1];
+          }
         } else {
-          epi.apply(row, p, c, cq[pp], pre[pp][vv], s0[vv] * sc[pp][0], s1[vv] * sc[pp][1]);
+          const float r = g.row_ss ? rs[vv] : 1.f;
+          epi.apply(row, p, c, cq[pp], pre[pp][vv], s0[vv] * sc[pp][0] * r, s1[vv] * sc[pp][1] * r);
         }
       }
     }
+  }
+  if (sp && g.fin_ctr) {
+    __shared__ int last;
+    const int nc = 32 * min(NP, g.NPT - pt0);
+    finish_split_tile<256>(g, nz, blockIdx.y * gridDim.x + blockIdx.x, m0, 16 * MT, 32 * pt0, nc, &last);
   }
 }
 
@@ -864,20 +959,31 @@ __global__ __launch_bounds__(512) void merge_gemm_kernel(GemmArgs g, AttnParts a
     red[wq][1][lane] = acc[1];
   }
   __syncthreads();
-  if (kh == 1 || pw >= g.NPT) return;
-  acc[0] += red[wq][0][lane];
-  acc[1] += red[wq][1][lane];
   const int N = 32 * g.NPT;
+  if (!(kh == 1 || pw >= g.NPT)) {
+    acc[0] += red[wq][0][lane];
+    acc[1] += red[wq][1][lane];
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int row = m0 + 4 * akg + v;
-    if (row >= g.R) continue;
-    if (sp) {
-      sp[(int64_t)row * N + 32 * p + c] = acc[0][v] * sc0;
-      sp[(int64_t)row * N + 32 * p + 16 + c] = acc[1][v] * sc1;
-    } else {
-      epi.apply(row, p, c, cq, pre[v], acc[0][v] * sc0, acc[1][v] * sc1);
+    for (int v = 0; v < 4; ++v) {
+      const int row = m0 + 4 * akg + v;
+      if (row >= g.R) continue;
+      if (sp) {
+        if (g.fin_ctr) {
+          st_device_f32(sp, (int64_t)row * N + 32 * p + c, acc[0][v] * sc0);
+          st_device_f32(sp, (int64_t)row * N + 32 * p + 16 + c, acc[1][v] * sc1);
+        } else {
+          sp[(int64_t)row * N + 32 * p + c] = acc[0][v] * sc0;
+          sp[(int64_t)row * N + 32 * p + 16 + c] = acc[1][v] * sc1;
+        }
+      } else {
+        epi.apply(row, p, c, cq, pre[v], acc[0][v] * sc0, acc[1][v] * sc1);
+      }
     }
+  }
+  if (sp && g.fin_ctr) {
+    __shared__ int last;
+    const int nc = 32 * min(4, g.NPT - bx * 4);
+    finish_split_tile<512>(g, g.K / KZ, (m0 / 16) * nx + bx, m0, 16, 32 * bx * 4, nc, &last);
   }
 }
 

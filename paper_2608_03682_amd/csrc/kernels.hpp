@@ -55,6 +55,24 @@ struct GemmArgs {
   float* split_out;
   int64_t split_stride;
   int split_k;
+  // optional row scale of the output, the RMSNorm folded into this GEMM: A
+  // holds bf16(h (1 + w)) and row r of the product is multiplied by
+  // 1 / sqrt(sum_t row_ss[r][t] / (32 row_nt) + row_eps) (row_nt = d / 32
+  // per-32-column sums of h^2 per row; small-row kernel only)
+  const float* row_ss;
+  int row_nt;
+  float row_eps;
+  // optional finishing of a split-K residual GEMM (with split_out; small-row
+  // and merging kernels): the last block to arrive at an output tile adds
+  // the split slices in order into fin_h (h += sum_s part[s]) and, with
+  // fin_gain set, stores bf16(h (1 + fin_gain)) into fin_a and the tile's
+  // per-row sums of h^2 into fin_ss [R][N / 32].  fin_ctr holds one counter
+  // per output tile, zero at launch and left zero.
+  float* fin_h;
+  bf16_t* fin_a;
+  float* fin_ss;
+  const float* fin_gain;
+  unsigned* fin_ctr;
 };
 
 // Split factor gemm launches use for a small-row GEMM (1 = no split).

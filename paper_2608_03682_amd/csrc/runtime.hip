@@ -112,6 +112,11 @@ struct phyai_expert {
   // per-layer key ranges: K [L][Bmax][nkv][ldk][D], V transposed [L][Bmax][nkv][D][ldk]
   void *kall = nullptr, *vt = nullptr;
   float* pend = nullptr;    // split-K partial sums of the residual GEMMs (small batches)
+  // norms folded into the GEMMs (pi0, small batches): per-32-column sums of
+  // h^2 of the rows the next GEMM normalises, and the residual GEMMs' tile
+  // counters (zero between launches)
+  float* ss = nullptr;
+  unsigned* fin_ctr = nullptr;
   // the partial buffers the next enqueue uses: part/pend, or the static
   // scratch for phyai_denoise_static
   float *part_cur = nullptr, *pend_cur = nullptr;
@@ -457,6 +462,30 @@ int resid_split(const phyai_expert& e, int which, int l, int B) {
   return gemm_split_k(B * e.M, w.NPT, w.K);
 }
 
+// Counters of the residual GEMMs' split-K finishing: one per output tile.
+constexpr int kFinCounters = 4096;
+
+// Whether the RMSNorms of block l > 0 (before the QKV GEMM) and of every
+// block's MLP fold into the GEMMs at batch B (the paper's fused residual-add
+// + RMSNorm, paragraph "Kernel fusion"): pi0 on the bf16 path, every residual
+// GEMM split over K (small batches), so that the block completing an output
+// tile adds the split slices into h and leaves bf16(h (1 + w)) and the
+// tile's sums of h^2 for the next GEMM, which scales its rows by 1/rms.
+// Opt-in (PHYAI_NORM_FOLD=1, read at enqueue time): on MI355X the tile
+// finishing (an atomic round trip, then the slices' device-scope loads) and
+// the row scales cost the residual and consuming GEMMs more than the two norm
+// launches per block they replace (pi0 batch 1: 8.86 against 8.29 ms).
+bool fold_norms(const phyai_expert& e, int B) {
+  if (e.c.variant != PHYAI_VARIANT_PI0 || e.f32 || !e.fin_ctr) return false;
+  const char* f = getenv("PHYAI_NORM_FOLD");
+  if (!f || f[0] != '1') return false;
+  const int R = B * e.M;
+  if ((int64_t)(e.d / 32) * ((R + 15) / 16) > kFinCounters) return false;
+  for (int l = 0; l < e.L; ++l)
+    if (resid_split(e, 0, l, B) <= 1 || resid_split(e, 1, l, B) <= 1) return false;
+  return true;
+}
+
 // The residual contribution a split GEMM left pending, for its consumer.
 PendingResid pending_of(const phyai_expert& e, int which, int l, int k, int B) {
   PendingResid p{};
@@ -518,8 +547,27 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   const bool merge_in_o = oproj_merges(e, l, B);
   at.defer_merge = merge_in_o ? 1 : 0;
   // output projection: from the merged attention output, or from its key-split partials
+  // folded norms: the residual GEMMs finish their tiles (next norm's gain
+  // `gain`, null after the last block), the QKV and gate/up GEMMs scale rows
+  const bool fold = fold_norms(e, B);
+  auto with_fin = [&](GemmArgs ga, const float* gain) {
+    if (fold) {
+      ga.fin_h = e.h;
+      ga.fin_a = static_cast<bf16_t*>(e.n);
+      ga.fin_ss = e.ss;
+      ga.fin_gain = gain;
+      ga.fin_ctr = e.fin_ctr;
+    }
+    return ga;
+  };
+  auto with_rows = [&](GemmArgs ga) {
+    ga.row_ss = e.ss;
+    ga.row_nt = d / 32;
+    ga.row_eps = e.c.rms_eps;
+    return ga;
+  };
   auto oproj = [&](const EpiResid& er) {
-    const GemmArgs ga = with_split(gargs(w.o, o, e.qd, R), 0);
+    const GemmArgs ga = with_fin(with_split(gargs(w.o, o, e.qd, R), 0), w.mlp_norm);
     if (merge_in_o) gemm_merge_resid(ga, attention_parts(at), er, s);
     else gemm_resid(ga, er, s);
   };
@@ -537,13 +585,15 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
     }
     switch (stage) {
       case ST_NORM1: {
+        if (fold && l > 0) break;                 // done by the previous down projection
         const PendingResid pd = l > 0 ? pending_of(e, 1, l - 1, k, B) : PendingResid{};
         norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul1, sh1, pd, s);
         break;
       }
       case ST_QKV: {
         EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, e.c.rope, M, e.ldk, 1, e.rope_cs, e.desc};
-        gemm_qkv(with_lo(gargs(w.qkv, n, d, R), n_lo), eq, s);
+        const GemmArgs ga = with_lo(gargs(w.qkv, n, d, R), n_lo);
+        gemm_qkv(fold && l > 0 ? with_rows(ga) : ga, eq, s);
         break;
       }
       case ST_ATTN: {
@@ -555,12 +605,20 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
       }
       case ST_OPROJ: oproj(EpiResid{e.h, d, nullptr, nullptr}); break;
       case ST_NORM2:
+        if (fold) break;                          // done by the output projection
         norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_RMS, mul2, sh2, pending_of(e, 0, l, k, B), s);
         break;
-      case ST_MLP_UP: gemm_geglu(with_lo(gargs(w.gu, n, d, R), n_lo), EpiGeglu<T>{g, e.F, g_lo}, s); break;
-      case ST_MLP_DOWN:
-        gemm_resid(with_split(with_lo(gargs(w.down, g, e.F, R), g_lo), 1), EpiResid{e.h, d, nullptr, nullptr}, s);
+      case ST_MLP_UP: {
+        const GemmArgs ga = with_lo(gargs(w.gu, n, d, R), n_lo);
+        gemm_geglu(fold ? with_rows(ga) : ga, EpiGeglu<T>{g, e.F, g_lo}, s);
         break;
+      }
+      case ST_MLP_DOWN: {
+        const float* next = l + 1 < L ? e.layers[l + 1].attn_norm : nullptr;
+        gemm_resid(with_fin(with_split(with_lo(gargs(w.down, g, e.F, R), g_lo), 1), next),
+                   EpiResid{e.h, d, nullptr, nullptr}, s);
+        break;
+      }
     }
     return;
   }
@@ -674,7 +732,7 @@ void enqueue_loop(phyai_expert& e, int B, int K, hipStream_t s) {
     ro.h = e.h; ro.B = B; ro.H = H; ro.M = M; ro.off = e.off; ro.d = d; ro.A = e.A;
     ro.eps = e.c.rms_eps;
     ro.out_w = e.out_w; ro.out_b = e.out_b; ro.dt = e.dt + k; ro.x = e.x;
-    ro.pend = pending_of(e, 1, L - 1, k, B);
+    ro.pend = fold_norms(e, B) ? PendingResid{} : pending_of(e, 1, L - 1, k, B);
     embedded = k + 1 < K && readout_fuses_embedding(e.A, d, B * H, ro.pend.n > 0);
     if (embedded) {
       ro.has_next = 1;
@@ -1029,6 +1087,11 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
     HIPC(hipMemsetAsync(e->vt, 0, L * e->kv_layer * ab, s));
   }
   e->g = e->mem.alloc(Bm * M * F * ab);
+  if (c.variant == PHYAI_VARIANT_PI0 && !e->f32) {
+    e->ss = e->mem.alloc_n<float>(Bm * M * (d / 32));
+    e->fin_ctr = static_cast<unsigned*>(e->mem.alloc(kFinCounters * sizeof(unsigned)));
+    HIPC(hipMemsetAsync(e->fin_ctr, 0, kFinCounters * sizeof(unsigned), s));
+  }
   // pi0.5's adaRMS path amplifies the bf16 rounding of the normalised
   // activations and of the GeGLU output; those GEMM operands carry a second
   // bf16 term there (weights are still read once).
