@@ -1,7 +1,8 @@
 // Suffix-query attention over the frozen prefix K/V and the suffix tokens'
-// own K/V (the "50-token query against a longer prefix, head dimension 256"
-// shape of Section "PhyAI Architecture", paragraph "Profiled operator
-// selection"), with online softmax and an optional split over the keys.
+// own K/V, with online softmax and an optional split over the keys.  The
+// shape is the one the paper profiles for the action expert (section PhyAI
+// Architecture, paragraph Profiled operator selection): some fifty suffix
+// queries per head over a prefix of several hundred keys, head_dim 256.
 //
 // Key layout.  Per layer, request and kv head the library keeps one key
 // range: K row-major [key][D] and V transposed [D][key].  Keys
