@@ -1,4 +1,5 @@
-"""Oracle for the action-expert denoising loop (float64 NumPy).
+"""Oracle for the action-expert denoising loop and the prefix K/V producer
+(float64 NumPy).
 
 TEST INFRASTRUCTURE ONLY: a plain, slow, obviously correct CPU reference.
 Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's
@@ -10,6 +11,7 @@ paper), which is stated there.
 """
 from .expert import (DecodedWeights, denoise, pi05_condition, velocity_dit, velocity_pi0,
                      velocity_pi05)
+from .prefix_lm import prefill, prefill_request
 from .numerics import (E2M1_TABLE, E4M3FN_TABLE, attention, attention_bruteforce, decode_bf16,
                        decode_fp4, decode_fp8, decode_stored, euler, gelu_tanh, layer_normalize, rms_normalize, rope,
                        sinusoid, swish)
@@ -19,5 +21,5 @@ __all__ = [
     "E2M1_TABLE", "E4M3FN_TABLE", "attention", "attention_bruteforce", "decode_bf16", "decode_fp4",
     "decode_fp8",
     "decode_stored", "euler", "gelu_tanh", "layer_normalize", "rms_normalize", "rope", "sinusoid",
-    "swish",
+    "swish", "prefill", "prefill_request",
 ]

@@ -35,6 +35,7 @@ __all__ = [
     "make_prefix", "make_prefix_lengths", "make_noise", "make_state",
     "default_timesteps", "make_case", "bf16_bits_from_f32", "e4m3fn_encode",
     "quantize_fp8_per_column", "e2m1_encode", "quantize_fp4_groups", "FP4_GROUP", "TRUNK_LINEARS",
+    "make_prefix_embeds", "PrefillCase", "make_prefill_case",
 ]
 
 
@@ -44,7 +45,9 @@ class ExpertConfig:
 
     variant: ``pi0`` (time mixed into action tokens by an MLP), ``pi05``
     (adaRMSNorm time conditioning) or ``dit`` (DiT head with adaLN-zero,
-    alternating cross/self attention).
+    alternating cross/self attention); ``prefix_lm`` is the vision-language
+    model's language part run over the prefix tokens, which produces the
+    prefix K/V an expert reads (horizon, action_dim and n_steps are 0).
     """
     name: str
     cfg_id: int
@@ -135,6 +138,22 @@ CONFIGS: Dict[str, ExpertConfig] = {
         n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=4096, horizon=50,
         action_dim=32, n_steps=10, prefix_cap=816, prefix_min=816, prefix_max=816,
         batch=1, state_token=True, rope=True, weight_dtype="fp4", kv_dtype="bf16"),
+    # The language part of the vision-language model over the prefix tokens
+    # (image tokens and text), producing the prefix K/V the expert reads: a
+    # tiny fp32 one whose output fits the tiny expert, and a Gemma-class one
+    # (18 layers of width 2048, 8 query heads and one K/V head of 256, GeGLU
+    # MLP 16384) over the pi0 prefix of 816 tokens, whose output fits the
+    # pi0-shaped expert.
+    "plm_tiny_fp32": _cfg(
+        name="plm_tiny_fp32", cfg_id=7, variant="prefix_lm", n_layers=2, d_model=256,
+        n_q_heads=4, n_kv_heads=1, head_dim=64, d_mlp=1024, horizon=0,
+        action_dim=0, n_steps=0, prefix_cap=64, prefix_min=64, prefix_max=64,
+        batch=1, state_token=False, rope=True, weight_dtype="f32", kv_dtype="f32", time_dim=0),
+    "plm_gemma_bf16_b1": _cfg(
+        name="plm_gemma_bf16_b1", cfg_id=8, variant="prefix_lm", n_layers=18, d_model=2048,
+        n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=16384, horizon=0,
+        action_dim=0, n_steps=0, prefix_cap=816, prefix_min=816, prefix_max=816,
+        batch=1, state_token=False, rope=True, weight_dtype="bf16", kv_dtype="bf16", time_dim=0),
 }
 
 # Per-layer linears that carry the fp8 / fp4 format when weight_dtype is one of those.
@@ -264,6 +283,22 @@ def weight_specs(cfg: ExpertConfig) -> Dict[str, tuple]:
     qd = cfg.n_q_heads * cfg.head_dim
     kd = cfg.n_kv_heads * cfg.head_dim
     s: Dict[str, tuple] = {}
+    if cfg.variant == "prefix_lm":
+        # the last layer's K/V depend only on its input: its output
+        # projection and MLP are never needed and not listed
+        for l in range(cfg.n_layers):
+            p = f"layers.{l}."
+            s[p + "attn_norm"] = (1, d)
+            s[p + "wq"] = (d, qd)
+            s[p + "wk"] = (d, kd)
+            s[p + "wv"] = (d, kd)
+            if l + 1 < cfg.n_layers:
+                s[p + "wo"] = (qd, d)
+                s[p + "mlp_norm"] = (1, d)
+                s[p + "w_gate"] = (d, F)
+                s[p + "w_up"] = (d, F)
+                s[p + "w_down"] = (F, d)
+        return s
     s["in_w"] = (A, d)
     s["in_b"] = (1, d)
     if cfg.variant == "pi0":
@@ -351,16 +386,25 @@ def make_weights(cfg: ExpertConfig, seed: int = 0,
     """Every parameter ~ N(0, init_std) in float32, then stored in the config's
     format.  ``overrides`` replaces named float32 masters before storage (used
     by tests that zero or plant specific weights)."""
-    out: Dict[str, StoredTensor] = {}
     overrides = overrides or {}
-    for name, (r, c) in weight_specs(cfg).items():
+    specs = weight_specs(cfg)
+
+    def one(name):
+        r, c = specs[name]
         if name in overrides:
             x = np.asarray(overrides[name], dtype=np.float32).reshape(r, c)
         else:
             g = _rng(seed, cfg.cfg_id, 0, zlib.crc32(name.encode()))
             x = g.standard_normal((r, c), dtype=np.float32) * np.float32(cfg.init_std)
-        out[name] = _store(x, storage_dtype(cfg, name))
-    return out
+        return _store(x, storage_dtype(cfg, name))
+
+    # each tensor has its own stream, so the order of generation does not
+    # matter; NumPy's generators and array kernels release the GIL
+    from concurrent.futures import ThreadPoolExecutor
+    import os
+    with ThreadPoolExecutor(max_workers=min(16, os.cpu_count() or 1)) as ex:
+        stored = list(ex.map(one, specs))
+    return dict(zip(specs, stored))
 
 
 def make_prefix_lengths(cfg: ExpertConfig, seed: int = 0, batch: Optional[int] = None) -> np.ndarray:
@@ -407,6 +451,20 @@ def make_prefix(cfg: ExpertConfig, prefix_len: np.ndarray, seed: int = 0,
                     buf[l, kv, i, :n] = bf16_bits_from_f32(blk) if bf else blk
                     buf[l, kv, i, n:] = pad
     return buf
+
+
+def make_prefix_embeds(cfg: ExpertConfig, prefix_len: np.ndarray, seed: int = 0,
+                       requests=None, pad_value: float = 0.0) -> np.ndarray:
+    """Input of a prefix LM: the prefix token embeddings, float32
+    [B][P_cap][d_model]; valid rows ~ N(0, 1), rows at or beyond
+    prefix_len[b] hold ``pad_value``."""
+    reqs = list(range(len(prefix_len))) if requests is None else list(requests)
+    out = np.empty((len(reqs), cfg.prefix_cap, cfg.d_model), dtype=np.float32)
+    for i, b in enumerate(reqs):
+        n = int(prefix_len[b])
+        out[i, :n] = _rng(seed, cfg.cfg_id, 6, b).standard_normal((n, cfg.d_model), dtype=np.float32)
+        out[i, n:] = pad_value
+    return out
 
 
 def make_noise(cfg: ExpertConfig, seed: int = 0, requests=None, batch=None) -> np.ndarray:
@@ -457,3 +515,21 @@ def make_case(cfg: ExpertConfig, seed: int = 0, batch: Optional[int] = None,
                 noise=make_noise(cfg, seed, batch=B),
                 state=make_state(cfg, seed, batch=B),
                 timesteps=default_timesteps(cfg.n_steps))
+
+
+@dataclasses.dataclass
+class PrefillCase:
+    cfg: ExpertConfig
+    weights: Dict[str, StoredTensor]
+    embeds: np.ndarray
+    prefix_len: np.ndarray
+
+
+def make_prefill_case(cfg: ExpertConfig, seed: int = 0, batch: Optional[int] = None,
+                      weights: Optional[Dict[str, StoredTensor]] = None) -> PrefillCase:
+    B = cfg.batch if batch is None else batch
+    plen = make_prefix_lengths(cfg, seed, B)
+    return PrefillCase(cfg=cfg,
+                       weights=weights if weights is not None else make_weights(cfg, seed),
+                       embeds=make_prefix_embeds(cfg, plen, seed),
+                       prefix_len=plen)
