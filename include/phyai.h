@@ -46,7 +46,9 @@ typedef enum {
 typedef enum {
   PHYAI_VARIANT_PI0 = 0,    /* time mixed into action tokens by a 2-layer MLP; optional state token */
   PHYAI_VARIANT_PI05 = 1,   /* adaRMSNorm timestep conditioning in every norm                      */
-  PHYAI_VARIANT_DIT = 2     /* DiT head: adaLN-zero, alternating cross/self attention              */
+  PHYAI_VARIANT_DIT = 2,    /* DiT head: adaLN-zero, alternating cross/self attention              */
+  PHYAI_VARIANT_PREFIX_LM = 3  /* the VLM's language part over the prefix tokens, producing the prefix
+                                  K/V cache the pi0 / pi0.5 experts read (see phyai_prefill)        */
 } phyai_variant;
 
 typedef enum {
@@ -89,6 +91,15 @@ typedef struct {
   float sin_max_period;
   float rope_base;          /* 10000                                                              */
 } phyai_config;
+
+/* PHYAI_VARIANT_PREFIX_LM uses n_layers, d_model, n_q_heads, n_kv_heads,
+ * head_dim, d_mlp, prefix_cap (rows per request: the prefix tokens),
+ * max_batch, rope (RoPE on queries and keys at positions 0 .. prefix_len-1),
+ * weight_dtype, kv_dtype, rms_eps and rope_base; horizon, action_dim,
+ * max_steps, time_dim and the sinusoid periods are ignored, state_token and
+ * d_feat must be 0, prefix_cap >= 1.  Its blocks are the pi0 trunk's
+ * (RMSNorm with gain (1 + w), fused QKV, GeGLU MLP, residual adds) with a
+ * bidirectional mask over the valid prefix tokens. */
 
 /* One named parameter, stored [rows][cols] row-major on the host.  Linear
  * weights are [in][out] (y = x W + b); vectors have rows = 1.  dtype must be
@@ -133,6 +144,10 @@ typedef struct phyai_expert phyai_expert;
  *          layers.l.ada_w [d][6d], ada_b [1][6d], layers.l.mlp_w1 [d][F],
  *          mlp_b1 [1][F], mlp_w2 [F][d], mlp_b2 [1][d],
  *          final_ada_w [d][2d], final_ada_b [1][2d]
+ *   PREFIX_LM: layers.l.{attn_norm [1][d], wq, wk, wv} for every layer and
+ *          layers.l.{wo, mlp_norm, w_gate, w_up, w_down} for every layer but
+ *          the last (whose keys and values depend only on its input); no
+ *          in/out, time or state tensors
  * Host buffers may be freed after the call returns.  On failure *out is set
  * to NULL and nothing is leaked.  The call synchronises `stream`. */
 int phyai_load_expert(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_tensors,
@@ -204,6 +219,39 @@ int phyai_denoise(phyai_expert* e, const void* prefix, const int32_t* prefix_len
 int phyai_denoise_static(phyai_expert* e, const void* prefix, const int32_t* prefix_len,
                          const float* noise, const float* timesteps, int32_t n_steps, int32_t batch,
                          const float* state, float* out_actions, void* stream);
+
+/* Produce the frozen prefix K/V cache of a batch of requests from their
+ * prefix token embeddings (handle of variant PHYAI_VARIANT_PREFIX_LM).
+ *
+ * Operation: the language-prefix phase of the pi-family, which the paper
+ * times separately from the vision tower and the action expert (Section
+ * "Evaluation", batch analysis of PI0.5) and whose per-layer K/V the action
+ * expert reads unchanged at every denoising step (Section "PhyAI
+ * Architecture", paragraph "Graph replay").  For every layer l and valid
+ * prefix token t: the keys (rotated at position t when rope = 1) and values
+ * of that layer's K/V projection, after layers 0 .. l-1 have run over all
+ * valid tokens of the request with bidirectional attention.
+ *
+ *   embeds      device float32 [B][prefix_cap][d_model]: the prefix token
+ *               embeddings (image tokens and text, already scaled), the
+ *               input of layer 0.  Rows at or beyond prefix_len[b] are never
+ *               read.
+ *   prefix_len  host [B], 0 <= prefix_len[b] <= prefix_cap.
+ *   kv_out      device, [L][2][B][prefix_cap][n_kv*head_dim] in kv_dtype
+ *               (index 0 = K, 1 = V): exactly the `prefix` argument of
+ *               phyai_denoise for an expert with the same n_layers, n_kv_heads,
+ *               head_dim and prefix_cap.  Rows at or beyond prefix_len[b] are
+ *               written as zeros.  Caller-owned.
+ *   batch       B, 1 <= B <= max_batch.
+ *   stream      work is enqueued on it; the call returns after enqueueing.
+ *
+ * embeds and kv_out must be 16-byte aligned.  Calls on one handle must be
+ * ordered on the device (they share its working buffers).  Errors:
+ * PHYAI_EINVAL for a NULL or non-prefix-LM handle, a NULL or misaligned
+ * pointer, a batch or prefix length out of range; PHYAI_EHIP if a launch
+ * fails.  The denoising entry points refuse a prefix-LM handle. */
+int phyai_prefill(phyai_expert* e, const float* embeds, const int32_t* prefix_len, void* kv_out, int32_t batch,
+                  void* stream);
 
 /* Capture the graph of the K-step loop for the (batch, n_steps) bucket ahead
  * of the first phyai_denoise with that shape, so that the first prediction

@@ -17,13 +17,13 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libphyai.so")
 
 PHYAI_OK, PHYAI_EINVAL, PHYAI_ENOMEM, PHYAI_EHIP, PHYAI_EUNSUPPORTED = 0, -1, -2, -3, -4
-_VARIANT = {"pi0": 0, "pi05": 1, "dit": 2}
+_VARIANT = {"pi0": 0, "pi05": 1, "dit": 2, "prefix_lm": 3}
 _DTYPE = {"f32": 0, "bf16": 1, "fp8": 2, "fp4": 3}
 
 # Every symbol include/phyai.h declares.
 EXPORTS = ("phyai_load_expert", "phyai_denoise", "phyai_denoise_static", "phyai_prepare", "phyai_debug_hidden",
            "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_free_expert", "phyai_last_error",
-           "phyai_version")
+           "phyai_version", "phyai_prefill")
 STAGES = {"norm1": 0, "qkv": 1, "attn": 2, "oproj": 3, "norm2": 4, "mlp_up": 5, "mlp_down": 6}
 
 
@@ -65,11 +65,12 @@ def lib() -> ctypes.CDLL:
         L.phyai_debug_hidden.argtypes = [vp, vp, i32, vp]
         L.phyai_fp8_to_bf16.argtypes = [vp, vp, i64, vp]
         L.phyai_profile_stage.argtypes = [vp, i32, i32, vp]
+        L.phyai_prefill.argtypes = [vp, vp, vp, vp, i32, vp]
         L.phyai_free_expert.argtypes = [vp]
         L.phyai_free_expert.restype = None
         L.phyai_last_error.restype = ctypes.c_char_p
         for f in ("phyai_load_expert", "phyai_denoise", "phyai_denoise_static", "phyai_prepare", "phyai_debug_hidden",
-                  "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_version"):
+                  "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_version", "phyai_prefill"):
             getattr(L, f).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -109,6 +110,26 @@ def make_config(cfg, max_batch: Optional[int] = None, max_steps: Optional[int] =
         rope_base=cfg.rope_base)
 
 
+def _tensor_array(weights: Dict[str, object]):
+    """The C tensor list of a weight dict (and the host arrays it points into)."""
+    keep = []
+    arr = (Tensor * len(weights))()
+    for i, (name, t) in enumerate(weights.items()):
+        data = np.ascontiguousarray(t.data)
+        keep.append(data)
+        sc = None
+        if t.scale is not None:
+            sc = np.ascontiguousarray(t.scale, dtype=np.float32)
+            keep.append(sc)
+        nm = name.encode()
+        keep.append(nm)
+        # fp4 data holds two codes per byte: the logical width is twice its columns
+        cols = data.shape[1] * (2 if t.dtype == "fp4" else 1)
+        arr[i] = Tensor(nm, _DTYPE[t.dtype], data.shape[0], cols, data.ctypes.data,
+                        None if sc is None else sc.ctypes.data)
+    return arr, keep
+
+
 class Expert:
     """One loaded expert (owns its device weights, buffers and graphs)."""
 
@@ -116,23 +137,10 @@ class Expert:
                  max_steps: Optional[int] = None, stream=None):
         self.cfg = cfg
         c = make_config(cfg, max_batch, max_steps)
-        keep = []
-        arr = (Tensor * len(weights))()
-        for i, (name, t) in enumerate(weights.items()):
-            data = np.ascontiguousarray(t.data)
-            keep.append(data)
-            sc = None
-            if t.scale is not None:
-                sc = np.ascontiguousarray(t.scale, dtype=np.float32)
-                keep.append(sc)
-            nm = name.encode()
-            keep.append(nm)
-            # fp4 data holds two codes per byte: the logical width is twice its columns
-            cols = data.shape[1] * (2 if t.dtype == "fp4" else 1)
-            arr[i] = Tensor(nm, _DTYPE[t.dtype], data.shape[0], cols, data.ctypes.data,
-                            None if sc is None else sc.ctypes.data)
+        arr, keep = _tensor_array(weights)
         h = ctypes.c_void_p()
         _check(lib().phyai_load_expert(ctypes.byref(c), arr, len(weights), _stream(stream), ctypes.byref(h)))
+        del keep
         self._h = h
 
     def prepare(self, batch: int, n_steps: int, stream=None):
@@ -167,6 +175,55 @@ class Expert:
 
     def profile_stage(self, stage: str, reps: int, stream=None):
         """Enqueue `reps` passes over all layers of one block stage (for timing)."""
+        _check(lib().phyai_profile_stage(self._h, STAGES[stage], reps, _stream(stream)))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().phyai_free_expert(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class PrefixLM:
+    """One loaded prefix LM (variant ``prefix_lm``): prefix token embeddings in,
+    the prefix K/V cache an expert reads out (``phyai_prefill``)."""
+
+    def __init__(self, cfg, weights: Dict[str, object], max_batch: Optional[int] = None, stream=None):
+        if cfg.variant != "prefix_lm":
+            raise ValueError("PrefixLM needs a prefix_lm config")
+        self.cfg = cfg
+        c = make_config(cfg, max_batch, 0)
+        arr, keep = _tensor_array(weights)
+        h = ctypes.c_void_p()
+        _check(lib().phyai_load_expert(ctypes.byref(c), arr, len(weights), _stream(stream), ctypes.byref(h)))
+        del keep
+        self._h = h
+
+    def prefill(self, embeds, prefix_len, out=None, stream=None):
+        """embeds: device float32 [B][prefix_cap][d]; prefix_len: host array.
+        Returns (or fills) the device K/V cache [L][2][B][prefix_cap][n_kv*d_h]
+        (bf16 bit patterns as int16, or float32 on the fp32 path)."""
+        c = self.cfg
+        plen = np.ascontiguousarray(prefix_len, dtype=np.int32)
+        B = int(embeds.shape[0])
+        if plen.shape[0] < B:
+            raise ValueError("prefix_len shorter than the batch")
+        if out is None:
+            import torch
+            dt = torch.float32 if c.kv_dtype == "f32" else torch.int16
+            out = torch.empty((c.n_layers, 2, B, c.prefix_cap, c.n_kv_heads * c.head_dim), dtype=dt,
+                              device=embeds.device)
+        _check(lib().phyai_prefill(self._h, _ptr(embeds), plen.ctypes.data, _ptr(out), B, _stream(stream)))
+        return out
+
+    def profile_stage(self, stage: str, reps: int, stream=None):
+        """Enqueue `reps` passes over the layers of one block stage (timing aid;
+        needs a previous prefill)."""
         _check(lib().phyai_profile_stage(self._h, STAGES[stage], reps, _stream(stream)))
 
     def close(self):

@@ -593,6 +593,49 @@ __global__ __launch_bounds__(256) void prefix_relayout_kernel(RelayoutArgs r) {
   }
 }
 
+// The prefix LM's keys and values of one layer back into the caller's prefix
+// layout, the inverse of prefix_relayout_kernel.  Block: 64 keys x D of one
+// (request, kv head).  The V^T tile comes into LDS as 16-byte runs along the
+// keys (the key range holds whole 64-key tiles) and leaves as rows; K rows
+// are copied; keys at or beyond prefix_len[b] (up to P) leave as zeros.
+template <typename T, int D>
+__global__ __launch_bounds__(256) void kv_export_kernel(KvExportArgs r) {
+  constexpr int VE = 16 / sizeof(T);           // elements per 16-byte move
+  constexpr int KC = 64 / VE;                  // 16-byte runs per V^T row of the tile
+  constexpr int CPR = D / VE;                  // 16-byte chunks per key row
+  __shared__ __attribute__((aligned(16))) T tile[D][64 + VE];
+  const int key0 = blockIdx.x * 64;
+  const int grp = blockIdx.y;                  // b * nkv + kvh
+  const int b = grp / r.nkv, kvh = grp % r.nkv;
+  const int plen = r.desc->prefix_len[b];
+  const int W = r.nkv * D;
+  const T* ks = static_cast<const T*>(r.K) + (int64_t)grp * r.ldk * D;
+  const T* vs = static_cast<const T*>(r.Vt) + (int64_t)grp * r.ldk * D;
+  T* ko = static_cast<T*>(r.out) + (int64_t)b * r.P * W + kvh * D;
+  T* vo = ko + r.half;
+  for (int i = threadIdx.x; i < D * KC; i += 256) {
+    const int d = i / KC, k = (i % KC) * VE;
+    *reinterpret_cast<uint4*>(&tile[d][k]) = *reinterpret_cast<const uint4*>(vs + (int64_t)d * r.ldk + key0 + k);
+  }
+  __syncthreads();
+  const int nk = min(64, r.P - key0);
+  for (int i = threadIdx.x; i < 64 * CPR; i += 256) {
+    const int kr = i / CPR, c = (i % CPR) * VE;
+    if (kr >= nk) continue;
+    const int key = key0 + kr;
+    uint4 kw = make_uint4(0, 0, 0, 0), vw = make_uint4(0, 0, 0, 0);
+    if (key < plen) {
+      kw = *reinterpret_cast<const uint4*>(ks + (int64_t)key * D + c);
+      __attribute__((aligned(16))) T run[VE];
+#pragma unroll
+      for (int e = 0; e < VE; ++e) run[e] = tile[c + e][kr];
+      vw = *reinterpret_cast<const uint4*>(run);
+    }
+    *reinterpret_cast<uint4*>(ko + (int64_t)key * W + c) = kw;
+    *reinterpret_cast<uint4*>(vo + (int64_t)key * W + c) = vw;
+  }
+}
+
 }  // namespace
 
 // Query rows per block: 128 (4 waves), or 64 (2 waves) when the 128-row
@@ -689,5 +732,17 @@ static void relayout_t(const RelayoutArgs& r, hipStream_t s) {
 
 void prefix_relayout_bf16(const RelayoutArgs& r, hipStream_t s) { relayout_t<bf16_t>(r, s); }
 void prefix_relayout_f32(const RelayoutArgs& r, hipStream_t s) { relayout_t<float>(r, s); }
+
+template <typename T>
+static void kv_export_t(const KvExportArgs& r, hipStream_t s) {
+  if (r.P <= 0 || r.B <= 0) return;
+  dim3 grid((r.P + 63) / 64, r.B * r.nkv);
+  if (r.D == 256) hipLaunchKernelGGL((kv_export_kernel<T, 256>), grid, dim3(256), 0, s, r);
+  else if (r.D == 128) hipLaunchKernelGGL((kv_export_kernel<T, 128>), grid, dim3(256), 0, s, r);
+  else if (r.D == 64) hipLaunchKernelGGL((kv_export_kernel<T, 64>), grid, dim3(256), 0, s, r);
+}
+
+void kv_export_bf16(const KvExportArgs& r, hipStream_t s) { kv_export_t<bf16_t>(r, s); }
+void kv_export_f32(const KvExportArgs& r, hipStream_t s) { kv_export_t<float>(r, s); }
 
 }  // namespace phyai

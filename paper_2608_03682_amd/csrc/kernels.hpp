@@ -478,6 +478,22 @@ struct RelayoutArgs {
 void prefix_relayout_bf16(const RelayoutArgs&, hipStream_t);
 void prefix_relayout_f32(const RelayoutArgs&, hipStream_t);
 
+// The prefix LM's keys and values of one layer, out of the library's key
+// ranges (K [ldk][D], V transposed [D][ldk] per request and kv head) into the
+// caller's prefix layout [2][B][P][nkv*D] (`out` points at the layer's
+// block; the V half starts `half` elements later): the layout the denoising
+// loop reads back as its frozen prefix.  Keys at or beyond prefix_len[b]
+// are written as zeros.
+struct KvExportArgs {
+  const CallDesc* desc;
+  const void* K; const void* Vt;
+  void* out;
+  int64_t half;
+  int B, P, nkv, D, ldk;
+};
+void kv_export_bf16(const KvExportArgs&, hipStream_t);
+void kv_export_f32(const KvExportArgs&, hipStream_t);
+
 // ---------------------------------------------------------------------------
 // Row kernels
 // ---------------------------------------------------------------------------
@@ -534,9 +550,17 @@ bool readout_fuses_embedding(int A, int d, int rows, bool pending);
 void copy_noise_to_state(const CallDesc* desc, float* x, int64_t n, hipStream_t);
 void copy_state_to_out(const CallDesc* desc, const float* x, int64_t n, hipStream_t);
 void set_call_desc(const CallDesc& host_desc, CallDesc* dev, hipStream_t);
-// RoPE table of one call: tab[b*M + t][i] = (cos, sin)((prefix_len[b] + t) * inv_freq[i]),
-// i < D/2 (positions of the suffix tokens follow their request's prefix).
-void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B, int M, int D, hipStream_t);
+// RoPE table of one call: tab[b*M + t][i] = (cos, sin)((p0 + t) * inv_freq[i]),
+// i < D/2, with p0 = prefix_len[b] when pos_after_prefix (the suffix tokens'
+// positions follow their request's prefix) and 0 otherwise (the prefix
+// tokens themselves).
+void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B, int M, int D, int pos_after_prefix,
+                hipStream_t);
+// Residual stream of the prefix LM from the caller's embeddings:
+// h[b*M + t] = embeds[b][t] for t < prefix_len[b], zero after (the caller's
+// rows past the prefix are never read).  d a multiple of 4, embeds 16-byte
+// aligned.
+void prefill_embed(const CallDesc* desc, const float* embeds, float* h, int B, int M, int d, hipStream_t);
 void fp8_to_bf16(const uint8_t* codes, bf16_t* out, int64_t n, hipStream_t);
 
 // ---------------------------------------------------------------------------

@@ -717,15 +717,24 @@ __global__ __launch_bounds__(256) void readout_rows_kernel(ReadoutArgs r) {
 }
 
 __global__ __launch_bounds__(128) void rope_table_kernel(const CallDesc* desc, const float* inv_freq, float2* tab,
-                                                        int M, int half) {
+                                                        int M, int half, int after_prefix) {
   const int row = blockIdx.x;                    // b*M + t
   const int b = row / M, t = row % M;
-  const float pos = (float)(desc->prefix_len[b] + t);
+  const float pos = (float)((after_prefix ? desc->prefix_len[b] : 0) + t);
   for (int i = threadIdx.x; i < half; i += blockDim.x) {
     float sn, cs;
     sincosf(pos * inv_freq[i], &sn, &cs);
     tab[(int64_t)row * half + i] = make_float2(cs, sn);
   }
+}
+
+__global__ __launch_bounds__(256) void prefill_embed_kernel(const CallDesc* desc, const float* embeds, float* h,
+                                                           int M, int d) {
+  const int row = blockIdx.x;                    // b*M + t
+  const bool valid = row % M < desc->prefix_len[row / M];
+  const float4* src = reinterpret_cast<const float4*>(embeds + (int64_t)row * d);
+  float4* dst = reinterpret_cast<float4*>(h + (int64_t)row * d);
+  for (int i = threadIdx.x; i < d / 4; i += 256) dst[i] = valid ? src[i] : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
 __global__ void copy_in_kernel(const CallDesc* desc, float* x, int64_t n) {
@@ -826,8 +835,13 @@ void copy_noise_to_state(const CallDesc* desc, float* x, int64_t n, hipStream_t 
 void copy_state_to_out(const CallDesc* desc, const float* x, int64_t n, hipStream_t s) {
   hipLaunchKernelGGL(copy_out_kernel, dim3((n + 255) / 256), dim3(256), 0, s, desc, x, n);
 }
-void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B, int M, int D, hipStream_t s) {
-  hipLaunchKernelGGL(rope_table_kernel, dim3(B * M), dim3(128), 0, s, desc, inv_freq, tab, M, D / 2);
+void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B, int M, int D, int pos_after_prefix,
+                hipStream_t s) {
+  hipLaunchKernelGGL(rope_table_kernel, dim3(B * M), dim3(128), 0, s, desc, inv_freq, tab, M, D / 2,
+                     pos_after_prefix);
+}
+void prefill_embed(const CallDesc* desc, const float* embeds, float* h, int B, int M, int d, hipStream_t s) {
+  if (B * M > 0) hipLaunchKernelGGL(prefill_embed_kernel, dim3(B * M), dim3(256), 0, s, desc, embeds, h, M, d);
 }
 void set_call_desc(const CallDesc& d, CallDesc* dev, hipStream_t s) {
   hipLaunchKernelGGL(set_desc_kernel, dim3(1), dim3(256), 0, s, d, dev);

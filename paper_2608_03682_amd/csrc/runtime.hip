@@ -532,6 +532,9 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
     return ga;
   };
   const int variant = e.c.variant;
+  // a prefix LM's rows are the prefix tokens: keys at positions 0 .. M-1,
+  // every valid token sees every valid token
+  const bool plm = variant == PHYAI_VARIANT_PREFIX_LM;
   const int S = 2 * L + 1;   // pi0.5 norm sites
   const LayerW& w = e.layers[l];
   const float inv_sqrt_d = 1.0f / std::sqrt((float)D);
@@ -591,14 +594,14 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
         break;
       }
       case ST_QKV: {
-        EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, e.c.rope, M, e.ldk, 1, e.rope_cs, e.desc};
+        EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, e.c.rope, M, e.ldk, plm ? 0 : 1, e.rope_cs, e.desc};
         const GemmArgs ga = with_lo(gargs(w.qkv, n, d, R), n_lo);
         gemm_qkv(fold && l > 0 ? with_rows(ga) : ga, eq, s);
         break;
       }
       case ST_ATTN: {
         at.keys_from_prefix = 1;
-        at.n_suffix = M;
+        at.n_suffix = plm ? 0 : M;
         at.mask_mode = e.c.state_token ? 1 : 0;
         if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
         break;
@@ -663,7 +666,7 @@ void enqueue_prologue(phyai_expert& e, int B, hipStream_t s) {
   const int d = e.d, M = e.M, H = e.H, L = e.L;
   const int variant = e.c.variant;
   copy_noise_to_state(e.desc, e.x, (int64_t)B * H * e.A, s);
-  if (e.c.rope) rope_table(e.desc, e.inv_freq, e.rope_cs, B, M, e.D, s);
+  if (e.c.rope) rope_table(e.desc, e.inv_freq, e.rope_cs, B, M, e.D, 1, s);
   if (e.c.state_token) embed_state(e.desc, e.state_w, e.state_b, e.e_state, B, e.A, d, s);
   if (variant == PHYAI_VARIANT_DIT) {
     // request-local cross-attention K/V: project the VLM features once per call
@@ -899,23 +902,54 @@ void enqueue_persist(phyai_expert& e, int K, hipStream_t s) {
   }
 }
 
+// The prefix LM over B requests: embeddings into the residual stream, the
+// RoPE table of positions 0 .., then per layer the norm, the QKV projection
+// (+ RoPE, K/V into the key range), the export of the layer's K/V into the
+// caller's buffer, and (all but the last layer) attention, the output
+// projection, the MLP norm and the MLP.  Eager launches: one pass per call,
+// dominated by its GEMMs.
+template <typename T>
+void enqueue_prefill(phyai_expert& e, const float* embeds, void* kv_out, int B, hipStream_t s) {
+  const int L = e.L;
+  prefill_embed(e.desc, embeds, e.h, B, e.M, e.d, s);
+  if (e.c.rope) rope_table(e.desc, e.inv_freq, e.rope_cs, B, e.M, e.D, 0, s);
+  const int64_t half = (int64_t)B * e.M * e.kd;          // one of K, V of one layer, caller layout
+  for (int l = 0; l < L; ++l) {
+    layer_stage<T>(e, ST_NORM1, l, 0, B, s);
+    layer_stage<T>(e, ST_QKV, l, 0, B, s);
+    KvExportArgs ka{e.desc, static_cast<T*>(e.kall) + (int64_t)l * e.kv_layer,
+                    static_cast<T*>(e.vt) + (int64_t)l * e.kv_layer,
+                    static_cast<T*>(kv_out) + (int64_t)l * 2 * half, half, B, e.M, e.nkv, e.D, e.ldk};
+    if (e.f32) kv_export_f32(ka, s); else kv_export_bf16(ka, s);
+    if (l + 1 == L) break;
+    for (int st : {ST_ATTN, ST_OPROJ, ST_NORM2, ST_MLP_UP, ST_MLP_DOWN}) layer_stage<T>(e, st, l, 0, B, s);
+  }
+}
+
 void check_config(const phyai_config& c) {
   auto req = [](bool ok, const std::string& m) { if (!ok) fail(PHYAI_EINVAL, m); };
-  req(c.variant >= 0 && c.variant <= 2, "variant out of range");
+  req(c.variant >= 0 && c.variant <= 3, "variant out of range");
   req(c.n_layers >= 1 && c.d_model >= 64 && c.n_q_heads >= 1 && c.n_kv_heads >= 1, "non-positive size");
   req(c.n_q_heads % c.n_kv_heads == 0, "n_q_heads must be a multiple of n_kv_heads");
   req(c.head_dim == 64 || c.head_dim == 128 || c.head_dim == 256, "head_dim must be 64, 128 or 256");
   // the row kernels take whole 256-column groups per thread block
   req(c.d_model % 256 == 0 && c.d_model <= 2048, "d_model must be a multiple of 256, at most 2048");
   req(c.d_mlp >= 64 && c.d_mlp % 64 == 0, "d_mlp must be a positive multiple of 64");
-  req(c.horizon >= 1 && c.action_dim >= 1 && c.action_dim <= 64, "horizon >= 1 and 1 <= action_dim <= 64");
-  req(c.max_steps >= 1 && c.max_steps <= 1024, "max_steps out of range");
   req(c.max_batch >= 1 && c.max_batch <= kMaxBatch, "max_batch out of range (1..512)");
   req(c.prefix_cap >= 0, "prefix_cap < 0");
-  req(c.time_dim >= 4 && c.time_dim % 64 == 0, "time_dim must be a multiple of 64");
   req(c.weight_dtype >= 0 && c.weight_dtype <= 3, "weight_dtype out of range");
   req(c.rms_eps > 0.f, "rms_eps must be positive");
-  req(c.sin_min_period > 0.f && c.sin_max_period > 0.f, "sinusoid periods must be positive");
+  if (c.variant == PHYAI_VARIANT_PREFIX_LM) {
+    // the prefix tokens are the model's rows: no actions, steps or timestep
+    // tables; keys and values per layer leave in the prefix layout
+    req(c.prefix_cap >= 1, "a prefix LM needs prefix_cap >= 1 rows");
+    req(c.state_token == 0 && c.d_feat == 0, "a prefix LM has no state token and no feature input");
+  } else {
+    req(c.horizon >= 1 && c.action_dim >= 1 && c.action_dim <= 64, "horizon >= 1 and 1 <= action_dim <= 64");
+    req(c.max_steps >= 1 && c.max_steps <= 1024, "max_steps out of range");
+    req(c.time_dim >= 4 && c.time_dim % 64 == 0, "time_dim must be a multiple of 64");
+    req(c.sin_min_period > 0.f && c.sin_max_period > 0.f, "sinusoid periods must be positive");
+  }
   const bool f32 = c.weight_dtype == PHYAI_DTYPE_F32;
   req(c.kv_dtype == (f32 ? PHYAI_DTYPE_F32 : PHYAI_DTYPE_BF16),
       "kv_dtype must be F32 on the fp32 path and BF16 on the bf16/fp8/fp4 path");
@@ -930,6 +964,90 @@ void check_config(const phyai_config& c) {
   req(qd % 64 == 0, "n_q_heads * head_dim must be a multiple of 64");
 }
 
+// Layers whose output projection and MLP exist: a prefix LM's last layer
+// only projects its keys and values.
+int full_layers(const phyai_expert& e) {
+  return e.c.variant == PHYAI_VARIANT_PREFIX_LM ? e.L - 1 : e.L;
+}
+
+// The prefix LM: the same blocks as the pi0 trunk over M = prefix_cap rows
+// per request (the prefix tokens), keys written at positions 0.., no
+// timestep tables.  Tensors: layers.l.{attn_norm, wq, wk, wv} for every
+// layer, layers.l.{wo, mlp_norm, w_gate, w_up, w_down} for all but the last.
+void load_prefix_lm(const phyai_tensor* tensors, int32_t n_tensors, hipStream_t s, phyai_expert* e) {
+  const phyai_config& c = e->c;
+  e->F = c.d_mlp;
+  e->H = 0; e->A = 0; e->off = 0;
+  e->M = c.prefix_cap;
+  e->P = 0;                 // no prefix of its own: its keys are its rows
+  e->qd = e->nq * e->D; e->kd = e->nkv * e->D;
+  e->Bmax = c.max_batch; e->Kmax = 0;
+  e->Wpre = e->kd;
+  const int d = e->d, L = e->L, D = e->D, F = e->F;
+  Params P;
+  for (int i = 0; i < n_tensors; ++i) {
+    if (!tensors[i].name) fail(PHYAI_EINVAL, "tensor with NULL name");
+    P.by_name[tensors[i].name] = &tensors[i];
+  }
+  const int wk_trunk = e->f32                                   ? W_F32
+                       : c.weight_dtype == PHYAI_DTYPE_FP8E4M3 ? W_FP8
+                       : c.weight_dtype == PHYAI_DTYPE_FP4E2M1 ? W_FP4 : W_BF16;
+  auto vec = [&](const std::string& n, int len) { return upload_f32(*e, P.get(n, 1, len), s); };
+  e->layers.resize(L);
+  for (int l = 0; l < L; ++l) {
+    LayerW& w = e->layers[l];
+    const std::string p = "layers." + std::to_string(l) + ".";
+    w.attn_norm = vec(p + "attn_norm", d);
+    w.qkv = pack_heads(*e, {P.get(p + "wq", d, e->qd), P.get(p + "wk", d, e->kd), P.get(p + "wv", d, e->kd)}, D,
+                       wk_trunk, s);
+    if (l + 1 == L) break;
+    w.o = pack_identity(*e, {P.get(p + "wo", e->qd, d)}, wk_trunk, s);
+    w.mlp_norm = vec(p + "mlp_norm", d);
+    w.gu = pack_geglu(*e, P.get(p + "w_gate", d, F), P.get(p + "w_up", d, F), wk_trunk, s);
+    w.down = pack_identity(*e, {P.get(p + "w_down", F, d)}, wk_trunk, s);
+  }
+  {
+    std::vector<float> inv(D / 2);
+    for (int i = 0; i < D / 2; ++i) inv[i] = (float)std::pow((double)c.rope_base, -2.0 * i / D);
+    e->inv_freq = e->mem.alloc_n<float>(D / 2);
+    HIPC(hipMemcpyAsync(e->inv_freq, inv.data(), inv.size() * 4, hipMemcpyHostToDevice, s));
+    if (c.rope) e->rope_cs = static_cast<float2*>(e->mem.alloc((size_t)c.max_batch * e->M * (D / 2) * sizeof(float2)));
+  }
+  const int64_t Bm = e->Bmax, M = e->M, ab = e->act_bytes;
+  e->h = e->mem.alloc_n<float>(Bm * M * d);
+  e->n = e->mem.alloc(Bm * M * d * ab);
+  e->q = e->mem.alloc(Bm * M * e->qd * ab);
+  e->o = e->mem.alloc(Bm * M * e->qd * ab);
+  e->g = e->mem.alloc(Bm * M * F * ab);
+  // key ranges: keys 0 .. M-1 written by the QKV epilogue, the tail to the
+  // next multiple of 64 stays zero (attention reads whole tiles)
+  e->ldk = (M + 63) / 64 * 64;
+  e->kv_layer = Bm * e->nkv * (int64_t)e->ldk * D;
+  e->kall = e->mem.alloc(L * e->kv_layer * ab);
+  e->vt = e->mem.alloc(L * e->kv_layer * ab);
+  HIPC(hipMemsetAsync(e->kall, 0, L * e->kv_layer * ab, s));
+  HIPC(hipMemsetAsync(e->vt, 0, L * e->kv_layer * ab, s));
+  int64_t part = 0, pend = 4;
+  if (!e->f32)
+    for (int B = 1; B <= e->Bmax; ++B) {
+      const int rows = e->M * (e->nq / e->nkv);
+      part = std::max(part, attention_partial_floats(B, e->M, e->nq, e->nkv, D, attn_splits_max(B, rows, e->nkv, e->M)));
+      const int R = B * e->M;
+      for (int l = 0; l < full_layers(*e); ++l)
+        for (int which = 0; which < 2; ++which) {
+          const Lin& w = which == 0 ? e->layers[l].o : e->layers[l].down;
+          const int sk = std::max(resid_split(*e, which, l, B), gemm_split_k(R, w.NPT, w.K));
+          if (sk > 1) pend = std::max(pend, (int64_t)sk * R * d);
+        }
+    }
+  e->part = e->mem.alloc_n<float>(part > 0 ? part : 4);
+  e->pend = e->mem.alloc_n<float>(pend);
+  e->part_cur = e->part;
+  e->pend_cur = e->pend;
+  e->desc = static_cast<CallDesc*>(e->mem.alloc(sizeof(CallDesc)));
+  HIPC(hipStreamSynchronize(s));
+}
+
 void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_tensors, hipStream_t s,
                phyai_expert* e) {
   const phyai_config& c = *cfg;
@@ -938,6 +1056,10 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
   e->f32 = c.weight_dtype == PHYAI_DTYPE_F32;
   e->act_bytes = e->f32 ? 4 : 2;
   e->L = c.n_layers; e->d = c.d_model; e->D = c.head_dim; e->nq = c.n_q_heads; e->nkv = c.n_kv_heads;
+  if (c.variant == PHYAI_VARIANT_PREFIX_LM) {
+    load_prefix_lm(tensors, n_tensors, s, e);
+    return;
+  }
   e->H = c.horizon; e->A = c.action_dim; e->F = c.d_mlp;
   e->off = c.state_token ? 1 : 0;
   e->M = e->H + e->off;
@@ -1194,6 +1316,7 @@ namespace {
 void check_call(phyai_expert* e, const void* prefix, const int32_t* prefix_len, const float* noise,
                 const float* timesteps, int n_steps, int batch, const float* state, const float* out_actions) {
   if (!e) fail(PHYAI_EINVAL, "NULL handle");
+  if (e->c.variant == PHYAI_VARIANT_PREFIX_LM) fail(PHYAI_EINVAL, "a prefix-LM handle: call phyai_prefill");
   if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range 1..max_batch");
   if (n_steps < 1 || n_steps > e->Kmax) fail(PHYAI_EINVAL, "n_steps out of range 1..max_steps");
   if (!prefix_len || !noise || !timesteps || !out_actions) fail(PHYAI_EINVAL, "NULL argument");
@@ -1256,7 +1379,7 @@ int64_t pend_floats(const phyai_expert& e, int B) {
   if (e.f32) return 0;
   const int R = B * e.M;
   int64_t need = 0;
-  for (int l = 0; l < e.L; ++l)
+  for (int l = 0; l < full_layers(e); ++l)
     for (int which = 0; which < 2; ++which) {
       const Lin& w = which == 0 ? e.layers[l].o : e.layers[l].down;
       const int sk = std::max(resid_split(e, which, l, B), gemm_split_k(R, w.NPT, w.K));
@@ -1316,6 +1439,7 @@ int phyai_prepare(phyai_expert* e, int32_t batch, int32_t n_steps, void* stream)
   (void)stream;
   return run_guarded([&] {
     if (!e) fail(PHYAI_EINVAL, "NULL handle");
+    if (e->c.variant == PHYAI_VARIANT_PREFIX_LM) fail(PHYAI_EINVAL, "a prefix-LM handle has no denoising loop");
     if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range");
     if (n_steps < 1 || n_steps > e->Kmax) fail(PHYAI_EINVAL, "n_steps out of range");
     if (use_graphs()) get_bucket(*e, batch, n_steps);
@@ -1409,10 +1533,31 @@ int phyai_profile_stage(phyai_expert* e, int32_t stage, int32_t reps, void* stre
     if (e->last_batch < 1) fail(PHYAI_EINVAL, "call phyai_denoise first (the stage reads its inputs)");
     hipStream_t s = static_cast<hipStream_t>(stream);
     for (int r = 0; r < reps; ++r)
-      for (int l = 0; l < e->L; ++l) {
+      for (int l = 0; l < full_layers(*e); ++l) {
         if (e->f32) layer_stage<float>(*e, stage, l, 0, e->last_batch, s);
         else layer_stage<bf16_t>(*e, stage, l, 0, e->last_batch, s);
       }
+    HIPC(hipGetLastError());
+  });
+}
+
+int phyai_prefill(phyai_expert* e, const float* embeds, const int32_t* prefix_len, void* kv_out, int32_t batch,
+                  void* stream) {
+  return run_guarded([&] {
+    if (!e) fail(PHYAI_EINVAL, "NULL handle");
+    if (e->c.variant != PHYAI_VARIANT_PREFIX_LM) fail(PHYAI_EINVAL, "not a prefix-LM handle");
+    if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range 1..max_batch");
+    if (!embeds || !prefix_len || !kv_out) fail(PHYAI_EINVAL, "NULL argument");
+    for (int b = 0; b < batch; ++b)
+      if (prefix_len[b] < 0 || prefix_len[b] > e->M)
+        fail(PHYAI_EINVAL, "prefix_len[" + std::to_string(b) + "] = " + std::to_string(prefix_len[b]) +
+                               " outside 0..prefix_cap");
+    auto aligned16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+    if (!aligned16(embeds) || !aligned16(kv_out)) fail(PHYAI_EINVAL, "embeds and kv_out must be 16-byte aligned");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    write_call_desc(*e, embeds, prefix_len, nullptr, batch, nullptr, nullptr, s);
+    if (e->f32) enqueue_prefill<float>(*e, embeds, kv_out, batch, s);
+    else enqueue_prefill<bf16_t>(*e, embeds, kv_out, batch, s);
     HIPC(hipGetLastError());
   });
 }

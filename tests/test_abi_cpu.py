@@ -69,3 +69,27 @@ def test_missing_tensor_rejected():
     rc = px.lib().phyai_load_expert(ctypes.byref(cfg), (px.Tensor * 1)(), 0, None, ctypes.byref(h))
     assert rc == px.PHYAI_EINVAL
     assert b"missing tensor 'in_w'" in px.lib().phyai_last_error()
+
+
+def test_prefix_lm_rejections_before_device_work():
+    """The prefix-LM variant: its own config rules and tensor list, and the
+    prefill entry point's NULL handling (no GPU needed)."""
+    import workloads as wl
+    L = px.lib()
+    assert L.phyai_prefill(None, None, None, None, 1, None) == px.PHYAI_EINVAL
+    assert b"NULL" in L.phyai_last_error()
+    base = wl.CONFIGS["plm_tiny_fp32"]
+    h = ctypes.c_void_p()
+    cfg = px.make_config(base, max_steps=0)
+    cfg.state_token = 1
+    assert L.phyai_load_expert(ctypes.byref(cfg), None, 0, None, ctypes.byref(h)) == px.PHYAI_EINVAL
+    assert b"no state token" in L.phyai_last_error()
+    cfg = px.make_config(base, max_steps=0)
+    cfg.prefix_cap = 0
+    assert L.phyai_load_expert(ctypes.byref(cfg), None, 0, None, ctypes.byref(h)) == px.PHYAI_EINVAL
+    assert b"prefix_cap >= 1" in L.phyai_last_error()
+    # horizon, action_dim, steps and timestep fields are not required
+    cfg = px.make_config(base, max_steps=0)
+    rc = L.phyai_load_expert(ctypes.byref(cfg), (px.Tensor * 1)(), 0, None, ctypes.byref(h))
+    assert rc == px.PHYAI_EINVAL and not h.value
+    assert b"missing tensor 'layers.0.attn_norm'" in L.phyai_last_error()
