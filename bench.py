@@ -15,6 +15,8 @@ Also measured in the same run and reported in the same JSON line:
     whole batch's MFMA fraction of the bf16 peak.
   * legs: the pi0.5-shaped and DiT-shaped batch-1 workloads and the tiny
     fp32 expert, ms per chunk each with its chunk roofline.
+  * prefill: the prefix LM that produces the prefix K/V (Gemma-class, 816
+    prefix tokens, batch 1): ms per call and its MFMA fraction.
   * roofline: the dominant kernel of the batch-1 leg, its algorithmic bytes
     per launch over its average duration, timed with HIP events on the stream
     it runs on.
@@ -418,6 +420,70 @@ def _leg_plain(args, px, wl, name, K, W, copy_gbs, env):
     return rec
 
 
+def prefill_flops(cfg, plen):
+    """MFMA work of one prefix-LM call: every layer's GEMMs over the valid
+    prefix rows (the last layer only its QKV projection) and attention of
+    each request over its own prefix (Q K^T and P V: 4 P^2 n_q d_h per
+    layer)."""
+    d, F, D, nq, nkv, L = cfg.d_model, cfg.d_mlp, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads, cfg.n_layers
+    qkv = 2 * d * (nq + 2 * nkv) * D
+    full = qkv + 2 * nq * D * d + 2 * d * 2 * F + 2 * F * d
+    rows = int(np.sum(plen))
+    attn = sum(4 * int(p) ** 2 * nq * D for p in plen)
+    return rows * (full * (L - 1) + qkv) + (L - 1) * attn
+
+
+def leg_prefill(args, px, wl, K, W):
+    """The prefix LM (the VLM's language part producing the prefix K/V) on
+    the Gemma-class workload over the pi0 prefix (816 tokens, batch 1): ms
+    per call, MFMA throughput, and per-stage launch times (graph replays)."""
+    import torch
+    cfg = wl.CONFIGS["plm_gemma_bf16_b1"]
+    _log(f"generating {cfg.name}")
+    case = wl.make_prefill_case(cfg, seed=args.seed)
+    m = px.PrefixLM(cfg, case.weights)
+    del case.weights
+    emb = torch.from_numpy(case.embeds).cuda()
+    out = torch.empty((cfg.n_layers, 2, cfg.batch, cfg.prefix_cap, cfg.n_kv_heads * cfg.head_dim),
+                      dtype=torch.int16, device="cuda")
+    _log(f"timing {cfg.name}")
+    wall, per = time_calls(lambda: m.prefill(emb, case.prefix_len, out=out), K, W)
+    ms = float(np.median(per))
+    fl = prefill_flops(cfg, case.prefix_len)
+    tf = fl / (ms * 1e-3) / 1e12
+    rec = {"config": {"workload": "prefix LM, Gemma-class (18 layers, width 2048, 8 query heads + 1 K/V head "
+                                  "of 256, GeGLU 16384), pi0 prefix of 816 tokens, batch 1",
+                      "weights": "bf16"},
+           "ms_per_call": round(ms, 3), "p99_ms": round(float(np.percentile(per, 99)), 3),
+           "tokens_per_s": round(float(np.sum(case.prefix_len)) / (ms * 1e-3), 1),
+           "flops_per_call": int(fl), "TFLOPs": round(tf, 1),
+           "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4)}
+    if not args.no_stages:
+        stages = {}
+        Lf = cfg.n_layers - 1                  # stages run over the layers with an MLP
+        cap = torch.cuda.Stream()
+        for st in ("norm1", "qkv", "attn", "oproj", "norm2", "mlp_up", "mlp_down"):
+            m.profile_stage(st, 1)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=cap):
+                m.profile_stage(st, 2)
+            g.replay()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            g.replay()
+            b.record()
+            torch.cuda.synchronize()
+            stages[st] = round(a.elapsed_time(b) * 1e3 / (2 * Lf), 2)
+            del g
+        rec["stage_us"] = stages
+    m.close()
+    del emb, out
+    torch.cuda.empty_cache()
+    return rec
+
+
 def leg_batch64(args, px, wl, K, W):
     import torch
     cfg = wl.CONFIGS["pi0_fp8_b64"]
@@ -477,6 +543,7 @@ def main():
     ap.add_argument("--no-batch1", action="store_true",
                     help="only the batch-64 leg (for counter passes; the line then has no batch-1 value)")
     ap.add_argument("--no-legs", action="store_true", help="skip the pi0.5, DiT and tiny fp32 workloads")
+    ap.add_argument("--no-prefill", action="store_true", help="skip the prefix-LM workload")
     ap.add_argument("--no-stages", action="store_true",
                     help="skip the per-stage graph timings and the rooflines built on them (counter passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -508,6 +575,8 @@ def main():
         # the persistent batch-1 loop (opt-in) on the pi0 workload
         rec["legs"]["pi0_bf16_b1_persistent"] = leg_plain(args, px, wl, "pi0_bf16_b1", Kl, Wl, copy,
                                                            env={"PHYAI_PERSIST": "1"})
+    if not args.no_prefill:
+        rec["prefill"] = leg_prefill(args, px, wl, max(1, min(K, 20)), min(W, 3))
     if not args.no_batch64:
         rec["batch64"] = leg_batch64(args, px, wl, K, W)
     print(json.dumps(rec), flush=True)

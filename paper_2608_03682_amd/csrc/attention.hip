@@ -639,14 +639,17 @@ __global__ __launch_bounds__(256) void kv_export_kernel(KvExportArgs r) {
 }  // namespace
 
 // Query rows per block: 128 (4 waves), or 64 (2 waves) when the 128-row
-// blocks of all requests number fewer than 64 (batch 1), so that with the
-// key splits the kernel spreads over more CUs and each block loads half the
-// queries and stores half the partials.  PHYAI_ATTN_ROWS=64|128 (tests, read
-// at enqueue time) forces it.
+// blocks of all requests number fewer than 64 (batch 1) and a request has a
+// suffix-sized query count, so that with the key splits the kernel spreads
+// over more CUs and each block loads half the queries and stores half the
+// partials.  A prefix LM's self-attention (thousands of query rows per
+// request) keeps 128 rows: there four waves share each key tile (batch-1
+// prefix of 816 tokens: 63 -> 34 us per launch).  PHYAI_ATTN_ROWS=64|128
+// (tests, read at enqueue time) forces it.
 int attention_rows_per_block(int B, int rows, int nkv) {
   const char* f = getenv("PHYAI_ATTN_ROWS");
   if (f) return atoi(f) == 64 ? 64 : 128;
-  return (int64_t)((rows + 127) / 128) * B * nkv < 64 ? 64 : 128;
+  return rows <= 1024 && (int64_t)((rows + 127) / 128) * B * nkv < 64 ? 64 : 128;
 }
 
 // Partials: bf16 O [tiles][split][rows_per_block][D] followed (at part_ml_off

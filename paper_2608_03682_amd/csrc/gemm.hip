@@ -692,7 +692,6 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
   const int wv = __builtin_amdgcn_readfirstlane(wave);
   const int wm = wave / WN, wn = wave % WN;
   const int lc = lane % 16, lg = lane / 16;
-  const int nkb = g.K / 64;
   const int mtiles = (g.R + 127) / 128, ntiles = g.NPT / 4;
   const int order = tile_order(g, Epi::kWaveTile, NS == 4);
   const int t = xcd_tile(blockIdx.x, 0, gridDim.x, mtiles * ntiles, order);
@@ -702,6 +701,10 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
   const int m0 = mi * 128, pt0 = ni * 4;
   const bf16_t* A = static_cast<const bf16_t*>(g.A);
   const uint8_t* W = static_cast<const uint8_t*>(g.W);
+  // K slice blockIdx.y of gridDim.y (split-K: the slice's raw sums go to
+  // split_out, the consumer adds the slices); the ring runs over its k-blocks
+  const int nkb = g.K / 64 / gridDim.y, kb0 = blockIdx.y * nkb;
+  float* const sp = g.split_out ? g.split_out + (int64_t)blockIdx.y * g.split_stride : nullptr;
 
   int aoff[C::A_LD];
 #pragma unroll
@@ -714,9 +717,10 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
   for (int i = 0; i < C::B_LD; ++i) {
     const int blk = NW * i + wave;
     const int f = blk / (C::FB / 1024), part = blk % (C::FB / 1024);
-    bsrc[i] = W + ((int64_t)(pt0 + f / 2) * nkb * 2 + f % 2) * C::FB + part * 1024 + lane * 16;
+    bsrc[i] = W + ((int64_t)(pt0 + f / 2) * (g.K / 64) * 2 + f % 2) * C::FB + part * 1024 + lane * 16;
   }
-  auto issue = [&](int slot, int kb) {
+  auto issue = [&](int slot, int kbl) {
+    const int kb = kb0 + kbl;
     uint8_t* base = ring + slot * C::STAGE;
 #pragma unroll
     for (int i = 0; i < C::A_LD; ++i) dma16(A + aoff[i] + kb * 64, (lds_void_t*)(base + (NW * i + wv) * 1024));
@@ -820,7 +824,25 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
     bare_barrier();
     epi.wave_tile(g, acc, m0 + 64 * wm, pt0 + 2 * wn, lc, lg, reinterpret_cast<bf16_t*>(ring) + wave * Epi::kVStage);
   } else if constexpr (kEarly) {
-    tile_epilogue_early<Epi, NT>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg, epre, esc);
+    if (sp) {
+      const int N = 32 * g.NPT;
+#pragma unroll
+      for (int pp = 0; pp < NT / 2; ++pp) {
+        const int p = pt0 + (NT / 2) * wn + pp;
+#pragma unroll
+        for (int mt = 0; mt < 4; ++mt)
+#pragma unroll
+          for (int v = 0; v < 4; ++v) {
+            const int row = m0 + 64 * wm + 16 * mt + 4 * lg + v;
+            if (row < g.R) {
+              sp[(int64_t)row * N + 32 * p + lc] = acc[mt][2 * pp][v] * esc[pp][0];
+              sp[(int64_t)row * N + 32 * p + 16 + lc] = acc[mt][2 * pp + 1][v] * esc[pp][1];
+            }
+          }
+      }
+    } else {
+      tile_epilogue_early<Epi, NT>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg, epre, esc);
+    }
   } else {
     tile_epilogue<0>(g, epi, acc, m0 + 64 * wm, pt0 + (NT / 2) * wn, lc, lg);
   }
@@ -833,7 +855,17 @@ gemm_ring_kernel(GemmArgs g, Epi epi) {
 // blocks) instead of 8 slices of 512 over 64-row blocks: the next norm
 // folds a quarter of the slices (8.39 -> 8.31 ms per chunk).
 int gemm_split_k(int R, int NPT, int K) {
-  if (R >= 256) return 1;                     // the tiled kernel has enough blocks
+  if (R >= 256) {
+    // many rows: the one-tile-per-CU ring splits K when its tiles fill at
+    // most half the CUs (the prefix LM's O and down projections: 112 tiles)
+    // and each slice keeps at least 16 k-blocks; PHYAI_GEMM_TILE (tests)
+    // forces a kernel without the split
+    if (getenv("PHYAI_GEMM_TILE") || NPT % 4 != 0) return 1;
+    const int tiles = ((R + 127) / 128) * (NPT / 4);
+    int s = 1;
+    while (s < 4 && tiles * s * 2 <= 256 && (K / 64) % (2 * s) == 0 && K / 64 / (2 * s) >= 16) s *= 2;
+    return s;
+  }
   const int blocks = NPT * ((R + 15) / 16);
   int s = (256 + blocks - 1) / blocks;
   const int cap = (K / 64) / 4;               // keep >= one k-block per wave
@@ -1020,10 +1052,11 @@ void launch(const GemmArgs& g, const Epi& epi, hipStream_t s) {
     // at most one tile per CU: no second block covers the load latency, so
     // the four-stage ring with eight waves (two per SIMD); otherwise the
     // two-stage ring for short K and the strided kernel for long K
-    const bool deep = !Epi::kWaveTile && (force ? strcmp(force, "deep") == 0 : tiles <= 256);
-    const bool ring = force ? strcmp(force, "strided") != 0 : g.K <= 1024;
+    const int nz = g.split_out ? g.split_k : 1;       // K slices (gemm_split_k), deep ring only
+    const bool deep = !Epi::kWaveTile && (nz > 1 || (force ? strcmp(force, "deep") == 0 : tiles <= 256));
+    const bool ring = force ? strcmp(force, "strided") != 0 : g.K <= 2048;
     if (deep) {
-      const dim3 rgrid(xcd_grid(tiles, 1 << 30));
+      const dim3 rgrid(xcd_grid(tiles, 1 << 30), nz);
       if constexpr (!Epi::kWaveTile) {
         if (g.kind == W_FP8) hipLaunchKernelGGL((gemm_ring_kernel<Epi, true, 4, 4>), rgrid, dim3(512), 0, s, g, epi);
         else hipLaunchKernelGGL((gemm_ring_kernel<Epi, false, 4, 4>), rgrid, dim3(512), 0, s, g, epi);

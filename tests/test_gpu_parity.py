@@ -218,6 +218,18 @@ def test_many_row_gemm_tiles(tile, wdt):
     compare(f"gemm tile {tile} {wdt}", gpu, _oracle(cfg, case), cfg)
 
 
+@pytest.mark.parametrize("wdt", ["bf16", "fp8"])
+def test_many_row_split_k_residual(wdt):
+    """The one-tile-per-CU ring GEMM with K split over blocks (few output
+    tiles, long K): 408 rows, down projection K = 2048 over 6 tiles, split
+    in two; the slices are added by the next norm and by the readout."""
+    cfg = small_cfg("pi0", batch=8, d_mlp=2048, weight_dtype=wdt)
+    print(f"[case] split-K residual {wdt}", flush=True)
+    case = wl.make_case(cfg, seed=6)
+    ex = _expert(cfg, case)
+    compare(f"split-K residual {wdt}", run_gpu(ex, case), _oracle(cfg, case), cfg)
+
+
 def test_fp4_scales_must_be_powers_of_two():
     """The fp4 format's scales are applied by the hardware conversion, which
     uses only their exponent: a scale that is not a power of two is refused

@@ -82,6 +82,9 @@ SMALL = [
     # fewer than 256 rows: split-K residual GEMMs, key-split attention merged
     # in the output projection
     ("bf16_small_rows", dict(prefix_cap=40, prefix_min=40, prefix_max=40, batch=1, n_layers=3)),
+    # many rows, a long-K down projection over few tiles: K split over blocks
+    ("bf16_split_k_down", dict(d_mlp=2048)),
+    ("fp8_split_k_down", dict(d_mlp=2048, weight_dtype="fp8")),
     ("fp8", dict(weight_dtype="fp8")),
     ("fp4", dict(weight_dtype="fp4")),
     ("f32", dict(weight_dtype="f32", kv_dtype="f32")),
