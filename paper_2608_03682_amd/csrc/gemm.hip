@@ -339,30 +339,65 @@ __global__ __launch_bounds__(256) void gemm_mfma_kernel(GemmArgs g, Epi epi) {
   }
 }
 
-// fp32 path: weights stored [K][N] (packed column order), one thread per
-// (row, column pair).
+// fp32 path: weights stored [K][N] (packed column order).  Block: 16 rows x
+// one pair tile (32 columns); K is split over 16 slices (thread = slice kq,
+// column c), each slice accumulating all 16 rows of its two columns with
+// 16-byte loads of four consecutive k of a row, and the slices are summed
+// through LDS in slice order.  K a multiple of 64 (every K of the configs).
 template <class Epi>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(GemmArgs g, Epi epi) {
-  const int c = threadIdx.x % 16, rr = threadIdx.x / 16;
+  __shared__ float red[16][16][33];             // [slice][row][column], padded
+  const int c = threadIdx.x % 16, kq = threadIdx.x / 16;
   const int p = blockIdx.x;
-  const int row = blockIdx.y * 16 + rr;
-  if (row >= g.R) return;
+  const int r0 = blockIdx.y * 16;
   const float* A = g.A_ind ? static_cast<const float*>(*g.A_ind) + g.a_off
                            : static_cast<const float*>(g.A);
-  bool ok = true;
-  if (g.rows_per_req > 0) ok = (row % g.rows_per_req) < g.desc->prefix_len[row / g.rows_per_req];
-  const float* a = A + (int64_t)row * g.lda;
   const float* w = static_cast<const float*>(g.W) + 32 * p + c;
   const int N = 32 * g.NPT;
-  float s0 = 0.f, s1 = 0.f;
-  if (ok) {
-    for (int k = 0; k < g.K; ++k) {
-      const float av = a[k];
-      s0 = fmaf(av, w[(int64_t)k * N], s0);
-      s1 = fmaf(av, w[(int64_t)k * N + 16], s1);
+  const int kc = g.K / 16;                      // slice length, a multiple of 4
+  const int k0 = kq * kc;
+  float s0[16], s1[16];
+#pragma unroll
+  for (int r = 0; r < 16; ++r) s0[r] = s1[r] = 0.f;
+  for (int k = k0; k < k0 + kc; k += 4) {
+    float w0[4], w1[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      w0[j] = w[(int64_t)(k + j) * N];
+      w1[j] = w[(int64_t)(k + j) * N + 16];
+    }
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      // rows past R read row R-1 (their sums are never used)
+      const float4 a = *reinterpret_cast<const float4*>(A + (int64_t)min(r0 + r, g.R - 1) * g.lda + k);
+      s0[r] = fmaf(a.x, w0[0], s0[r]);
+      s0[r] = fmaf(a.y, w0[1], s0[r]);
+      s0[r] = fmaf(a.z, w0[2], s0[r]);
+      s0[r] = fmaf(a.w, w0[3], s0[r]);
+      s1[r] = fmaf(a.x, w1[0], s1[r]);
+      s1[r] = fmaf(a.y, w1[1], s1[r]);
+      s1[r] = fmaf(a.z, w1[2], s1[r]);
+      s1[r] = fmaf(a.w, w1[3], s1[r]);
     }
   }
-  epi(row, p, c, s0, s1);
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    red[kq][r][c] = s0[r];
+    red[kq][r][16 + c] = s1[r];
+  }
+  __syncthreads();
+  const int rr = threadIdx.x / 16;
+  const int row = r0 + rr;
+  if (row >= g.R) return;
+  float t0 = 0.f, t1 = 0.f;
+#pragma unroll
+  for (int q = 0; q < 16; ++q) {
+    t0 += red[q][rr][c];
+    t1 += red[q][rr][16 + c];
+  }
+  // rows of a request past its prefix length (rows_per_req > 0) count as zero
+  if (g.rows_per_req > 0 && (row % g.rows_per_req) >= g.desc->prefix_len[row / g.rows_per_req]) t0 = t1 = 0.f;
+  epi(row, p, c, t0, t1);
 }
 
 // ---------------------------------------------------------------------------
