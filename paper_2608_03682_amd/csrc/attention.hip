@@ -123,9 +123,8 @@ __device__ __forceinline__ float pair_sum(float x) {
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
 }
 
-#ifndef PHYAI_ATTN_PD
-#define PHYAI_ATTN_PD 4
-#endif
+// LDS fragment reads issued this many MFMAs ahead of their use
+constexpr int kReadAhead = 4;
 
 // Instruction order of one MFMA loop of n products whose operands come from
 // LDS: the first pd fragment reads, then each MFMA followed by the next read,
@@ -167,7 +166,7 @@ __device__ __forceinline__ void attn_tile(const bf16_t* TK, const bf16_t* TVt, c
     st[0] = mfma32x32x16(kf[0][s], qf[s], st[0]);
     st[1] = mfma32x32x16(kf[1][s], qf[s], st[1]);
   }
-  lds_mfma_pipeline<D / 8, PHYAI_ATTN_PD>();
+  lds_mfma_pipeline<D / 8, kReadAhead>();
   // Scores are masked only where a mask can bite: the tile holding the end
   // of the key range, and for state-token queries the tiles that reach past
   // the prefix (wave-uniform test; a state-token row shares its wave with
@@ -244,7 +243,7 @@ __device__ __forceinline__ void attn_tile(const bf16_t* TK, const bf16_t* TVt, c
   for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) o[db] = mfma32x32x16(vf[t][db], pf[t], o[db]);
-  lds_mfma_pipeline<D / 8, PHYAI_ATTN_PD>();
+  lds_mfma_pipeline<D / 8, kReadAhead>();
 }
 
 template <int D, int NWB>
