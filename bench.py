@@ -54,14 +54,14 @@ _GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/ke
              "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
 _MERGE_SRC = _GEMM_SRC + ("paper_2608_03682_amd/csrc/attention.hip",)
 MEASURED_TRAFFIC = {
-    ("pi0_bf16_b1", "attn"): {"bytes": 6231859, "sources": _ATTN_SRC, "sha256": "74aad99adabf4f7d"},
-    ("pi0_bf16_b1", "qkv"): {"bytes": 6525440, "sources": _GEMM_SRC, "sha256": "e06d88475c1f8331"},
-    ("pi0_bf16_b1", "oproj"): {"bytes": 9334784, "sources": _MERGE_SRC, "sha256": "07991a5493ad3863"},
-    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18225152, "sources": _GEMM_SRC, "sha256": "e06d88475c1f8331"},
-    ("pi0_bf16_b1", "mlp_down"): {"bytes": 12483584, "sources": _GEMM_SRC, "sha256": "e06d88475c1f8331"},
-    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90396877, "sources": _GEMM_SRC, "sha256": "e06d88475c1f8331"},
-    ("pi0_fp8_b64", "qkv"): {"bytes": 107266560, "sources": _GEMM_SRC, "sha256": "e06d88475c1f8331"},
-    ("pi0_fp8_b64", "attn"): {"bytes": 84656128, "sources": _ATTN_SRC, "sha256": "74aad99adabf4f7d"},
+    ("pi0_bf16_b1", "attn"): {"bytes": 6240111, "sources": _ATTN_SRC, "sha256": "38e4cce543771614"},
+    ("pi0_bf16_b1", "qkv"): {"bytes": 6537698, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
+    ("pi0_bf16_b1", "oproj"): {"bytes": 9339861, "sources": _MERGE_SRC, "sha256": "ebb1953c3f8ad4a7"},
+    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18220963, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
+    ("pi0_bf16_b1", "mlp_down"): {"bytes": 12472252, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90362981, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
+    ("pi0_fp8_b64", "qkv"): {"bytes": 107307562, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
+    ("pi0_fp8_b64", "attn"): {"bytes": 84646463, "sources": _ATTN_SRC, "sha256": "38e4cce543771614"},
 }
 
 
