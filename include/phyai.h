@@ -11,7 +11,10 @@
  * "Graph replay" and "Profiled operator selection").  The prefix state is
  * valid for one chunk: it is read, never written, and stays fixed across
  * the K steps.  Requests in a batch are independent (Section "Cloud
- * Batching").
+ * Batching").  The same library also runs the step before the loop: the
+ * vision-language model's language part over the prefix tokens, which
+ * produces that prefix K/V cache (phyai_prefill, on a handle of variant
+ * PHYAI_VARIANT_PREFIX_LM).
  *
  * Every step runs in hand-written HIP kernels; the K-step loop is captured
  * in a HIP graph per (batch, steps) bucket and replayed.

@@ -22,7 +22,7 @@
 // as 16x16, which is what a single wave per SIMD needs to keep the matrix
 // core busy.
 //
-// Block: 4 waves x 32 query rows (2 waves when the grid is small, see
+// Block: 4 waves x 32 query rows (2 waves for a batch-1-sized suffix, see
 // attention_rows_per_block); 64-key tiles double-buffered in LDS and filled
 // by direct global->LDS loads, the next tile in flight while the current one
 // is computed.
