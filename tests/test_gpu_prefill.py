@@ -6,8 +6,9 @@ output to bf16 (unit roundoff u = 2^-8); one layer's rounding errors are
 random in sign, so they add in quadrature over the L + 1 rounding stages a
 cache entry has passed (its own output rounding included), and the largest
 error over the cache stays within about six standard deviations: max-abs <=
-6 u sqrt(L + 1) max(1, rms) (0.041 at 2 layers, 0.10 at 18).  The fp32 path keeps the actions' fp32 bar (1e-4).  Fed into
-the expert, the cache must give actions within the actions' own bar
+6 u sqrt(L + 1) max(1, rms) (0.041 at 2 layers, 0.10 at 18).  The fp32 path
+keeps the actions' fp32 bar (1e-4).  Fed into the expert, the cache must give
+actions within the actions' own bar
 (test_prefill_then_denoise_matches_the_oracle_chain).
 """
 import ctypes
@@ -85,6 +86,10 @@ SMALL = [
     # many rows, a long-K down projection over few tiles: K split over blocks
     ("bf16_split_k_down", dict(d_mlp=2048)),
     ("fp8_split_k_down", dict(d_mlp=2048, weight_dtype="fp8")),
+    # more than 1,024 query rows per request: 128-row attention blocks with key
+    # splits and their merge kernel, ragged prefixes ending mid-tile
+    ("bf16_long_queries_ragged", dict(head_dim=256, n_q_heads=4, d_model=512, prefix_cap=300, prefix_min=270,
+                                      prefix_max=300, batch=3)),
     ("fp8", dict(weight_dtype="fp8")),
     ("fp4", dict(weight_dtype="fp4")),
     ("f32", dict(weight_dtype="f32", kv_dtype="f32")),
