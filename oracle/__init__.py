@@ -1,5 +1,5 @@
-"""Oracle for the action-expert denoising loop and the prefix K/V producer
-(float64 NumPy).
+"""Oracle for the action-expert denoising loop, the prefix K/V producer and
+the vision tower before it (float64 NumPy).
 
 TEST INFRASTRUCTURE ONLY: a plain, slow, obviously correct CPU reference.
 Only ``tests/``, ``__graft_entry__.smoke()`` and the benchmark's
@@ -12,6 +12,7 @@ paper), which is stated there.
 from .expert import (DecodedWeights, denoise, pi05_condition, velocity_dit, velocity_pi0,
                      velocity_pi05)
 from .prefix_lm import prefill, prefill_request
+from .vision import encode_images
 from .numerics import (E2M1_TABLE, E4M3FN_TABLE, attention, attention_bruteforce, decode_bf16,
                        decode_fp4, decode_fp8, decode_stored, euler, gelu_tanh, layer_normalize, rms_normalize, rope,
                        sinusoid, swish)
@@ -21,5 +22,5 @@ __all__ = [
     "E2M1_TABLE", "E4M3FN_TABLE", "attention", "attention_bruteforce", "decode_bf16", "decode_fp4",
     "decode_fp8",
     "decode_stored", "euler", "gelu_tanh", "layer_normalize", "rms_normalize", "rope", "sinusoid",
-    "swish", "prefill", "prefill_request",
+    "swish", "prefill", "prefill_request", "encode_images",
 ]

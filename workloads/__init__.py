@@ -35,7 +35,7 @@ __all__ = [
     "make_prefix", "make_prefix_lengths", "make_noise", "make_state",
     "default_timesteps", "make_case", "bf16_bits_from_f32", "e4m3fn_encode",
     "quantize_fp8_per_column", "e2m1_encode", "quantize_fp4_groups", "FP4_GROUP", "TRUNK_LINEARS",
-    "make_prefix_embeds", "PrefillCase", "make_prefill_case",
+    "make_prefix_embeds", "PrefillCase", "make_prefill_case", "make_patches", "VisionCase", "make_vision_case",
 ]
 
 
@@ -47,7 +47,10 @@ class ExpertConfig:
     (adaRMSNorm time conditioning) or ``dit`` (DiT head with adaLN-zero,
     alternating cross/self attention); ``prefix_lm`` is the vision-language
     model's language part run over the prefix tokens, which produces the
-    prefix K/V an expert reads (horizon, action_dim and n_steps are 0).
+    prefix K/V an expert reads (horizon, action_dim and n_steps are 0);
+    ``vision`` is the vision tower that turns each request's image patches
+    into the image tokens at the head of that prefix (n_images images of
+    n_patches patches of patch_dim values each, tokens of width d_out).
     """
     name: str
     cfg_id: int
@@ -76,6 +79,10 @@ class ExpertConfig:
     sin_max_period: float = 4.0
     rope_base: float = 10000.0
     init_std: float = 0.02
+    n_images: int = 0         # vision: images per request
+    n_patches: int = 0        # vision: patches (tokens) per image
+    patch_dim: int = 0        # vision: values per patch
+    d_out: int = 0            # vision: width of the projected image tokens
 
     @property
     def tokens(self) -> int:
@@ -149,6 +156,16 @@ CONFIGS: Dict[str, ExpertConfig] = {
         n_q_heads=4, n_kv_heads=1, head_dim=64, d_mlp=1024, horizon=0,
         action_dim=0, n_steps=0, prefix_cap=64, prefix_min=64, prefix_max=64,
         batch=1, state_token=False, rope=True, weight_dtype="f32", kv_dtype="f32", time_dim=0),
+    # The vision tower before it: a SigLIP-L/16-class ViT (24 layers of width
+    # 1024, 16 heads of 64, GELU MLP 4096, LayerNorm, biases everywhere) over 3
+    # images of 256 patches of 16 x 16 x 3 values, whose tokens are projected
+    # to the Gemma-class LM's width 2048.
+    "vit_siglip_bf16_b1": _cfg(
+        name="vit_siglip_bf16_b1", cfg_id=9, variant="vision", n_layers=24, d_model=1024,
+        n_q_heads=16, n_kv_heads=16, head_dim=64, d_mlp=4096, horizon=0,
+        action_dim=0, n_steps=0, prefix_cap=768, prefix_min=768, prefix_max=768,
+        batch=1, state_token=False, rope=False, weight_dtype="bf16", kv_dtype="bf16", time_dim=0,
+        n_images=3, n_patches=256, patch_dim=768, d_out=2048),
     "plm_gemma_bf16_b1": _cfg(
         name="plm_gemma_bf16_b1", cfg_id=8, variant="prefix_lm", n_layers=18, d_model=2048,
         n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=16384, horizon=0,
@@ -283,6 +300,32 @@ def weight_specs(cfg: ExpertConfig) -> Dict[str, tuple]:
     qd = cfg.n_q_heads * cfg.head_dim
     kd = cfg.n_kv_heads * cfg.head_dim
     s: Dict[str, tuple] = {}
+    if cfg.variant == "vision":
+        # LayerNorm scales are stored as their deviation from one (the (1 + w)
+        # convention of the norms elsewhere here)
+        s["patch_w"] = (cfg.patch_dim, d)
+        s["patch_b"] = (1, d)
+        s["pos_emb"] = (cfg.n_patches, d)
+        for l in range(cfg.n_layers):
+            p = f"layers.{l}."
+            s[p + "ln1_w"] = (1, d)
+            s[p + "ln1_b"] = (1, d)
+            for nm in ("wq", "wk", "wv"):
+                s[p + nm] = (d, d)
+                s[p + "b" + nm[1]] = (1, d)
+            s[p + "wo"] = (d, d)
+            s[p + "bo"] = (1, d)
+            s[p + "ln2_w"] = (1, d)
+            s[p + "ln2_b"] = (1, d)
+            s[p + "mlp_w1"] = (d, F)
+            s[p + "mlp_b1"] = (1, F)
+            s[p + "mlp_w2"] = (F, d)
+            s[p + "mlp_b2"] = (1, d)
+        s["post_ln_w"] = (1, d)
+        s["post_ln_b"] = (1, d)
+        s["proj_w"] = (d, cfg.d_out)
+        s["proj_b"] = (1, cfg.d_out)
+        return s
     if cfg.variant == "prefix_lm":
         # the last layer's K/V depend only on its input: its output
         # projection and MLP are never needed and not listed
@@ -533,3 +576,27 @@ def make_prefill_case(cfg: ExpertConfig, seed: int = 0, batch: Optional[int] = N
                        weights=weights if weights is not None else make_weights(cfg, seed),
                        embeds=make_prefix_embeds(cfg, plen, seed),
                        prefix_len=plen)
+
+
+def make_patches(cfg: ExpertConfig, seed: int = 0, batch: Optional[int] = None, requests=None) -> np.ndarray:
+    """Input of a vision tower: normalised pixel patches ~ N(0, 1), float32
+    [B][n_images][n_patches][patch_dim]."""
+    B = cfg.batch if batch is None else batch
+    reqs = list(range(B)) if requests is None else list(requests)
+    out = np.empty((len(reqs), cfg.n_images, cfg.n_patches, cfg.patch_dim), dtype=np.float32)
+    for i, b in enumerate(reqs):
+        out[i] = _rng(seed, cfg.cfg_id, 7, b).standard_normal(out.shape[1:], dtype=np.float32)
+    return out
+
+
+@dataclasses.dataclass
+class VisionCase:
+    cfg: ExpertConfig
+    weights: Dict[str, StoredTensor]
+    patches: np.ndarray
+
+
+def make_vision_case(cfg: ExpertConfig, seed: int = 0, batch: Optional[int] = None,
+                     weights: Optional[Dict[str, StoredTensor]] = None) -> VisionCase:
+    return VisionCase(cfg=cfg, weights=weights if weights is not None else make_weights(cfg, seed),
+                      patches=make_patches(cfg, seed, batch))
