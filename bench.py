@@ -17,6 +17,8 @@ Also measured in the same run and reported in the same JSON line:
     fp32 expert, ms per chunk each with its chunk roofline.
   * prefill: the prefix LM that produces the prefix K/V (Gemma-class, 816
     prefix tokens, batch 1): ms per call and its MFMA fraction.
+  * vision: the vision tower before it (SigLIP-class ViT, three 256-patch
+    images per request, batch 1): ms per call and its MFMA fraction.
   * roofline: the dominant kernel of the batch-1 leg, its algorithmic bytes
     per launch over its average duration, timed with HIP events on the stream
     it runs on.
@@ -484,6 +486,65 @@ def leg_prefill(args, px, wl, K, W):
     return rec
 
 
+def vision_flops(cfg, B):
+    """MFMA work of one vision-tower call over B requests: per image the
+    patch embedding, every block's QKV, O and MLP GEMMs and attention (Q K^T
+    and P V: 4 N^2 n_heads d_h per block), and the projector."""
+    d, F, D, H, L, N = cfg.d_model, cfg.d_mlp, cfg.head_dim, cfg.n_q_heads, cfg.n_layers, cfg.n_patches
+    per_row = 2 * cfg.patch_dim * d + L * (2 * d * 3 * H * D + 2 * H * D * d + 2 * d * F * 2) + 2 * d * cfg.d_out
+    per_img = N * per_row + L * 4 * N * N * H * D
+    return B * cfg.n_images * per_img
+
+
+def leg_vision(args, px, wl, K, W):
+    """The vision tower (image patches to the image tokens that open the
+    prefix) on the SigLIP-class workload, batch 1: ms per call, MFMA
+    throughput, and per-stage launch times (graph replays)."""
+    import torch
+    cfg = wl.CONFIGS["vit_siglip_bf16_b1"]
+    _log(f"generating {cfg.name}")
+    case = wl.make_vision_case(cfg, seed=args.seed)
+    m = px.VisionTower(cfg, case.weights)
+    del case.weights
+    pt = torch.from_numpy(case.patches).cuda()
+    out = torch.empty((cfg.batch, cfg.n_images * cfg.n_patches, cfg.d_out), dtype=torch.float32, device="cuda")
+    _log(f"timing {cfg.name}")
+    wall, per = time_calls(lambda: m.encode(pt, out=out), K, W)
+    ms = float(np.median(per))
+    fl = vision_flops(cfg, cfg.batch)
+    tf = fl / (ms * 1e-3) / 1e12
+    rec = {"config": {"workload": "vision tower, SigLIP-class ViT (24 blocks of width 1024, 16 heads of 64, GELU "
+                                  "MLP 4096), 3 images of 256 patches of 768 values, projected to 2048, batch 1",
+                      "weights": "bf16"},
+           "ms_per_call": round(ms, 3), "p99_ms": round(float(np.percentile(per, 99)), 3),
+           "images_per_s": round(cfg.batch * cfg.n_images / (ms * 1e-3), 1),
+           "flops_per_call": int(fl), "TFLOPs": round(tf, 1),
+           "frac_of_bf16_peak": round(tf / BF16_PEAK_TFLOPS, 4)}
+    if not args.no_stages:
+        stages = {}
+        cap = torch.cuda.Stream()
+        for st in ("norm1", "qkv", "attn", "oproj", "norm2", "mlp_up", "mlp_down"):
+            m.profile_stage(st, 1)
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=cap):
+                m.profile_stage(st, 2)
+            g.replay()
+            torch.cuda.synchronize()
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            g.replay()
+            b.record()
+            torch.cuda.synchronize()
+            stages[st] = round(a.elapsed_time(b) * 1e3 / (2 * cfg.n_layers), 2)
+            del g
+        rec["stage_us"] = stages
+    m.close()
+    del pt, out
+    torch.cuda.empty_cache()
+    return rec
+
+
 def leg_batch64(args, px, wl, K, W):
     import torch
     cfg = wl.CONFIGS["pi0_fp8_b64"]
@@ -544,6 +605,7 @@ def main():
                     help="only the batch-64 leg (for counter passes; the line then has no batch-1 value)")
     ap.add_argument("--no-legs", action="store_true", help="skip the pi0.5, DiT and tiny fp32 workloads")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefix-LM workload")
+    ap.add_argument("--no-vision", action="store_true", help="skip the vision-tower workload")
     ap.add_argument("--no-stages", action="store_true",
                     help="skip the per-stage graph timings and the rooflines built on them (counter passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -577,6 +639,8 @@ def main():
                                                            env={"PHYAI_PERSIST": "1"})
     if not args.no_prefill:
         rec["prefill"] = leg_prefill(args, px, wl, max(1, min(K, 20)), min(W, 3))
+    if not args.no_vision:
+        rec["vision"] = leg_vision(args, px, wl, max(1, min(K, 20)), min(W, 3))
     if not args.no_batch64:
         rec["batch64"] = leg_batch64(args, px, wl, K, W)
     print(json.dumps(rec), flush=True)

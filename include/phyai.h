@@ -14,7 +14,9 @@
  * Batching").  The same library also runs the step before the loop: the
  * vision-language model's language part over the prefix tokens, which
  * produces that prefix K/V cache (phyai_prefill, on a handle of variant
- * PHYAI_VARIANT_PREFIX_LM).
+ * PHYAI_VARIANT_PREFIX_LM), and the vision tower before it, which turns the
+ * camera images into the image tokens at the head of that prefix
+ * (phyai_encode_images, variant PHYAI_VARIANT_VISION).
  *
  * Every step runs in hand-written HIP kernels; the K-step loop is captured
  * in a HIP graph per (batch, steps) bucket and replayed.
@@ -50,8 +52,10 @@ typedef enum {
   PHYAI_VARIANT_PI0 = 0,    /* time mixed into action tokens by a 2-layer MLP; optional state token */
   PHYAI_VARIANT_PI05 = 1,   /* adaRMSNorm timestep conditioning in every norm                      */
   PHYAI_VARIANT_DIT = 2,    /* DiT head: adaLN-zero, alternating cross/self attention              */
-  PHYAI_VARIANT_PREFIX_LM = 3  /* the VLM's language part over the prefix tokens, producing the prefix
+  PHYAI_VARIANT_PREFIX_LM = 3, /* the VLM's language part over the prefix tokens, producing the prefix
                                   K/V cache the pi0 / pi0.5 experts read (see phyai_prefill)        */
+  PHYAI_VARIANT_VISION = 4     /* the VLM's vision tower: image patches to the image tokens that open
+                                  the prefix (see phyai_encode_images)                              */
 } phyai_variant;
 
 typedef enum {
@@ -93,6 +97,10 @@ typedef struct {
   float sin_min_period;     /* sinusoid periods run geometrically from min to max                 */
   float sin_max_period;
   float rope_base;          /* 10000                                                              */
+  int32_t n_images;         /* VISION: images per request; 0 otherwise                           */
+  int32_t n_patches;        /* VISION: patches (tokens) per image                                 */
+  int32_t patch_dim;        /* VISION: values per patch (multiple of 64)                          */
+  int32_t d_out;            /* VISION: width of the projected image tokens (multiple of 32)       */
 } phyai_config;
 
 /* PHYAI_VARIANT_PREFIX_LM uses n_layers, d_model, n_q_heads, n_kv_heads,
@@ -102,12 +110,23 @@ typedef struct {
  * max_steps, time_dim and the sinusoid periods are ignored, state_token and
  * d_feat must be 0, prefix_cap >= 1.  Its blocks are the pi0 trunk's
  * (RMSNorm with gain (1 + w), fused QKV, GeGLU MLP, residual adds) with a
- * bidirectional mask over the valid prefix tokens. */
+ * bidirectional mask over the valid prefix tokens.
+ *
+ * PHYAI_VARIANT_VISION uses n_layers, d_model, n_q_heads = n_kv_heads,
+ * head_dim, d_mlp, max_batch (requests; max_batch * n_images <= 512),
+ * weight_dtype, kv_dtype, rms_eps (the LayerNorm epsilon), n_images,
+ * n_patches, patch_dim and d_out; rope, state_token and d_feat must be 0 and
+ * the other fields are ignored.  Its blocks are a pre-norm vision
+ * transformer's (LayerNorm with gain (1 + w) and bias, multi-head attention
+ * with biased projections over the patches of one image, GELU MLP with
+ * biases, residual adds), after a linear patch embedding plus a learned
+ * position embedding and before a final LayerNorm and a linear projector to
+ * d_out. */
 
 /* One named parameter, stored [rows][cols] row-major on the host.  Linear
  * weights are [in][out] (y = x W + b); vectors have rows = 1.  dtype must be
  * the config's weight_dtype for the per-layer trunk linears
- * (wq, wk, wv, wo, w_gate, w_up, w_down; DiT: mlp_w1, mlp_w2) and F32 or BF16 (matching the path:
+ * (wq, wk, wv, wo, w_gate, w_up, w_down; DiT and VISION: mlp_w1, mlp_w2) and F32 or BF16 (matching the path:
  * F32 for the fp32 path, BF16 otherwise) for every other tensor.  For
  * FP8E4M3, `scale` holds `cols` float32 scales (W_ij = code_ij * scale_j).
  * For FP4E2M1, `data` holds rows x cols/2 bytes (byte (i, j) = the codes of
@@ -151,6 +170,11 @@ typedef struct phyai_expert phyai_expert;
  *          layers.l.{wo, mlp_norm, w_gate, w_up, w_down} for every layer but
  *          the last (whose keys and values depend only on its input); no
  *          in/out, time or state tensors
+ *   VISION: patch_w [patch_dim][d], patch_b [1][d], pos_emb [n_patches][d],
+ *          layers.l.{ln1_w, ln1_b, ln2_w, ln2_b} [1][d],
+ *          layers.l.{wq, wk, wv, wo} [d][d], layers.l.{bq, bk, bv, bo} [1][d],
+ *          layers.l.mlp_w1 [d][F], mlp_b1 [1][F], mlp_w2 [F][d], mlp_b2 [1][d],
+ *          post_ln_w, post_ln_b [1][d], proj_w [d][d_out], proj_b [1][d_out]
  * Host buffers may be freed after the call returns.  On failure *out is set
  * to NULL and nothing is leaked.  The call synchronises `stream`. */
 int phyai_load_expert(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_tensors,
@@ -255,6 +279,38 @@ int phyai_denoise_static(phyai_expert* e, const void* prefix, const int32_t* pre
  * fails.  The denoising entry points refuse a prefix-LM handle. */
 int phyai_prefill(phyai_expert* e, const float* embeds, const int32_t* prefix_len, void* kv_out, int32_t batch,
                   void* stream);
+
+/* Encode the camera images of a batch of requests into image tokens (handle
+ * of variant PHYAI_VARIANT_VISION).
+ *
+ * Operation: the vision-tower phase of the pi-family, which the paper times
+ * separately from the language prefix and the action expert (Section
+ * "Evaluation", batch analysis of PI0.5); its tokens are the first rows of
+ * the prefix embeddings that phyai_prefill takes.  Per image: h = patches
+ * W_patch + b_patch + pos_emb; per block h += Attn(LN1(h)) W_o + b_o (every
+ * patch attends to every patch of its own image, scale 1/sqrt(head_dim)),
+ * h += GELU_tanh(LN2(h) W_1 + b_1) W_2 + b_2; tokens = LN_post(h) W_proj +
+ * b_proj, with LN(x) = (x - mean) / sqrt(var + rms_eps) * (1 + w) + b.
+ *
+ *   patches     device float32 [B][n_images][n_patches][patch_dim]: the
+ *               images already cut into patches and normalised.
+ *   tokens_out  device float32 [B][out_rows][d_out]: rows 0 ..
+ *               n_images*n_patches-1 of request b receive its image tokens,
+ *               image-major; rows from n_images*n_patches on are not
+ *               touched (so a prefix-embedding buffer [B][prefix_cap][d]
+ *               with d = d_out can take the text embeddings there).
+ *               Caller-owned.
+ *   out_rows    rows per request in tokens_out, >= n_images*n_patches.
+ *   batch       B requests, 1 <= B <= max_batch.
+ *   stream      work is enqueued on it; the call returns after enqueueing.
+ *
+ * patches and tokens_out must be 16-byte aligned.  Calls on one handle must
+ * be ordered on the device (they share its working buffers).  Errors:
+ * PHYAI_EINVAL for a NULL or non-vision handle, a NULL or misaligned
+ * pointer, a batch or out_rows out of range; PHYAI_EHIP if a launch fails.
+ * The denoising entry points and phyai_prefill refuse a vision handle. */
+int phyai_encode_images(phyai_expert* e, const float* patches, float* tokens_out, int32_t out_rows,
+                        int32_t batch, void* stream);
 
 /* Capture the graph of the K-step loop for the (batch, n_steps) bucket ahead
  * of the first phyai_denoise with that shape, so that the first prediction

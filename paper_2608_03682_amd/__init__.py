@@ -17,13 +17,13 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libphyai.so")
 
 PHYAI_OK, PHYAI_EINVAL, PHYAI_ENOMEM, PHYAI_EHIP, PHYAI_EUNSUPPORTED = 0, -1, -2, -3, -4
-_VARIANT = {"pi0": 0, "pi05": 1, "dit": 2, "prefix_lm": 3}
+_VARIANT = {"pi0": 0, "pi05": 1, "dit": 2, "prefix_lm": 3, "vision": 4}
 _DTYPE = {"f32": 0, "bf16": 1, "fp8": 2, "fp4": 3}
 
 # Every symbol include/phyai.h declares.
 EXPORTS = ("phyai_load_expert", "phyai_denoise", "phyai_denoise_static", "phyai_prepare", "phyai_debug_hidden",
            "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_free_expert", "phyai_last_error",
-           "phyai_version", "phyai_prefill")
+           "phyai_version", "phyai_prefill", "phyai_encode_images")
 STAGES = {"norm1": 0, "qkv": 1, "attn": 2, "oproj": 3, "norm2": 4, "mlp_up": 5, "mlp_down": 6}
 
 
@@ -38,7 +38,8 @@ class Config(ctypes.Structure):
         "variant", "n_layers", "d_model", "n_q_heads", "n_kv_heads", "head_dim", "d_mlp", "horizon",
         "action_dim", "max_steps", "prefix_cap", "max_batch", "state_token", "rope", "weight_dtype",
         "kv_dtype", "d_feat", "time_dim")] + [(n, ctypes.c_float) for n in (
-        "rms_eps", "sin_min_period", "sin_max_period", "rope_base")]
+        "rms_eps", "sin_min_period", "sin_max_period", "rope_base")] + [(n, ctypes.c_int32) for n in (
+        "n_images", "n_patches", "patch_dim", "d_out")]
 
 
 class Tensor(ctypes.Structure):
@@ -66,11 +67,13 @@ def lib() -> ctypes.CDLL:
         L.phyai_fp8_to_bf16.argtypes = [vp, vp, i64, vp]
         L.phyai_profile_stage.argtypes = [vp, i32, i32, vp]
         L.phyai_prefill.argtypes = [vp, vp, vp, vp, i32, vp]
+        L.phyai_encode_images.argtypes = [vp, vp, vp, i32, i32, vp]
         L.phyai_free_expert.argtypes = [vp]
         L.phyai_free_expert.restype = None
         L.phyai_last_error.restype = ctypes.c_char_p
         for f in ("phyai_load_expert", "phyai_denoise", "phyai_denoise_static", "phyai_prepare", "phyai_debug_hidden",
-                  "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_version", "phyai_prefill"):
+                  "phyai_profile_stage", "phyai_fp8_to_bf16", "phyai_version", "phyai_prefill",
+                  "phyai_encode_images"):
             getattr(L, f).restype = ctypes.c_int
         _lib_handle = L
     return _lib_handle
@@ -107,7 +110,8 @@ def make_config(cfg, max_batch: Optional[int] = None, max_steps: Optional[int] =
         state_token=int(cfg.state_token), rope=int(cfg.rope), weight_dtype=_DTYPE[cfg.weight_dtype],
         kv_dtype=_DTYPE[cfg.kv_dtype], d_feat=cfg.d_feat, time_dim=cfg.time_dim,
         rms_eps=cfg.rms_eps, sin_min_period=cfg.sin_min_period, sin_max_period=cfg.sin_max_period,
-        rope_base=cfg.rope_base)
+        rope_base=cfg.rope_base, n_images=getattr(cfg, "n_images", 0), n_patches=getattr(cfg, "n_patches", 0),
+        patch_dim=getattr(cfg, "patch_dim", 0), d_out=getattr(cfg, "d_out", 0))
 
 
 def _tensor_array(weights: Dict[str, object]):
@@ -224,6 +228,53 @@ class PrefixLM:
     def profile_stage(self, stage: str, reps: int, stream=None):
         """Enqueue `reps` passes over the layers of one block stage (timing aid;
         needs a previous prefill)."""
+        _check(lib().phyai_profile_stage(self._h, STAGES[stage], reps, _stream(stream)))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().phyai_free_expert(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class VisionTower:
+    """One loaded vision tower (variant ``vision``): image patches in, the
+    image tokens that open the prefix out (``phyai_encode_images``)."""
+
+    def __init__(self, cfg, weights: Dict[str, object], max_batch: Optional[int] = None, stream=None):
+        if cfg.variant != "vision":
+            raise ValueError("VisionTower needs a vision config")
+        self.cfg = cfg
+        c = make_config(cfg, max_batch, 0)
+        arr, keep = _tensor_array(weights)
+        h = ctypes.c_void_p()
+        _check(lib().phyai_load_expert(ctypes.byref(c), arr, len(weights), _stream(stream), ctypes.byref(h)))
+        del keep
+        self._h = h
+
+    def encode(self, patches, out=None, out_rows: Optional[int] = None, stream=None):
+        """patches: device float32 [B][n_images][n_patches][patch_dim].  Returns
+        (or fills rows 0 .. n_images*n_patches-1 of each request's slab of)
+        the device float32 tokens [B][out_rows][d_out]; out_rows defaults to
+        out's second dimension, or n_images*n_patches for a new buffer."""
+        c = self.cfg
+        B = int(patches.shape[0])
+        n_tok = c.n_images * c.n_patches
+        if out is None:
+            import torch
+            out = torch.empty((B, out_rows or n_tok, c.d_out), dtype=torch.float32, device=patches.device)
+        rows = out_rows if out_rows is not None else int(out.shape[1])
+        _check(lib().phyai_encode_images(self._h, _ptr(patches), _ptr(out), rows, B, _stream(stream)))
+        return out
+
+    def profile_stage(self, stage: str, reps: int, stream=None):
+        """Enqueue `reps` passes over the blocks of one stage (timing aid; needs
+        a previous encode)."""
         _check(lib().phyai_profile_stage(self._h, STAGES[stage], reps, _stream(stream)))
 
     def close(self):

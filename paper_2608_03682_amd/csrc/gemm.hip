@@ -893,12 +893,15 @@ int gemm_split_k(int R, int NPT, int K) {
   if (R >= 256) {
     // many rows: the one-tile-per-CU ring splits K when its tiles fill at
     // most half the CUs (the prefix LM's O and down projections: 112 tiles)
-    // and each slice keeps at least 16 k-blocks; PHYAI_GEMM_TILE (tests)
-    // forces a kernel without the split
+    // and each slice keeps at least 16 k-blocks, or 4 when the tiles fill at
+    // most a quarter of the CUs (the vision tower's O projection, 48 tiles
+    // of K = 1024: 14.8 -> 8.8 us, the norm adding the slices 3 -> 5 us);
+    // PHYAI_GEMM_TILE (tests) forces a kernel without the split
     if (getenv("PHYAI_GEMM_TILE") || NPT % 4 != 0) return 1;
     const int tiles = ((R + 127) / 128) * (NPT / 4);
+    const int minkb = tiles <= 64 ? 4 : 16;
     int s = 1;
-    while (s < 4 && tiles * s * 2 <= 256 && (K / 64) % (2 * s) == 0 && K / 64 / (2 * s) >= 16) s *= 2;
+    while (s < 4 && tiles * s * 2 <= 256 && (K / 64) % (2 * s) == 0 && K / 64 / (2 * s) >= minkb) s *= 2;
     return s;
   }
   const int blocks = NPT * ((R + 15) / 16);

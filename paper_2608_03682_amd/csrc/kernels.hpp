@@ -201,6 +201,8 @@ struct EpiGeglu {
 // two halves that RoPE rotates together.  q goes to [R][nq*D]; k and v go
 // into the layer's key range (K [b][kvh][key][D], V transposed
 // [b][kvh][D][key]) at key = (prefix_len[b] if keys_after_prefix) + token.
+// An optional bias [(nq + 2 nkv) * D], in the unpacked head order, is added
+// before RoPE.
 template <typename OutT>
 struct EpiQkv {
   static constexpr bool kWaveTile = true;   // see wave_tile
@@ -212,6 +214,7 @@ struct EpiQkv {
   int keys_after_prefix;
   const float2* rope_cs;    // [rows][D/2]: (cos, sin) of position * base^(-2i/D)
   const CallDesc* desc;     // positions start at prefix_len[b]
+  const float* bias;        // or null
   struct ColPre {};
   struct Pre { float2 cs; int plen; };
   __device__ __forceinline__ ColPre colpre(int, int) const { return ColPre{}; }
@@ -229,6 +232,10 @@ struct EpiQkv {
     const int head = p / tiles;
     const int i = 16 * (p % tiles) + c;
     const int b = r / M, tok = r % M;
+    if (bias) {
+      a0 += bias[head * D + i];
+      a1 += bias[head * D + i + D / 2];
+    }
     if (rope && head < nq + nkv) {
       const float x1 = a0, x2 = a1;
       a0 = x1 * q.cs.x - x2 * q.cs.y;
@@ -278,7 +285,7 @@ struct EpiQkv {
       sc[pp][0] = g.scale ? g.scale[32 * (p0 + pp) + lc] : 1.f;
       sc[pp][1] = g.scale ? g.scale[32 * (p0 + pp) + 16 + lc] : 1.f;
     }
-    if (r0 + 64 > g.R) {
+    if (r0 + 64 > g.R) {      // bias added by the per-element form
 #pragma unroll
       for (int pp = 0; pp < 2; ++pp)
 #pragma unroll
@@ -290,6 +297,15 @@ struct EpiQkv {
               (*this)(row, p0 + pp, lc, acc[mt][2 * pp][v] * sc[pp][0], acc[mt][2 * pp + 1][v] * sc[pp][1]);
           }
       return;
+    }
+    float bs[2][2] = {{0.f, 0.f}, {0.f, 0.f}};
+    if (bias) {
+#pragma unroll
+      for (int pp = 0; pp < 2; ++pp) {
+        const int i = 16 * ((p0 + pp) % tiles) + lc;
+        bs[pp][0] = bias[head * D + i];
+        bs[pp][1] = bias[head * D + i + D / 2];
+      }
     }
     auto emit = [&](auto kind) {
       constexpr int KIND = decltype(kind)::value;     // 0: q, 1: k, 2: v
@@ -313,7 +329,8 @@ struct EpiQkv {
           for (int v = 0; v < 4; ++v) {
             const int row = r0 + 16 * mt + 4 * lg + v;
             const int i = 16 * ((p0 + pp) % tiles) + lc;
-            const float x1 = acc[mt][2 * pp][v] * sc[pp][0], x2 = acc[mt][2 * pp + 1][v] * sc[pp][1];
+            const float x1 = acc[mt][2 * pp][v] * sc[pp][0] + bs[pp][0];
+            const float x2 = acc[mt][2 * pp + 1][v] * sc[pp][1] + bs[pp][1];
             float a0 = x1, a1 = x2;
             if (KIND < 2 && rope) {
               a0 = x1 * cs[pp][v].x - x2 * cs[pp][v].y;
@@ -340,7 +357,7 @@ struct EpiQkv {
     else {
       if constexpr (std::is_same<OutT, bf16_t>::value) {
         if (st != nullptr) {
-          store_v_staged(acc, sc, r0, p0, lc, lg, st);
+          store_v_staged(acc, sc, bs, r0, p0, lc, lg, st);
           return;
         }
       }
@@ -348,8 +365,9 @@ struct EpiQkv {
     }
   }
 
-  __device__ __forceinline__ void store_v_staged(const f32x4 (&acc)[4][4], const float (&sc)[2][2], int r0, int p0,
-                                                 int lc, int lg, bf16_t* st) const {
+  __device__ __forceinline__ void store_v_staged(const f32x4 (&acc)[4][4], const float (&sc)[2][2],
+                                                 const float (&bs)[2][2], int r0, int p0, int lc, int lg,
+                                                 bf16_t* st) const {
     const int tiles = D / 32;
     const int head = p0 / tiles;
     {
@@ -360,8 +378,8 @@ struct EpiQkv {
 #pragma unroll
           for (int v = 0; v < 4; ++v) {
             const int row = 16 * mt + 4 * lg + v;
-            st[(32 * pp + lc) * kVRow + row] = f32_to_bf16(acc[mt][2 * pp][v] * sc[pp][0]);
-            st[(32 * pp + 16 + lc) * kVRow + row] = f32_to_bf16(acc[mt][2 * pp + 1][v] * sc[pp][1]);
+            st[(32 * pp + lc) * kVRow + row] = f32_to_bf16(acc[mt][2 * pp][v] * sc[pp][0] + bs[pp][0]);
+            st[(32 * pp + 16 + lc) * kVRow + row] = f32_to_bf16(acc[mt][2 * pp + 1][v] * sc[pp][1] + bs[pp][1]);
           }
       const int lane = 16 * lg + lc;
       const int row = r0 + lane;
@@ -561,6 +579,13 @@ void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B,
 // rows past the prefix are never read).  d a multiple of 4, embeds 16-byte
 // aligned.
 void prefill_embed(const CallDesc* desc, const float* embeds, float* h, int B, int M, int d, hipStream_t);
+// Vision tower input: patches [R][patch_dim] float32 into the GEMM operand
+// `a` (bf16 or float32, same layout) and the position embedding of each row's
+// patch (row % n_patches) into the residual stream h [R][d].
+void vision_embed_bf16(const float* patches, bf16_t* a, float* h, const float* pos, int R, int n_patches,
+                       int patch_dim, int d, hipStream_t);
+void vision_embed_f32(const float* patches, float* a, float* h, const float* pos, int R, int n_patches,
+                      int patch_dim, int d, hipStream_t);
 void fp8_to_bf16(const uint8_t* codes, bf16_t* out, int64_t n, hipStream_t);
 
 // ---------------------------------------------------------------------------

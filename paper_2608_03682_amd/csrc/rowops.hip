@@ -737,6 +737,26 @@ __global__ __launch_bounds__(256) void prefill_embed_kernel(const CallDesc* desc
   for (int i = threadIdx.x; i < d / 4; i += 256) dst[i] = valid ? src[i] : make_float4(0.f, 0.f, 0.f, 0.f);
 }
 
+// One block per patch row: the patch (patch_dim a multiple of 64) converted
+// into the patch-embedding GEMM's operand, and the row's position embedding
+// into the residual stream (the GEMM then adds x W + b on top).
+template <typename T>
+__global__ __launch_bounds__(256) void vision_embed_kernel(const float* __restrict__ patches, T* __restrict__ a,
+                                                           float* __restrict__ h, const float* __restrict__ pos,
+                                                           int n_patches, int patch_dim, int d) {
+  const int row = blockIdx.x;
+  const float4* src = reinterpret_cast<const float4*>(patches + (int64_t)row * patch_dim);
+  T* dst = a + (int64_t)row * patch_dim;
+  for (int i = threadIdx.x; i < patch_dim / 4; i += 256) {
+    const float4 v = src[i];
+    const float w[4] = {v.x, v.y, v.z, v.w};
+    ActIO<T>::store4(dst + 4 * i, w);
+  }
+  const float4* ps = reinterpret_cast<const float4*>(pos + (int64_t)(row % n_patches) * d);
+  float4* hd = reinterpret_cast<float4*>(h + (int64_t)row * d);
+  for (int i = threadIdx.x; i < d / 4; i += 256) hd[i] = ps[i];
+}
+
 __global__ void copy_in_kernel(const CallDesc* desc, float* x, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) x[i] = desc->noise[i];
@@ -842,6 +862,18 @@ void rope_table(const CallDesc* desc, const float* inv_freq, float2* tab, int B,
 }
 void prefill_embed(const CallDesc* desc, const float* embeds, float* h, int B, int M, int d, hipStream_t s) {
   if (B * M > 0) hipLaunchKernelGGL(prefill_embed_kernel, dim3(B * M), dim3(256), 0, s, desc, embeds, h, M, d);
+}
+void vision_embed_bf16(const float* patches, bf16_t* a, float* h, const float* pos, int R, int n_patches,
+                       int patch_dim, int d, hipStream_t s) {
+  if (R > 0)
+    hipLaunchKernelGGL(vision_embed_kernel<bf16_t>, dim3(R), dim3(256), 0, s, patches, a, h, pos, n_patches,
+                       patch_dim, d);
+}
+void vision_embed_f32(const float* patches, float* a, float* h, const float* pos, int R, int n_patches,
+                      int patch_dim, int d, hipStream_t s) {
+  if (R > 0)
+    hipLaunchKernelGGL(vision_embed_kernel<float>, dim3(R), dim3(256), 0, s, patches, a, h, pos, n_patches,
+                       patch_dim, d);
 }
 void set_call_desc(const CallDesc& d, CallDesc* dev, hipStream_t s) {
   hipLaunchKernelGGL(set_desc_kernel, dim3(1), dim3(256), 0, s, d, dev);

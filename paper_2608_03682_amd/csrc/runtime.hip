@@ -79,6 +79,8 @@ struct LayerW {
   Lin qkv, kv_cross, o, gu, down, attn_mod, mlp_mod, ada;
   float *attn_norm = nullptr, *mlp_norm = nullptr;
   float *attn_mod_b = nullptr, *mlp_mod_b = nullptr, *ada_b = nullptr, *mlp_b1 = nullptr, *mlp_b2 = nullptr;
+  // vision tower: LayerNorm biases, the fused [q | k | v] bias and the O bias
+  float *attn_norm_b = nullptr, *mlp_norm_b = nullptr, *qkv_b = nullptr, *o_b = nullptr;
 };
 
 struct Bucket {
@@ -102,6 +104,10 @@ struct phyai_expert {
   float *out_w = nullptr, *out_b = nullptr, *final_norm = nullptr;
   float *time_b1 = nullptr, *time_b2 = nullptr, *cond_b1 = nullptr, *cond_b2 = nullptr, *final_b = nullptr;
   Lin time_w1t, time_w2, cond_w1, cond_w2, final_mod;
+  // vision tower: patch embedding, final LayerNorm bias, projector
+  Lin patch_lin, proj_lin;
+  float *patch_b = nullptr, *final_norm_b = nullptr, *proj_b = nullptr;
+  int n_img = 1;            // images per request (vision); 1 otherwise
   std::vector<LayerW> layers;
   float* inv_freq = nullptr;
   float2* rope_cs = nullptr;   // per-call RoPE table [max_batch * M][D/2]
@@ -215,6 +221,17 @@ float* upload_f32(phyai_expert& e, const phyai_tensor* t, hipStream_t s) {
   for (int64_t i = 0; i < n; ++i) v[i] = elem_f32(t, i);
   float* p = e.mem.alloc_n<float>(n);
   HIPC(hipMemcpyAsync(p, v.data(), n * 4, hipMemcpyHostToDevice, s));
+  HIPC(hipStreamSynchronize(s));
+  return p;
+}
+
+// Vectors ([1][n] each) concatenated into one fp32 device array.
+float* upload_concat_f32(phyai_expert& e, const std::vector<const phyai_tensor*>& srcs, hipStream_t s) {
+  std::vector<float> v;
+  for (auto* t : srcs)
+    for (int64_t i = 0; i < (int64_t)t->rows * t->cols; ++i) v.push_back(elem_f32(t, i));
+  float* p = e.mem.alloc_n<float>(v.size());
+  HIPC(hipMemcpyAsync(p, v.data(), v.size() * 4, hipMemcpyHostToDevice, s));
   HIPC(hipStreamSynchronize(s));
   return p;
 }
@@ -421,6 +438,10 @@ int attn_splits_for(int B, int rows, int nkv, int keys, int rpb) {
   const int cap = (keys + 63) / 64;                     // at least one 64-key tile per split
   if (s > cap) s = cap;
   if (s > 16) s = 16;                                   // the merge kernel takes up to 16
+  // a few key tiles over a grid that already covers a quarter of the chip:
+  // the combine launch costs more than the split saves (vision tower, 256
+  // keys, 96 blocks: 7.0 us unsplit against 12.8 with 3 splits + combine)
+  if (cap <= 4 && base >= 64) s = 1;
   return s < 1 ? 1 : s;
 }
 int attn_splits(int B, int rows, int nkv, int keys) {
@@ -499,6 +520,7 @@ PendingResid pending_of(const phyai_expert& e, int which, int l, int k, int B) {
     p.gate = which == 0 ? ada + 2 * e.d : ada + 5 * e.d;
     p.bias = which == 0 ? nullptr : e.layers[l].mlp_b2;
   }
+  if (e.c.variant == PHYAI_VARIANT_VISION) p.bias = which == 0 ? e.layers[l].o_b : e.layers[l].mlp_b2;
   return p;
 }
 
@@ -515,8 +537,10 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
   const int R = B * M;
   T* n = static_cast<T*>(e.n);
   T* q = static_cast<T*>(e.q);
-  T* kl = static_cast<T*>(e.kall) + (int64_t)l * e.kv_layer;
-  T* vl = static_cast<T*>(e.vt) + (int64_t)l * e.kv_layer;
+  // the vision tower needs a block's keys only inside that block: one range
+  const int64_t kv_slot = e.c.variant == PHYAI_VARIANT_VISION ? 0 : l;
+  T* kl = static_cast<T*>(e.kall) + kv_slot * e.kv_layer;
+  T* vl = static_cast<T*>(e.vt) + kv_slot * e.kv_layer;
   T* o = static_cast<T*>(e.o);
   T* g = static_cast<T*>(e.g);
   T* n_lo = static_cast<T*>(e.n_lo);
@@ -575,6 +599,38 @@ void layer_stage(phyai_expert& e, int stage, int l, int k, int B, hipStream_t s)
     else gemm_resid(ga, er, s);
   };
 
+  if (variant == PHYAI_VARIANT_VISION) {
+    // pre-norm ViT block over the patches of each image (the rows of one
+    // image are one "request" of M = n_patches keys, all valid)
+    switch (stage) {
+      case ST_NORM1: {
+        const PendingResid pd = l > 0 ? pending_of(e, 1, l - 1, k, B) : PendingResid{};
+        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, w.attn_norm, w.attn_norm_b, pd, s);
+        break;
+      }
+      case ST_QKV: {
+        EpiQkv<T> eq{q, kl, vl, D, e.nq, e.nkv, 0, M, e.ldk, 0, nullptr, e.desc, w.qkv_b};
+        gemm_qkv(gargs(w.qkv, n, d, R), eq, s);
+        break;
+      }
+      case ST_ATTN: {
+        at.keys_from_prefix = 1;
+        at.n_suffix = 0;
+        at.mask_mode = 0;
+        if (e.f32) attention_f32(at, s); else attention_bf16(at, s);
+        break;
+      }
+      case ST_OPROJ: oproj(EpiResid{e.h, d, w.o_b, nullptr}); break;
+      case ST_NORM2:
+        norm_rows(e.h, n, n_lo, R, d, e.c.rms_eps, NORM_LN, w.mlp_norm, w.mlp_norm_b, pending_of(e, 0, l, k, B), s);
+        break;
+      case ST_MLP_UP:
+        gemm_store(gargs(w.gu, n, d, R), store_epi<T>(g, e.F, w.mlp_b1, nullptr, ACT_GELU), s);
+        break;
+      case ST_MLP_DOWN: gemm_resid(with_split(gargs(w.down, g, e.F, R), 1), EpiResid{e.h, d, w.mlp_b2, nullptr}, s); break;
+    }
+    return;
+  }
   if (variant != PHYAI_VARIANT_DIT) {
     const float* mul1 = w.attn_norm;
     const float* sh1 = nullptr;
@@ -926,9 +982,35 @@ void enqueue_prefill(phyai_expert& e, const float* embeds, void* kv_out, int B, 
   }
 }
 
+// The vision tower over B requests (B * n_img images of M = n_patches rows):
+// patches into the GEMM operand and position embeddings into the residual
+// stream, the patch-embedding GEMM adding x W + b on top, the blocks, the
+// final LayerNorm (folding the last block's pending residual), and the
+// projector writing each request's tokens at rows 0 .. n_img*M-1 of its
+// out_rows-row slab of the caller's buffer.  Eager launches, like the prefill.
+template <typename T>
+void enqueue_vision(phyai_expert& e, const float* patches, float* tokens_out, int out_rows, int B, hipStream_t s) {
+  const int Bi = B * e.n_img, R = Bi * e.M, d = e.d, pd = e.c.patch_dim;
+  T* a = static_cast<T*>(e.g);
+  if constexpr (std::is_same<T, float>::value)
+    vision_embed_f32(patches, a, e.h, e.pos, R, e.M, pd, d, s);
+  else
+    vision_embed_bf16(patches, a, e.h, e.pos, R, e.M, pd, d, s);
+  gemm_resid(gargs(e.patch_lin, a, pd, R), EpiResid{e.h, d, e.patch_b, nullptr}, s);
+  for (int l = 0; l < e.L; ++l)
+    for (int st = 0; st < kStages; ++st) layer_stage<T>(e, st, l, 0, Bi, s);
+  norm_rows(e.h, static_cast<T*>(e.n), static_cast<T*>(nullptr), R, d, e.c.rms_eps, NORM_LN, e.final_norm,
+            e.final_norm_b, pending_of(e, 1, e.L - 1, 0, Bi), s);
+  EpiStore<float> es = store_epi<float>(tokens_out, e.c.d_out, e.proj_b, nullptr, ACT_NONE);
+  es.grp = e.n_img * e.M;
+  es.grp_stride = out_rows;
+  es.grp_off = 0;
+  gemm_store(gargs(e.proj_lin, e.n, d, R), es, s);
+}
+
 void check_config(const phyai_config& c) {
   auto req = [](bool ok, const std::string& m) { if (!ok) fail(PHYAI_EINVAL, m); };
-  req(c.variant >= 0 && c.variant <= 3, "variant out of range");
+  req(c.variant >= 0 && c.variant <= 4, "variant out of range");
   req(c.n_layers >= 1 && c.d_model >= 64 && c.n_q_heads >= 1 && c.n_kv_heads >= 1, "non-positive size");
   req(c.n_q_heads % c.n_kv_heads == 0, "n_q_heads must be a multiple of n_kv_heads");
   req(c.head_dim == 64 || c.head_dim == 128 || c.head_dim == 256, "head_dim must be 64, 128 or 256");
@@ -939,7 +1021,16 @@ void check_config(const phyai_config& c) {
   req(c.prefix_cap >= 0, "prefix_cap < 0");
   req(c.weight_dtype >= 0 && c.weight_dtype <= 3, "weight_dtype out of range");
   req(c.rms_eps > 0.f, "rms_eps must be positive");
-  if (c.variant == PHYAI_VARIANT_PREFIX_LM) {
+  if (c.variant == PHYAI_VARIANT_VISION) {
+    // the patches of every image are the model's rows; no actions, steps,
+    // timestep tables or positions beyond the learned embedding
+    req(c.n_images >= 1 && c.n_patches >= 1, "a vision tower needs n_images >= 1 and n_patches >= 1");
+    req((int64_t)c.max_batch * c.n_images <= kMaxBatch, "max_batch * n_images must be at most 512");
+    req(c.patch_dim >= 64 && c.patch_dim % 64 == 0, "patch_dim must be a positive multiple of 64");
+    req(c.d_out >= 32 && c.d_out % 32 == 0, "d_out must be a positive multiple of 32");
+    req(c.n_q_heads == c.n_kv_heads, "vision attention has one key/value head per query head");
+    req(c.rope == 0 && c.state_token == 0 && c.d_feat == 0, "a vision tower has no RoPE, state token or features");
+  } else if (c.variant == PHYAI_VARIANT_PREFIX_LM) {
     // the prefix tokens are the model's rows: no actions, steps or timestep
     // tables; keys and values per layer leave in the prefix layout
     req(c.prefix_cap >= 1, "a prefix LM needs prefix_cap >= 1 rows");
@@ -1048,6 +1139,93 @@ void load_prefix_lm(const phyai_tensor* tensors, int32_t n_tensors, hipStream_t 
   HIPC(hipStreamSynchronize(s));
 }
 
+// The vision tower: M = n_patches rows per image, B * n_images images per
+// call; the key range of one block (reused by every block), no timestep
+// tables.  Tensors as listed in the header.
+void load_vision(const phyai_tensor* tensors, int32_t n_tensors, hipStream_t s, phyai_expert* e) {
+  const phyai_config& c = e->c;
+  e->F = c.d_mlp;
+  e->H = 0; e->A = 0; e->off = 0;
+  e->M = c.n_patches;
+  e->n_img = c.n_images;
+  e->P = 0;
+  e->qd = e->nq * e->D; e->kd = e->nkv * e->D;
+  e->Bmax = c.max_batch * c.n_images;    // image batch
+  e->Kmax = 0;
+  e->Wpre = e->kd;
+  const int d = e->d, L = e->L, D = e->D, F = e->F;
+  Params P;
+  for (int i = 0; i < n_tensors; ++i) {
+    if (!tensors[i].name) fail(PHYAI_EINVAL, "tensor with NULL name");
+    P.by_name[tensors[i].name] = &tensors[i];
+  }
+  const int wk_plain = e->f32 ? W_F32 : W_BF16;
+  const int wk_trunk = e->f32                                   ? W_F32
+                       : c.weight_dtype == PHYAI_DTYPE_FP8E4M3 ? W_FP8
+                       : c.weight_dtype == PHYAI_DTYPE_FP4E2M1 ? W_FP4 : W_BF16;
+  auto vec = [&](const std::string& n, int len) { return upload_f32(*e, P.get(n, 1, len), s); };
+  e->patch_lin = pack_identity(*e, {P.get("patch_w", c.patch_dim, d)}, wk_plain, s);
+  e->patch_b = vec("patch_b", d);
+  e->pos = upload_f32(*e, P.get("pos_emb", c.n_patches, d), s);
+  e->layers.resize(L);
+  for (int l = 0; l < L; ++l) {
+    LayerW& w = e->layers[l];
+    const std::string p = "layers." + std::to_string(l) + ".";
+    w.attn_norm = vec(p + "ln1_w", d);
+    w.attn_norm_b = vec(p + "ln1_b", d);
+    w.qkv = pack_heads(*e, {P.get(p + "wq", d, e->qd), P.get(p + "wk", d, e->kd), P.get(p + "wv", d, e->kd)}, D,
+                       wk_trunk, s);
+    w.qkv_b = upload_concat_f32(*e, {P.get(p + "bq", 1, e->qd), P.get(p + "bk", 1, e->kd), P.get(p + "bv", 1, e->kd)},
+                                s);
+    w.o = pack_identity(*e, {P.get(p + "wo", e->qd, d)}, wk_trunk, s);
+    w.o_b = vec(p + "bo", d);
+    w.mlp_norm = vec(p + "ln2_w", d);
+    w.mlp_norm_b = vec(p + "ln2_b", d);
+    w.gu = pack_identity(*e, {P.get(p + "mlp_w1", d, F)}, wk_trunk, s);
+    w.mlp_b1 = vec(p + "mlp_b1", F);
+    w.down = pack_identity(*e, {P.get(p + "mlp_w2", F, d)}, wk_trunk, s);
+    w.mlp_b2 = vec(p + "mlp_b2", d);
+  }
+  e->final_norm = vec("post_ln_w", d);
+  e->final_norm_b = vec("post_ln_b", d);
+  e->proj_lin = pack_identity(*e, {P.get("proj_w", d, c.d_out)}, wk_plain, s);
+  e->proj_b = vec("proj_b", c.d_out);
+  const int64_t Bm = e->Bmax, M = e->M, ab = e->act_bytes;
+  e->h = e->mem.alloc_n<float>(Bm * M * d);
+  e->n = e->mem.alloc(Bm * M * d * ab);
+  e->q = e->mem.alloc(Bm * M * e->qd * ab);
+  e->o = e->mem.alloc(Bm * M * e->qd * ab);
+  // the MLP activations, and before the blocks the patch-embedding operand
+  e->g = e->mem.alloc(Bm * M * std::max(F, c.patch_dim) * ab);
+  // one key range: keys 0 .. M-1 written by the QKV epilogue, the tail to
+  // the next multiple of 64 stays zero (attention reads whole tiles)
+  e->ldk = (M + 63) / 64 * 64;
+  e->kv_layer = Bm * e->nkv * (int64_t)e->ldk * D;
+  e->kall = e->mem.alloc(e->kv_layer * ab);
+  e->vt = e->mem.alloc(e->kv_layer * ab);
+  HIPC(hipMemsetAsync(e->kall, 0, e->kv_layer * ab, s));
+  HIPC(hipMemsetAsync(e->vt, 0, e->kv_layer * ab, s));
+  int64_t part = 0, pend = 4;
+  if (!e->f32)
+    for (int B = 1; B <= e->Bmax; ++B) {
+      const int rows = e->M * (e->nq / e->nkv);
+      part = std::max(part, attention_partial_floats(B, e->M, e->nq, e->nkv, D, attn_splits_max(B, rows, e->nkv, e->M)));
+      const int R = B * e->M;
+      for (int l = 0; l < L; ++l)
+        for (int which = 0; which < 2; ++which) {
+          const Lin& w = which == 0 ? e->layers[l].o : e->layers[l].down;
+          const int sk = std::max(resid_split(*e, which, l, B), gemm_split_k(R, w.NPT, w.K));
+          if (sk > 1) pend = std::max(pend, (int64_t)sk * R * d);
+        }
+    }
+  e->part = e->mem.alloc_n<float>(part > 0 ? part : 4);
+  e->pend = e->mem.alloc_n<float>(pend);
+  e->part_cur = e->part;
+  e->pend_cur = e->pend;
+  e->desc = static_cast<CallDesc*>(e->mem.alloc(sizeof(CallDesc)));
+  HIPC(hipStreamSynchronize(s));
+}
+
 void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_tensors, hipStream_t s,
                phyai_expert* e) {
   const phyai_config& c = *cfg;
@@ -1058,6 +1236,10 @@ void load_impl(const phyai_config* cfg, const phyai_tensor* tensors, int32_t n_t
   e->L = c.n_layers; e->d = c.d_model; e->D = c.head_dim; e->nq = c.n_q_heads; e->nkv = c.n_kv_heads;
   if (c.variant == PHYAI_VARIANT_PREFIX_LM) {
     load_prefix_lm(tensors, n_tensors, s, e);
+    return;
+  }
+  if (c.variant == PHYAI_VARIANT_VISION) {
+    load_vision(tensors, n_tensors, s, e);
     return;
   }
   e->H = c.horizon; e->A = c.action_dim; e->F = c.d_mlp;
@@ -1317,6 +1499,7 @@ void check_call(phyai_expert* e, const void* prefix, const int32_t* prefix_len, 
                 const float* timesteps, int n_steps, int batch, const float* state, const float* out_actions) {
   if (!e) fail(PHYAI_EINVAL, "NULL handle");
   if (e->c.variant == PHYAI_VARIANT_PREFIX_LM) fail(PHYAI_EINVAL, "a prefix-LM handle: call phyai_prefill");
+  if (e->c.variant == PHYAI_VARIANT_VISION) fail(PHYAI_EINVAL, "a vision handle: call phyai_encode_images");
   if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range 1..max_batch");
   if (n_steps < 1 || n_steps > e->Kmax) fail(PHYAI_EINVAL, "n_steps out of range 1..max_steps");
   if (!prefix_len || !noise || !timesteps || !out_actions) fail(PHYAI_EINVAL, "NULL argument");
@@ -1440,6 +1623,7 @@ int phyai_prepare(phyai_expert* e, int32_t batch, int32_t n_steps, void* stream)
   return run_guarded([&] {
     if (!e) fail(PHYAI_EINVAL, "NULL handle");
     if (e->c.variant == PHYAI_VARIANT_PREFIX_LM) fail(PHYAI_EINVAL, "a prefix-LM handle has no denoising loop");
+    if (e->c.variant == PHYAI_VARIANT_VISION) fail(PHYAI_EINVAL, "a vision handle has no denoising loop");
     if (batch < 1 || batch > e->Bmax) fail(PHYAI_EINVAL, "batch out of range");
     if (n_steps < 1 || n_steps > e->Kmax) fail(PHYAI_EINVAL, "n_steps out of range");
     if (use_graphs()) get_bucket(*e, batch, n_steps);
@@ -1558,6 +1742,28 @@ int phyai_prefill(phyai_expert* e, const float* embeds, const int32_t* prefix_le
     write_call_desc(*e, embeds, prefix_len, nullptr, batch, nullptr, nullptr, s);
     if (e->f32) enqueue_prefill<float>(*e, embeds, kv_out, batch, s);
     else enqueue_prefill<bf16_t>(*e, embeds, kv_out, batch, s);
+    HIPC(hipGetLastError());
+  });
+}
+
+int phyai_encode_images(phyai_expert* e, const float* patches, float* tokens_out, int32_t out_rows,
+                        int32_t batch, void* stream) {
+  return run_guarded([&] {
+    if (!e) fail(PHYAI_EINVAL, "NULL handle");
+    if (e->c.variant != PHYAI_VARIANT_VISION) fail(PHYAI_EINVAL, "not a vision handle");
+    if (batch < 1 || batch > e->c.max_batch) fail(PHYAI_EINVAL, "batch out of range 1..max_batch");
+    if (!patches || !tokens_out) fail(PHYAI_EINVAL, "NULL argument");
+    if (out_rows < e->n_img * e->M) fail(PHYAI_EINVAL, "out_rows < n_images * n_patches");
+    auto aligned16 = [](const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; };
+    if (!aligned16(patches) || !aligned16(tokens_out))
+      fail(PHYAI_EINVAL, "patches and tokens_out must be 16-byte aligned");
+    hipStream_t s = static_cast<hipStream_t>(stream);
+    // every image is one attention "request" whose M patches are all valid keys
+    const int Bi = batch * e->n_img;
+    std::vector<int32_t> keys(Bi, e->M);
+    write_call_desc(*e, nullptr, keys.data(), nullptr, Bi, nullptr, nullptr, s);
+    if (e->f32) enqueue_vision<float>(*e, patches, tokens_out, out_rows, batch, s);
+    else enqueue_vision<bf16_t>(*e, patches, tokens_out, out_rows, batch, s);
     HIPC(hipGetLastError());
   });
 }

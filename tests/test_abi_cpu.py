@@ -93,3 +93,26 @@ def test_prefix_lm_rejections_before_device_work():
     rc = L.phyai_load_expert(ctypes.byref(cfg), (px.Tensor * 1)(), 0, None, ctypes.byref(h))
     assert rc == px.PHYAI_EINVAL and not h.value
     assert b"missing tensor 'layers.0.attn_norm'" in L.phyai_last_error()
+
+
+def test_vision_rejections_before_device_work():
+    """The vision variant: its own config rules and tensor list, and the
+    encode entry point's NULL handling (no GPU needed)."""
+    import workloads as wl
+    L = px.lib()
+    assert L.phyai_encode_images(None, None, None, 768, 1, None) == px.PHYAI_EINVAL
+    assert b"NULL" in L.phyai_last_error()
+    base = wl.CONFIGS["vit_siglip_bf16_b1"]
+    h = ctypes.c_void_p()
+    for field, value, needle in [("patch_dim", 100, b"patch_dim"), ("d_out", 48, b"d_out"),
+                                 ("n_kv_heads", 4, b"one key/value head per query head"),
+                                 ("rope", 1, b"no RoPE"), ("n_images", 0, b"n_images >= 1"),
+                                 ("max_batch", 200, b"max_batch * n_images")]:
+        cfg = px.make_config(base, max_steps=0)
+        setattr(cfg, field, value)
+        assert L.phyai_load_expert(ctypes.byref(cfg), None, 0, None, ctypes.byref(h)) == px.PHYAI_EINVAL, field
+        assert needle in L.phyai_last_error(), (field, L.phyai_last_error())
+    cfg = px.make_config(base, max_steps=0)
+    rc = L.phyai_load_expert(ctypes.byref(cfg), (px.Tensor * 1)(), 0, None, ctypes.byref(h))
+    assert rc == px.PHYAI_EINVAL and not h.value
+    assert b"missing tensor 'patch_w'" in L.phyai_last_error()

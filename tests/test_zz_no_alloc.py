@@ -63,10 +63,11 @@ def test_static_entry_point_full_batch1_workload():
 def test_static_entry_point_rejects_oversized_scratch():
     """A call whose key-split partials exceed the 32 MiB array is refused
     before anything is enqueued: 255 requests of one 128-row attention block
-    each, two key splits, head_dim 256 (about 34 MB of partials)."""
+    each, two key splits over 307 keys (five key tiles, enough to split),
+    head_dim 256 (about 34 MB of partials)."""
     px = _px()
     cfg = small_cfg("pi0", batch=255, n_layers=1, d_model=512, n_q_heads=2, head_dim=256, d_mlp=512,
-                    prefix_cap=128, prefix_min=128, prefix_max=128)
+                    prefix_cap=256, prefix_min=256, prefix_max=256)
     print("[case] static entry point oversized scratch", flush=True)
     case = wl.make_case(cfg, seed=34)
     ex = px.Expert(cfg, case.weights)
