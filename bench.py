@@ -18,7 +18,8 @@ Also measured in the same run and reported in the same JSON line:
   * prefill: the prefix LM that produces the prefix K/V (Gemma-class, 816
     prefix tokens, batch 1): ms per call and its MFMA fraction.
   * vision: the vision tower before it (SigLIP-class ViT, three 256-patch
-    images per request, batch 1): ms per call and its MFMA fraction.
+    images per request, batch 1, and batch 32): ms per call and its MFMA
+    fraction.
   * roofline: the dominant kernel of the batch-1 leg, its algorithmic bytes
     per launch over its average duration, timed with HIP events on the stream
     it runs on.
@@ -539,6 +540,20 @@ def leg_vision(args, px, wl, K, W):
             stages[st] = round(a.elapsed_time(b) * 1e3 / (2 * cfg.n_layers), 2)
             del g
         rec["stage_us"] = stages
+    m.close()
+    del pt, out
+    torch.cuda.empty_cache()
+    # the same tower at batch 32 (96 images), the batch of the paper's phase analysis
+    c32 = wl.CONFIGS["vit_siglip_bf16_b32"]
+    _log(f"timing {c32.name}")
+    m = px.VisionTower(c32, wl.make_weights(c32, args.seed))
+    pt = torch.from_numpy(wl.make_patches(c32, args.seed)).cuda()
+    out = torch.empty((c32.batch, c32.n_images * c32.n_patches, c32.d_out), dtype=torch.float32, device="cuda")
+    wall, per = time_calls(lambda: m.encode(pt, out=out), max(1, K // 2), max(1, W))
+    ms32 = float(np.median(per))
+    tf32 = vision_flops(c32, c32.batch) / (ms32 * 1e-3) / 1e12
+    rec["batch32"] = {"ms_per_call": round(ms32, 3), "images_per_s": round(c32.batch * c32.n_images / (ms32 * 1e-3), 1),
+                      "TFLOPs": round(tf32, 1), "frac_of_bf16_peak": round(tf32 / BF16_PEAK_TFLOPS, 4)}
     m.close()
     del pt, out
     torch.cuda.empty_cache()

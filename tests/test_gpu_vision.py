@@ -235,3 +235,20 @@ def test_siglip_class_tower_full_size():
     assert np.array_equal(got, again)
     ref = oracle.encode_images(cfg, case.weights, case.patches)
     check_tokens("vision siglip full size", cfg, got, ref)
+
+
+def test_siglip_class_tower_batch32_sampled():
+    """The tower at batch 32 (96 images, 24,576 rows: the many-tile GEMM and
+    attention launches): the first and last requests' tokens against the
+    oracle, every token finite."""
+    cfg = wl.CONFIGS["vit_siglip_bf16_b32"]
+    print("[case] vision siglip batch 32", flush=True)
+    w = wl.make_weights(cfg, 0)
+    patches = wl.make_patches(cfg, 0)
+    m = _px().VisionTower(cfg, w)
+    got = run_encode(cfg, wl.VisionCase(cfg, w, patches), model=m)
+    m.close()
+    assert np.isfinite(got).all()
+    for b in (0, cfg.batch - 1):
+        ref = oracle.encode_images(cfg, w, patches[b:b + 1])
+        check_tokens(f"vision siglip batch 32 request {b}", cfg, got[b:b + 1], ref)

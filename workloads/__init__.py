@@ -166,6 +166,13 @@ CONFIGS: Dict[str, ExpertConfig] = {
         action_dim=0, n_steps=0, prefix_cap=768, prefix_min=768, prefix_max=768,
         batch=1, state_token=False, rope=False, weight_dtype="bf16", kv_dtype="bf16", time_dim=0,
         n_images=3, n_patches=256, patch_dim=768, d_out=2048),
+    # the same tower at batch 32, the batch of the paper's phase analysis (96 images)
+    "vit_siglip_bf16_b32": _cfg(
+        name="vit_siglip_bf16_b32", cfg_id=10, variant="vision", n_layers=24, d_model=1024,
+        n_q_heads=16, n_kv_heads=16, head_dim=64, d_mlp=4096, horizon=0,
+        action_dim=0, n_steps=0, prefix_cap=768, prefix_min=768, prefix_max=768,
+        batch=32, state_token=False, rope=False, weight_dtype="bf16", kv_dtype="bf16", time_dim=0,
+        n_images=3, n_patches=256, patch_dim=768, d_out=2048),
     "plm_gemma_bf16_b1": _cfg(
         name="plm_gemma_bf16_b1", cfg_id=8, variant="prefix_lm", n_layers=18, d_model=2048,
         n_q_heads=8, n_kv_heads=1, head_dim=256, d_mlp=16384, horizon=0,
