@@ -20,6 +20,8 @@ Also measured in the same run and reported in the same JSON line:
   * vision: the vision tower before it (SigLIP-class ViT, three 256-patch
     images per request, batch 1, and batch 32): ms per call and its MFMA
     fraction.
+  * pipeline: one pi0 chunk from the observation at batch 1 (tower -> prefix
+    LM -> expert, back to back on one stream): ms per chunk.
   * roofline: the dominant kernel of the batch-1 leg, its algorithmic bytes
     per launch over its average duration, timed with HIP events on the stream
     it runs on.
@@ -560,6 +562,52 @@ def leg_vision(args, px, wl, K, W):
     return rec
 
 
+def leg_pipeline(args, px, wl, K, W):
+    """One pi0 chunk from the observation at batch 1, every phase on the
+    GPU back to back on one stream: the vision tower writes the 768 image
+    tokens into the prefix embeddings (48 text rows after them), the prefix
+    LM turns the 816 rows into the per-layer K/V, and the denoising loop
+    reads that cache.  ms per chunk (the paper's end-to-end figure, with its
+    own vision and language models, is context only)."""
+    import torch
+    vc, pc, ec = (wl.CONFIGS[n] for n in ("vit_siglip_bf16_b1", "plm_gemma_bf16_b1", "pi0_bf16_b1"))
+    _log("generating the pipeline's three models")
+    tower = px.VisionTower(vc, wl.make_weights(vc, args.seed))
+    lm = px.PrefixLM(pc, wl.make_weights(pc, args.seed))
+    ecase = wl.make_case(ec, seed=args.seed)
+    ex = px.Expert(ec, ecase.weights)
+    del ecase.weights
+    pcase_len = wl.make_prefix_lengths(pc, args.seed)
+    emb = torch.from_numpy(wl.make_prefix_embeds(pc, pcase_len, args.seed)).cuda()
+    patches = torch.from_numpy(wl.make_patches(vc, args.seed)).cuda()
+    kv = torch.empty((pc.n_layers, 2, 1, pc.prefix_cap, pc.n_kv_heads * pc.head_dim), dtype=torch.int16,
+                     device="cuda")
+    noise = torch.from_numpy(ecase.noise).cuda()
+    state = torch.from_numpy(ecase.state).cuda()
+    out = torch.empty_like(noise)
+    ex.prepare(1, ec.n_steps)
+
+    def chunk():
+        tower.encode(patches, out=emb)
+        lm.prefill(emb, pcase_len, out=kv)
+        ex.denoise(kv, pcase_len, noise, ecase.timesteps, state, out=out)
+
+    _log("timing the pipeline")
+    wall, per = time_calls(chunk, K, W)
+    assert np.isfinite(out.cpu().numpy()).all()
+    ms = float(np.median(per))
+    rec = {"config": {"workload": "pi0 chunk from the observation, batch 1: SigLIP-class tower over 3 images "
+                                  "-> Gemma-class prefix LM over 816 tokens -> pi0 expert, 10 steps",
+                      "weights": "bf16"},
+           "ms_per_chunk": round(ms, 3), "p99_ms": round(float(np.percentile(per, 99)), 3)}
+    tower.close()
+    lm.close()
+    ex.close()
+    del emb, patches, kv, noise, state, out
+    torch.cuda.empty_cache()
+    return rec
+
+
 def leg_batch64(args, px, wl, K, W):
     import torch
     cfg = wl.CONFIGS["pi0_fp8_b64"]
@@ -621,6 +669,8 @@ def main():
     ap.add_argument("--no-legs", action="store_true", help="skip the pi0.5, DiT and tiny fp32 workloads")
     ap.add_argument("--no-prefill", action="store_true", help="skip the prefix-LM workload")
     ap.add_argument("--no-vision", action="store_true", help="skip the vision-tower workload")
+    ap.add_argument("--no-pipeline", action="store_true",
+                    help="skip the chunk-from-observation pipeline (tower -> prefix LM -> expert)")
     ap.add_argument("--no-stages", action="store_true",
                     help="skip the per-stage graph timings and the rooflines built on them (counter passes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -656,6 +706,8 @@ def main():
         rec["prefill"] = leg_prefill(args, px, wl, max(1, min(K, 20)), min(W, 3))
     if not args.no_vision:
         rec["vision"] = leg_vision(args, px, wl, max(1, min(K, 20)), min(W, 3))
+    if not args.no_pipeline:
+        rec["pipeline"] = leg_pipeline(args, px, wl, max(1, min(K, 20)), min(W, 3))
     if not args.no_batch64:
         rec["batch64"] = leg_batch64(args, px, wl, K, W)
     print(json.dumps(rec), flush=True)

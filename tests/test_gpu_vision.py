@@ -252,3 +252,42 @@ def test_siglip_class_tower_batch32_sampled():
     for b in (0, cfg.batch - 1):
         ref = oracle.encode_images(cfg, w, patches[b:b + 1])
         check_tokens(f"vision siglip batch 32 request {b}", cfg, got[b:b + 1], ref)
+
+
+def test_vision_prefill_denoise_chain():
+    """The whole observation-to-action path at small sizes, every phase on the
+    GPU (tower -> prefix LM -> expert), against the oracle's chain; the
+    actions on their own bar."""
+    px = _px()
+    from gpu_helpers import compare, small_cfg
+    from test_gpu_prefill import plm_cfg
+    ecfg = small_cfg("pi0")
+    vcfg = vit_cfg(n_images=2, n_patches=30, batch=ecfg.batch, d_out=512)
+    n_tok = vcfg.n_images * vcfg.n_patches
+    pcfg = plm_cfg(n_layers=ecfg.n_layers, n_kv_heads=ecfg.n_kv_heads, head_dim=ecfg.head_dim,
+                   prefix_cap=ecfg.prefix_cap, prefix_min=n_tok + 1, prefix_max=ecfg.prefix_cap,
+                   batch=ecfg.batch, d_model=512, n_q_heads=8, d_mlp=1024)
+    print("[case] vision -> prefill -> denoise chain", flush=True)
+    vcase = wl.make_vision_case(vcfg, seed=53)
+    pcase = wl.make_prefill_case(pcfg, seed=53)
+    ecase = wl.make_case(ecfg, seed=53)
+    plen = pcase.prefix_len
+    tower = px.VisionTower(vcfg, vcase.weights)
+    lm = px.PrefixLM(pcfg, pcase.weights, max_batch=ecfg.batch)
+    ex = px.Expert(ecfg, ecase.weights)
+    emb = torch.from_numpy(pcase.embeds).cuda()
+    tower.encode(torch.from_numpy(vcase.patches).cuda(), out=emb)
+    kv = lm.prefill(emb, plen)
+    y = ex.denoise(kv, plen, torch.from_numpy(ecase.noise).cuda(), ecase.timesteps,
+                   torch.from_numpy(ecase.state).cuda())
+    torch.cuda.synchronize()
+    got = y.cpu().numpy().astype(np.float64)
+    ref_emb = pcase.embeds.astype(np.float64).copy()
+    ref_emb[:, :n_tok] = oracle.encode_images(vcfg, vcase.weights, vcase.patches)
+    ref_kv = oracle.prefill(pcfg, pcase.weights, ref_emb, plen)
+    stored = wl.bf16_bits_from_f32(ref_kv.astype(np.float32))
+    ref = oracle.denoise(ecfg, ecase.weights, stored, plen, ecase.noise, ecase.timesteps, ecase.state)
+    compare("vision -> prefill -> denoise", got, ref, ecfg)
+    tower.close()
+    lm.close()
+    ex.close()
