@@ -59,14 +59,14 @@ _GEMM_SRC = ("paper_2608_03682_amd/csrc/gemm.hip", "paper_2608_03682_amd/csrc/ke
              "paper_2608_03682_amd/csrc/common.hpp", "paper_2608_03682_amd/csrc/runtime.hip")
 _MERGE_SRC = _GEMM_SRC + ("paper_2608_03682_amd/csrc/attention.hip",)
 MEASURED_TRAFFIC = {
-    ("pi0_bf16_b1", "attn"): {"bytes": 6240111, "sources": _ATTN_SRC, "sha256": "38e4cce543771614"},
-    ("pi0_bf16_b1", "qkv"): {"bytes": 6537698, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
-    ("pi0_bf16_b1", "oproj"): {"bytes": 9339861, "sources": _MERGE_SRC, "sha256": "ebb1953c3f8ad4a7"},
-    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18220963, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
-    ("pi0_bf16_b1", "mlp_down"): {"bytes": 12472252, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
-    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90362981, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
-    ("pi0_fp8_b64", "qkv"): {"bytes": 107307562, "sources": _GEMM_SRC, "sha256": "2defa5d9da1813eb"},
-    ("pi0_fp8_b64", "attn"): {"bytes": 84646463, "sources": _ATTN_SRC, "sha256": "38e4cce543771614"},
+    ("pi0_bf16_b1", "attn"): {"bytes": 6240129, "sources": _ATTN_SRC, "sha256": "fc85730cbaeea999"},
+    ("pi0_bf16_b1", "qkv"): {"bytes": 6536714, "sources": _GEMM_SRC, "sha256": "4fa368c185b08404"},
+    ("pi0_bf16_b1", "oproj"): {"bytes": 9340935, "sources": _MERGE_SRC, "sha256": "2a06dd1a5a827dc6"},
+    ("pi0_bf16_b1", "mlp_up"): {"bytes": 18212884, "sources": _GEMM_SRC, "sha256": "4fa368c185b08404"},
+    ("pi0_bf16_b1", "mlp_down"): {"bytes": 12464135, "sources": _GEMM_SRC, "sha256": "4fa368c185b08404"},
+    ("pi0_fp8_b64", "mlp_up"): {"bytes": 90550049, "sources": _GEMM_SRC, "sha256": "4fa368c185b08404"},
+    ("pi0_fp8_b64", "qkv"): {"bytes": 107004929, "sources": _GEMM_SRC, "sha256": "4fa368c185b08404"},
+    ("pi0_fp8_b64", "attn"): {"bytes": 84646916, "sources": _ATTN_SRC, "sha256": "fc85730cbaeea999"},
 }
 
 
