@@ -287,6 +287,40 @@ def cpu_baseline_batch(cfg, case, seed, n_req=2):
                       f"oracle, scaled to the batch", "cpu_model": model, "blas": blas}
 
 
+def cpu_baseline_prefill(cfg, case):
+    """The float64 prefix-LM oracle on a bounded sample of the call: one layer's
+    K/V projection alone (the last layer's work) and a full layer plus that
+    projection, over the whole prefix; a call is (L - 1) full layers plus one
+    K/V projection."""
+    import oracle
+    cores, model, blas = _host_info()
+    t0 = time.perf_counter()
+    oracle.prefill(cfg, case.weights, case.embeds, case.prefix_len, n_layers=1)
+    t_kv = time.perf_counter() - t0
+    t0 = time.perf_counter()
+    oracle.prefill(cfg, case.weights, case.embeds, case.prefix_len, n_layers=2)
+    t_full = max(time.perf_counter() - t0 - t_kv, 0.0)
+    call = (cfg.n_layers - 1) * t_full + t_kv
+    return {"value": round(call * 1e3, 1), "unit": "ms/call", "cores": cores, "kind": "oracle",
+            "sample": f"layer 0 in full and one K/V projection over the {int(case.prefix_len.sum())}-token prefix, "
+                      f"float64 NumPy oracle, scaled to {cfg.n_layers - 1} full layers + the last layer's K/V",
+            "cpu_model": model, "blas": blas}
+
+
+def cpu_baseline_vision(cfg, weights, patches):
+    """The float64 vision-tower oracle on one image (all blocks, the projector),
+    scaled to the call's images (images are independent)."""
+    import oracle
+    cores, model, blas = _host_info()
+    t0 = time.perf_counter()
+    oracle.encode_images(cfg, weights, patches[:1, :1])
+    t = time.perf_counter() - t0
+    n = patches.shape[0] * patches.shape[1]
+    return {"value": round(t * n * 1e3, 1), "unit": "ms/call", "cores": cores, "kind": "oracle",
+            "sample": f"1 of the {n} images ({cfg.n_layers} blocks and the projector), float64 NumPy oracle, "
+                      f"scaled to the call", "cpu_model": model, "blas": blas}
+
+
 def measured_roofs():
     """The paper's roof measurement, on this GPU: best of 50 after 10 warm-up
     iterations of a 4 GiB device copy (memory roof) and an 8192^2 bf16 GEMM
@@ -447,7 +481,6 @@ def leg_prefill(args, px, wl, K, W):
     _log(f"generating {cfg.name}")
     case = wl.make_prefill_case(cfg, seed=args.seed)
     m = px.PrefixLM(cfg, case.weights)
-    del case.weights
     emb = torch.from_numpy(case.embeds).cuda()
     out = torch.empty((cfg.n_layers, 2, cfg.batch, cfg.prefix_cap, cfg.n_kv_heads * cfg.head_dim),
                       dtype=torch.int16, device="cuda")
@@ -486,6 +519,10 @@ def leg_prefill(args, px, wl, K, W):
     m.close()
     del emb, out
     torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        _log("timing the prefix-LM oracle")
+        rec["cpu_baseline"] = cpu_baseline_prefill(cfg, case)
+    del case
     return rec
 
 
@@ -508,7 +545,6 @@ def leg_vision(args, px, wl, K, W):
     _log(f"generating {cfg.name}")
     case = wl.make_vision_case(cfg, seed=args.seed)
     m = px.VisionTower(cfg, case.weights)
-    del case.weights
     pt = torch.from_numpy(case.patches).cuda()
     out = torch.empty((cfg.batch, cfg.n_images * cfg.n_patches, cfg.d_out), dtype=torch.float32, device="cuda")
     _log(f"timing {cfg.name}")
@@ -545,6 +581,10 @@ def leg_vision(args, px, wl, K, W):
     m.close()
     del pt, out
     torch.cuda.empty_cache()
+    if not args.no_cpu_baseline:
+        _log("timing the vision oracle")
+        rec["cpu_baseline"] = cpu_baseline_vision(cfg, case.weights, case.patches)
+    del case
     # the same tower at batch 32 (96 images), the batch of the paper's phase analysis
     c32 = wl.CONFIGS["vit_siglip_bf16_b32"]
     _log(f"timing {c32.name}")
@@ -708,6 +748,13 @@ def main():
         rec["vision"] = leg_vision(args, px, wl, max(1, min(K, 20)), min(W, 3))
     if not args.no_pipeline:
         rec["pipeline"] = leg_pipeline(args, px, wl, max(1, min(K, 20)), min(W, 3))
+        parts = [rec.get("cpu_baseline"), rec.get("prefill", {}).get("cpu_baseline"),
+                 rec.get("vision", {}).get("cpu_baseline")]
+        if all(parts):
+            rec["pipeline"]["cpu_baseline"] = {
+                "value": round(sum(p["value"] for p in parts), 1), "unit": "ms/chunk", "cores": parts[0]["cores"],
+                "kind": "oracle", "sample": "the sum of the three phases' oracle timings (expert chunk, prefix-LM "
+                                            "call, vision call) reported with their legs"}
     if not args.no_batch64:
         rec["batch64"] = leg_batch64(args, px, wl, K, W)
     print(json.dumps(rec), flush=True)
