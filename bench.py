@@ -472,6 +472,17 @@ def prefill_flops(cfg, plen):
     return rows * (full * (L - 1) + qkv) + (L - 1) * attn
 
 
+def stage_mfma_roofline(stage_us, flops):
+    """The MFMA roofline of a leg's dominant GEMM or attention stage: its
+    algorithmic FLOPs per launch over its replayed per-launch time."""
+    dom = max((s for s in flops if s in stage_us), key=lambda s: stage_us[s])
+    ach = flops[dom] / (stage_us[dom] * 1e-6) / 1e12
+    return {"bound": "mfma", "achieved": round(ach, 1), "peak": BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+            "frac": round(ach / BF16_PEAK_TFLOPS, 4), "traffic": None, "kernel": dom,
+            "flops_per_launch": int(flops[dom]), "avg_us": stage_us[dom],
+            "timing": "graph replay of the stage over all layers, HIP events on the replay stream"}
+
+
 def leg_prefill(args, px, wl, K, W):
     """The prefix LM (the VLM's language part producing the prefix K/V) on
     the Gemma-class workload over the pi0 prefix (816 tokens, batch 1): ms
@@ -516,6 +527,11 @@ def leg_prefill(args, px, wl, K, W):
             stages[st] = round(a.elapsed_time(b) * 1e3 / (2 * Lf), 2)
             del g
         rec["stage_us"] = stages
+        d, F, D, nq, nkv = cfg.d_model, cfg.d_mlp, cfg.head_dim, cfg.n_q_heads, cfg.n_kv_heads
+        rows = int(np.sum(case.prefix_len))
+        rec["roofline"] = stage_mfma_roofline(stages, {
+            "qkv": 2 * rows * d * (nq + 2 * nkv) * D, "attn": sum(4 * int(p) ** 2 * nq * D for p in case.prefix_len),
+            "oproj": 2 * rows * nq * D * d, "mlp_up": 2 * rows * d * 2 * F, "mlp_down": 2 * rows * F * d})
     m.close()
     del emb, out
     torch.cuda.empty_cache()
@@ -578,6 +594,11 @@ def leg_vision(args, px, wl, K, W):
             stages[st] = round(a.elapsed_time(b) * 1e3 / (2 * cfg.n_layers), 2)
             del g
         rec["stage_us"] = stages
+        d, F, D, H, N = cfg.d_model, cfg.d_mlp, cfg.head_dim, cfg.n_q_heads, cfg.n_patches
+        R = cfg.batch * cfg.n_images * N
+        rec["roofline"] = stage_mfma_roofline(stages, {
+            "qkv": 2 * R * d * 3 * H * D, "attn": cfg.batch * cfg.n_images * 4 * N * N * H * D,
+            "oproj": 2 * R * H * D * d, "mlp_up": 2 * R * d * F, "mlp_down": 2 * R * F * d})
     m.close()
     del pt, out
     torch.cuda.empty_cache()
